@@ -1,0 +1,196 @@
+"""Oracle for the greedy verify + KV realign step (EqSpec, arXiv 2510.22876).
+
+TEST INFRASTRUCTURE ONLY.  A plain, slow, scalar CPU implementation (C in
+``specdec_oracle.c``, compiled with gcc, called through ctypes on numpy
+arrays) that the HIP library is checked against.  It shares no code with the
+library and is never imported by the product path; only ``tests/``, the smoke
+check and the CPU-baseline leg of the benchmark use it.
+
+Each function names the passage of the paper it follows; the C source header
+lists the readings taken where the paper is silent.  Every function here is
+pinned by the ``-m "not gpu"`` tests (brute force, closed forms, the paper's
+corollaries and invariants, an independent replay of each row alone).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from pathlib import Path
+
+import numpy as np
+
+_HERE = Path(__file__).resolve().parent
+_SRC = _HERE / "specdec_oracle.c"
+_LIB_PATH = _HERE / "libspecdec_oracle.so"
+
+F32, BF16, F16 = 0, 1, 2
+DTYPE_CODE = {"f32": F32, "bf16": BF16, "f16": F16}
+
+
+def build(force: bool = True) -> Path:
+    """Compile the oracle with gcc (plain -O2, no vector intrinsics)."""
+    if force or not _LIB_PATH.exists():
+        tmp = _LIB_PATH.with_suffix(".so.tmp")
+        subprocess.run(["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-Wall", "-Wextra",
+                        str(_SRC), "-o", str(tmp), "-lm"], check=True)
+        os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+class Oracle:
+    """ctypes handle on one build of the oracle library (tests load mutant builds too)."""
+
+    def __init__(self, path: Path | str | None = None):
+        if path is None:
+            if not _LIB_PATH.exists():
+                build(force=False)
+            path = _LIB_PATH
+        lib = ctypes.CDLL(str(path))
+        P = ctypes.c_void_p
+        i32, i64 = ctypes.c_int32, ctypes.c_int64
+        lib.oracle_argmax.argtypes = [P, ctypes.c_int, i64]
+        lib.oracle_argmax.restype = i64
+        lib.oracle_verify.argtypes = [P, ctypes.c_int, P, P, i32, i32, i64, i32, P, P, P, P, P]
+        lib.oracle_verify.restype = ctypes.c_int
+        lib.oracle_realign_kv.argtypes = [P, i64, P, i64, i32, i32, i32, i32, i32, i32, P, P, i32]
+        lib.oracle_realign_kv.restype = ctypes.c_int
+        lib.oracle_posmask.argtypes = [P, i32, i32, i32, P, P, i64]
+        lib.oracle_posmask.restype = ctypes.c_int
+        self.lib = lib
+
+
+_default: Oracle | None = None
+
+
+def _load(o: "Oracle | None" = None):
+    global _default
+    if o is not None:
+        return o.lib
+    if _default is None:
+        _default = Oracle()
+    return _default.lib
+
+
+class OracleError(RuntimeError):
+    pass
+
+
+def _ptr(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _c(a, dtype):
+    return np.ascontiguousarray(a, dtype=dtype)
+
+
+def _raw_logits(logits, dtype: str):
+    """Accept numpy arrays (uint16 bit patterns for bf16/f16) or CPU torch tensors."""
+    try:
+        import torch
+        if isinstance(logits, torch.Tensor):
+            t = logits.detach().cpu().contiguous()
+            if t.dtype in (torch.bfloat16, torch.float16):
+                return t.view(torch.int16).numpy().view(np.uint16)
+            return t.numpy()
+    except ImportError:  # pragma: no cover
+        pass
+    a = np.ascontiguousarray(logits)
+    if dtype == "f32":
+        return _c(a, np.float32)
+    if a.dtype == np.float16:
+        return a.view(np.uint16)
+    return _c(a, np.uint16)
+
+
+def argmax(row, dtype: str = "f32", oracle: Oracle | None = None) -> int:
+    """Greedy prediction of one logit row (Algorithm 3, argmax over the vocabulary):
+    lowest index of the maximum, first NaN wins."""
+    r = _raw_logits(row, dtype).reshape(-1)
+    return int(_load(oracle).oracle_argmax(_ptr(r), DTYPE_CODE[dtype], r.size))
+
+
+def verify(logits, dtype: str, draft, pad_in, W_in: int, oracle: Oracle | None = None):
+    """BatchVerify (Algorithm 3) plus the new width and offsets (Eq. 1 and Eq. 2).
+
+    logits [B][k+1][V]; draft [B][k]; pad_in [B].  Returns a dict with
+    tokens [B][k+1], n_acc [B], bonus [B], pad_out [B], w_new (int).
+    """
+    lg = _raw_logits(logits, dtype)
+    B, kp1, V = lg.shape
+    k = kp1 - 1
+    d = _c(np.asarray(draft).reshape(B, k), np.int32)
+    p = _c(np.asarray(pad_in).reshape(B), np.int32)
+    tokens = np.zeros((B, k + 1), np.int32)
+    n_acc = np.zeros(B, np.int32)
+    bonus = np.zeros(B, np.int32)
+    pad_out = np.zeros(B, np.int32)
+    w_new = np.zeros(1, np.int32)
+    rc = _load(oracle).oracle_verify(_ptr(lg), DTYPE_CODE[dtype], _ptr(d), _ptr(p), B, k, V, W_in,
+                               _ptr(tokens), _ptr(n_acc), _ptr(bonus), _ptr(pad_out), _ptr(w_new))
+    if rc:
+        raise OracleError(f"oracle_verify rejected its arguments (code {rc})")
+    return dict(tokens=tokens, n_acc=n_acc, bonus=bonus, pad_out=pad_out, w_new=int(w_new[0]))
+
+
+def _kv_bits(kv):
+    try:
+        import torch
+        if isinstance(kv, torch.Tensor):
+            return kv.detach().cpu().contiguous().view(torch.int16).numpy().view(np.uint16)
+    except ImportError:  # pragma: no cover
+        pass
+    return _c(kv, np.uint16)
+
+
+def realign_kv(src, k: int, W_in: int, pad_in, n_acc, w_new: int, dst=None, dst_cap=None,
+               oracle: Oracle | None = None):
+    """Unpad-append-repad of the KV cache (Section 3.1; Theorem B.1's relocation).
+
+    src: bf16 [n_layers][2][B][H][cap][D] as uint16 bit patterns (or a torch
+    bf16 tensor).  Returns dst (uint16, same layout, ``dst_cap`` columns);
+    columns [0, w_new) are the result.  When ``dst`` is given it is written in
+    place of a fresh array (columns beyond w_new keep their contents).
+    """
+    s = _kv_bits(src)
+    nl, two, B, H, cap, D = s.shape
+    assert two == 2
+    if dst is None:
+        dcap = dst_cap if dst_cap is not None else cap
+        dst = np.zeros((nl, 2, B, H, dcap, D), np.uint16)
+    assert dst.dtype == np.uint16 and dst.flags["C_CONTIGUOUS"]
+    p = _c(np.asarray(pad_in).reshape(B), np.int32)
+    a = _c(np.asarray(n_acc).reshape(B), np.int32)
+    rc = _load(oracle).oracle_realign_kv(_ptr(s), cap, _ptr(dst), dst.shape[4], nl, B, H, D, k, W_in,
+                                   _ptr(p), _ptr(a), int(w_new))
+    if rc:
+        raise OracleError(f"oracle_realign_kv rejected its arguments (code {rc})")
+    return dst
+
+
+def posmask(pad_out, w_new: int, k: int, pm_cap: int | None = None, oracle: Oracle | None = None):
+    """Position ids and attention mask of invariant I2, columns [0, w_new+k+1).
+
+    Returns (pos int64 [B][pm_cap], mask uint8 [B][pm_cap]); columns beyond
+    w_new+k+1 are zero.
+    """
+    p = _c(np.asarray(pad_out).reshape(-1), np.int32)
+    B = p.size
+    cap = pm_cap if pm_cap is not None else w_new + k + 1
+    pos = np.zeros((B, cap), np.int64)
+    mask = np.zeros((B, cap), np.uint8)
+    rc = _load(oracle).oracle_posmask(_ptr(p), int(w_new), B, k, _ptr(pos), _ptr(mask), cap)
+    if rc:
+        raise OracleError(f"oracle_posmask rejected its arguments (code {rc})")
+    return pos, mask
+
+
+def step(logits, dtype: str, draft, pad_in, kv, W_in: int, dst_cap=None,
+         oracle: Oracle | None = None):
+    """One whole step: verify, then realign, then position ids and mask."""
+    v = verify(logits, dtype, draft, pad_in, W_in, oracle=oracle)
+    k = np.asarray(draft).shape[-1]
+    out = realign_kv(kv, k, W_in, pad_in, v["n_acc"], v["w_new"], dst_cap=dst_cap, oracle=oracle)
+    pos, mask = posmask(v["pad_out"], v["w_new"], k, oracle=oracle)
+    v.update(kv=out, pos=pos, mask=mask)
+    return v

@@ -1,0 +1,257 @@
+/*
+ * Oracle for one step of batch speculative decoding under the EqSpec method:
+ * greedy batch verification followed by "unpad-append-repad" realignment of a
+ * left-padded contiguous KV cache.
+ *
+ * TEST INFRASTRUCTURE ONLY.  This file is the plain, slow, scalar CPU
+ * definition that the HIP library is checked against.  It shares no code,
+ * header, table or helper with the library; nothing in the product path may
+ * link or call it.  Only the test suite, the smoke check and the CPU-baseline
+ * leg of the benchmark use it.
+ *
+ * What it follows (arXiv 2510.22876):
+ *   - BatchVerify, Algorithm 3 (Appendix "BatchVerify Algorithm Details"):
+ *     predicted tokens are the argmax over the vocabulary, the first mismatch
+ *     against the drafts gives the accepted prefix, and the bonus token is the
+ *     target's prediction at the first mismatch.
+ *   - Equation (1): the new batch width is the longest updated row,
+ *     L' = max_j (c_j + a_j); Equation (2): per-row padding offset
+ *     delta_i = (L' - L) - a_i; new padding p_i + delta_i.
+ *   - Invariant I1 (rectangular alignment, p_i + c_i = L for every row) and
+ *     invariant I2 (position ids are the running count of content tokens
+ *     minus one, floored at zero; every content column carries the cached
+ *     entry of its own token).
+ *   - Section 3.1, paragraph "Unpad-Append-Repad" and Theorem B.1: realignment
+ *     is a relocation; kept entries are moved unchanged, rejected entries are
+ *     dropped, and the bonus token has no cache entry yet.
+ *
+ * Readings taken where the paper is silent or ambiguous (each is listed in
+ * the design notes of the repository):
+ *   - Cache state model.  Before the step, row i holds c_i = L - p_i cached
+ *     entries in columns [p_i, L) of a width-L region, followed by the k+1
+ *     entries the target just computed for the verify window
+ *     [pending token, d_1 .. d_k] in columns [L, L+k+1).  The window's logit
+ *     rows r = 0..k predict the token after window slot r.  The number of
+ *     entries appended to the cache is a_i = (accepted drafts) + 1: the
+ *     pending token plus each accepted draft; the bonus token becomes the new
+ *     pending token.  In token terms this is the paper's a_i (accepted +
+ *     bonus), so Eq. (1) and Eq. (2) apply unchanged with L counted in cache
+ *     columns.
+ *   - When every draft matches, Algorithm 3's argmax over the all-false
+ *     mismatch vector would return 0; the accepted count is k instead and the
+ *     bonus is the prediction after the last draft.
+ *   - The bonus token is the prediction at window slot n_acc (0-based),
+ *     independent of left padding.
+ *   - Ties in the argmax go to the lowest index; -0.0 equals +0.0; a NaN
+ *     ranks above every number and the first NaN wins.
+ *   - Pad columns of the cache hold bf16 +0.0; position ids of pad columns
+ *     are 0 (the max(0, .) of I2); the mask is 1 on content columns.
+ *   - Position ids and the mask are emitted for columns [0, L'+k+1): the
+ *     realigned cache plus the next verify window.
+ *
+ * Floating point: logits are widened exactly to double and compared there.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+enum { OR_F32 = 0, OR_BF16 = 1, OR_F16 = 2 };
+
+enum {
+  OR_OK = 0,
+  OR_EINVAL = 1,   /* an argument is out of range */
+  OR_ENOMEM = 2,
+};
+
+/* ---- exact widening of one logit to double -------------------------------- */
+
+static double half_bits_to_double(uint16_t h) {
+  int sign = h >> 15;
+  int e = (h >> 10) & 0x1F;
+  int m = h & 0x3FF;
+  double v;
+  if (e == 0) {
+    v = ldexp((double)m, -24);                 /* subnormal: m * 2^-24 */
+  } else if (e == 31) {
+    v = m ? NAN : INFINITY;
+  } else {
+    v = ldexp((double)(m | 0x400), e - 25);    /* (1 + m/1024) * 2^(e-15) */
+  }
+  return sign ? -v : v;
+}
+
+static double logit_at(const void* base, int dtype, int64_t i) {
+  if (dtype == OR_F32) {
+    float f;
+    memcpy(&f, (const char*)base + 4 * i, 4);
+    return (double)f;
+  }
+  uint16_t h;
+  memcpy(&h, (const char*)base + 2 * i, 2);
+  if (dtype == OR_BF16) {
+    uint32_t u = (uint32_t)h << 16;            /* bf16 is the top half of an fp32 */
+    float f;
+    memcpy(&f, &u, 4);
+    return (double)f;
+  }
+  return half_bits_to_double(h);
+}
+
+int oracle_logit_bytes(int dtype) {
+  return dtype == OR_F32 ? 4 : (dtype == OR_BF16 || dtype == OR_F16) ? 2 : 0;
+}
+
+/* Greedy prediction of one logit row (Algorithm 3: argmax over the
+ * vocabulary).  Lowest index among equal maxima; the first NaN wins.
+ * Returns -1 for an empty row or an unknown dtype. */
+int64_t oracle_argmax(const void* row, int dtype, int64_t V) {
+  if (V <= 0 || oracle_logit_bytes(dtype) == 0) return -1;
+  int64_t best = 0;
+  double best_v = logit_at(row, dtype, 0);
+  if (isnan(best_v)) return 0;
+  for (int64_t v = 1; v < V; ++v) {
+    double x = logit_at(row, dtype, v);
+    if (isnan(x)) return v;
+    if (x > best_v) {           /* strict: an equal value later keeps the earlier index */
+      best_v = x;
+      best = v;
+    }
+  }
+  return best;
+}
+
+/* ---- verification and the width / offset rule ---------------------------- */
+
+/*
+ * logits  [B][k+1][V] (dtype), row r of sequence i scores the token after
+ *         verify-window slot r
+ * draft   [B][k]      draft tokens d_1..d_k
+ * pad_in  [B]         p_i, left padding before the step
+ * W_in                width of the cache handed in, including the k+1 window
+ *                     columns; L = W_in - (k+1)
+ * outputs: tokens [B][k+1] (target predictions), n_acc [B] (accepted drafts,
+ *          0..k), bonus [B], pad_out [B] (p_i + delta_i), *w_new (L')
+ */
+int oracle_verify(const void* logits, int dtype, const int32_t* draft, const int32_t* pad_in,
+                  int32_t B, int32_t k, int64_t V, int32_t W_in,
+                  int32_t* tokens, int32_t* n_acc, int32_t* bonus, int32_t* pad_out,
+                  int32_t* w_new) {
+  int eb = oracle_logit_bytes(dtype);
+  if (B < 0 || k < 0 || V <= 0 || eb == 0 || W_in < k + 1) return OR_EINVAL;
+  const int32_t L = W_in - (k + 1);
+  for (int32_t i = 0; i < B; ++i)
+    if (pad_in[i] < 0 || pad_in[i] > L) return OR_EINVAL;
+
+  /* Algorithm 3: pred_tokens <- argmax(logits, dim=vocab) */
+  for (int32_t i = 0; i < B; ++i)
+    for (int32_t r = 0; r <= k; ++r) {
+      const char* row = (const char*)logits + ((int64_t)i * (k + 1) + r) * V * eb;
+      tokens[(int64_t)i * (k + 1) + r] = (int32_t)oracle_argmax(row, dtype, V);
+    }
+
+  /* first mismatch j between pred_tokens and D; A[i] = D[i][:j];
+   * bonus B[i] = prediction at the first mismatch (k when all match) */
+  for (int32_t i = 0; i < B; ++i) {
+    int32_t j = k;
+    for (int32_t r = 0; r < k; ++r)
+      if (draft[(int64_t)i * k + r] != tokens[(int64_t)i * (k + 1) + r]) {
+        j = r;
+        break;
+      }
+    n_acc[i] = j;
+    if (bonus) bonus[i] = tokens[(int64_t)i * (k + 1) + j];
+  }
+
+  /* Eq. (1): L' = max_j (c_j + a_j), with c_j = L - p_j and a_j = n_acc + 1 */
+  int32_t Lp = 0;
+  for (int32_t i = 0; i < B; ++i) {
+    int32_t c = L - pad_in[i];
+    int32_t a = n_acc[i] + 1;
+    if (c + a > Lp) Lp = c + a;
+  }
+  /* Eq. (2): delta_i = (L' - L) - a_i; new padding p_i + delta_i */
+  for (int32_t i = 0; i < B; ++i) {
+    int32_t a = n_acc[i] + 1;
+    int32_t delta = (Lp - L) - a;
+    pad_out[i] = pad_in[i] + delta;
+  }
+  *w_new = Lp;
+  return OR_OK;
+}
+
+/* ---- KV realignment: unpad, append, repad ---------------------------------- */
+
+/*
+ * src  bf16 [n_layers][2][B][H][src_cap][D] (raw 16-bit patterns)
+ * dst  bf16 [n_layers][2][B][H][dst_cap][D]; columns [0, w_new) of every row
+ *      are written, columns beyond are left untouched
+ * pad_in, n_acc [B]; w_new = L' from verification; W_in as in oracle_verify.
+ *
+ * For every (layer, K/V, row, head) span: unpad (take the c_i cached entries
+ * in [p_i, L)), append (the first a_i = n_acc+1 window entries, columns
+ * [L, L+a_i); the rest of the window belongs to rejected drafts and is
+ * dropped), repad (write w_new - (c_i + a_i) zero columns, then the entries).
+ * src and dst must not overlap.
+ */
+int oracle_realign_kv(const uint16_t* src, int64_t src_cap, uint16_t* dst, int64_t dst_cap,
+                      int32_t n_layers, int32_t B, int32_t H, int32_t D, int32_t k,
+                      int32_t W_in, const int32_t* pad_in, const int32_t* n_acc, int32_t w_new) {
+  if (n_layers < 0 || B < 0 || H < 0 || D <= 0 || k < 0 || W_in < k + 1) return OR_EINVAL;
+  if (src_cap < W_in || dst_cap < w_new || w_new < 0) return OR_EINVAL;
+  const int32_t L = W_in - (k + 1);
+  for (int32_t i = 0; i < B; ++i) {
+    if (pad_in[i] < 0 || pad_in[i] > L || n_acc[i] < 0 || n_acc[i] > k) return OR_EINVAL;
+    if ((L - pad_in[i]) + n_acc[i] + 1 > w_new) return OR_EINVAL;
+  }
+  uint16_t* row = (uint16_t*)malloc(sizeof(uint16_t) * (size_t)(W_in > 0 ? W_in : 1) * (size_t)D);
+  if (!row) return OR_ENOMEM;
+  for (int32_t l = 0; l < n_layers; ++l)
+    for (int32_t kv = 0; kv < 2; ++kv)
+      for (int32_t i = 0; i < B; ++i)
+        for (int32_t h = 0; h < H; ++h) {
+          int64_t span = (((int64_t)l * 2 + kv) * B + i) * H + h;
+          const uint16_t* s = src + span * src_cap * D;
+          uint16_t* d = dst + span * dst_cap * D;
+          int32_t c = L - pad_in[i];
+          int32_t a = n_acc[i] + 1;
+          int64_t n = 0;
+          /* unpad: the cached content of the row */
+          for (int32_t j = pad_in[i]; j < L; ++j, ++n)
+            memcpy(row + n * D, s + (int64_t)j * D, sizeof(uint16_t) * D);
+          /* append: entries of the pending token and the accepted drafts */
+          for (int32_t j = L; j < L + a; ++j, ++n)
+            memcpy(row + n * D, s + (int64_t)j * D, sizeof(uint16_t) * D);
+          /* repad to the new width with fresh left padding */
+          int32_t p_new = w_new - (c + a);
+          for (int64_t j = 0; j < p_new; ++j)
+            memset(d + j * D, 0, sizeof(uint16_t) * D);
+          memcpy(d + (int64_t)p_new * D, row, sizeof(uint16_t) * (size_t)n * D);
+        }
+  free(row);
+  return OR_OK;
+}
+
+/* ---- position ids and attention mask (I2) ---------------------------------- */
+
+/*
+ * For columns j in [0, w_new + k + 1): mask[i][j] = 1 on content (j >= pad_out[i]),
+ * pos[i][j] = max(0, (number of content columns q <= j) - 1).
+ * pos, mask are [B][pm_cap].
+ */
+int oracle_posmask(const int32_t* pad_out, int32_t w_new, int32_t B, int32_t k,
+                   int64_t* pos, uint8_t* mask, int64_t pm_cap) {
+  if (B < 0 || k < 0 || w_new < 0 || pm_cap < (int64_t)w_new + k + 1) return OR_EINVAL;
+  const int64_t width = (int64_t)w_new + k + 1;
+  for (int32_t i = 0; i < B; ++i) {
+    if (pad_out[i] < 0 || pad_out[i] > w_new) return OR_EINVAL;
+    int64_t count = 0;
+    for (int64_t j = 0; j < width; ++j) {
+      uint8_t m = (j >= pad_out[i]) ? 1 : 0;
+      mask[(int64_t)i * pm_cap + j] = m;
+      count += m;
+      pos[(int64_t)i * pm_cap + j] = count - 1 > 0 ? count - 1 : 0;
+    }
+  }
+  return OR_OK;
+}

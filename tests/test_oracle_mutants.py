@@ -1,0 +1,81 @@
+"""Each plausible mistake planted in a copy of the oracle's C source must be
+caught by at least one pin (CPU only).
+
+A mutant is built from the oracle source with one text substitution, loaded in
+a child process, and the pins are run against it; the child must fail (an
+assertion, an error code, or a crash all count as caught).  Mistakes modelled
+on the paper's bug taxonomy are included: a bonus token taken from the draft
+(DSD), rejected window entries kept in the cache (BSP), positions that ignore
+the padding, a cache that is not shifted, and Algorithm 3's all-accept case.
+"""
+import os
+import subprocess
+import sys
+import tempfile
+from pathlib import Path
+
+import pytest
+
+ROOT = Path(__file__).resolve().parent.parent
+SRC = ROOT / "oracle" / "specdec_oracle.c"
+
+MUTANTS = {
+    "argmax_ties_to_last": ("if (x > best_v) {", "if (x >= best_v) {"),
+    "argmax_ignores_nan": ("if (isnan(x)) return v;", ""),
+    "bf16_widen_wrong_shift": ("(uint32_t)h << 16", "(uint32_t)h << 15"),
+    # (a slip in the f16 exponent bias or subnormal scale keeps the order of all
+    # values, so no argmax can observe it; these two break the order)
+    "f16_mantissa_bit": ("(m | 0x400)", "(m | 0x200)"),
+    "f16_sign_dropped": ("return sign ? -v : v;", "(void)sign;\n  return v;"),
+    "all_accept_reads_as_zero": ("int32_t j = k;", "int32_t j = 0;"),
+    "bonus_from_draft": ("if (bonus) bonus[i] = tokens[(int64_t)i * (k + 1) + j];",
+                         "if (bonus) bonus[i] = (j < k) ? draft[(int64_t)i * k + j] : tokens[(int64_t)i * (k + 1) + j];"),
+    "width_without_pending_entry": ("int32_t a = n_acc[i] + 1;\n    if (c + a > Lp)",
+                                    "int32_t a = n_acc[i];\n    if (c + a > Lp)"),
+    "offset_sign": ("int32_t delta = (Lp - L) - a;", "int32_t delta = a - (Lp - L);"),
+    "window_start_off_by_one": ("const int32_t L = W_in - (k + 1);\n  for (int32_t i = 0; i < B; ++i)\n    if (pad_in[i] < 0",
+                                "const int32_t L = W_in - k;\n  for (int32_t i = 0; i < B; ++i)\n    if (pad_in[i] < 0"),
+    # rejected window entries kept in place of accepted ones (the last a_i window
+    # columns appended instead of the first a_i)
+    "keeps_rejected_entries": ("for (int32_t j = L; j < L + a; ++j, ++n)",
+                               "for (int32_t j = L + (k + 1 - a); j < L + k + 1; ++j, ++n)"),
+    "unpad_skips_first_entry": ("for (int32_t j = pad_in[i]; j < L; ++j, ++n)", "for (int32_t j = pad_in[i] + (pad_in[i] < L); j < L; ++j, ++n)"),
+    "no_shift": ("memcpy(d + (int64_t)p_new * D, row,", "memcpy(d + (int64_t)(p_new > pad_in[i] ? pad_in[i] : p_new) * D, row,"),
+    "pads_not_cleared": ("memset(d + j * D, 0, sizeof(uint16_t) * D);", "(void)j;"),
+    "mask_off_by_one": ("uint8_t m = (j >= pad_out[i]) ? 1 : 0;", "uint8_t m = (j > pad_out[i]) ? 1 : 0;"),
+    "positions_from_one": ("pos[(int64_t)i * pm_cap + j] = count - 1 > 0 ? count - 1 : 0;",
+                           "pos[(int64_t)i * pm_cap + j] = count;"),
+    "positions_raw_column": ("pos[(int64_t)i * pm_cap + j] = count - 1 > 0 ? count - 1 : 0;",
+                             "pos[(int64_t)i * pm_cap + j] = j;"),
+}
+
+RUNNER = r"""
+import sys
+sys.path.insert(0, {root!r})
+import oracle
+from tests import pins
+o = oracle.Oracle({lib!r})
+failed = []
+for pin in pins.ALL_PINS:
+    try:
+        pin(o)
+    except Exception as e:
+        failed.append(pin.__name__)
+print("FAILED_PINS", failed)
+sys.exit(1 if failed else 0)
+"""
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_mutant_is_caught(name, tmp_path):
+    old, new = MUTANTS[name]
+    src = SRC.read_text()
+    assert src.count(old) == 1, f"mutation anchor for {name} not unique/present"
+    mutated = tmp_path / "mutant.c"
+    mutated.write_text(src.replace(old, new))
+    lib = tmp_path / "libmutant.so"
+    subprocess.run(["gcc", "-O2", "-std=c11", "-fPIC", "-shared", str(mutated), "-o", str(lib), "-lm"],
+                   check=True, capture_output=True)
+    r = subprocess.run([sys.executable, "-c", RUNNER.format(root=str(ROOT), lib=str(lib))],
+                       capture_output=True, text=True, timeout=600, cwd=str(ROOT))
+    assert r.returncode != 0, f"mutant {name} survived every pin:\n{r.stdout[-2000:]}\n{r.stderr[-2000:]}"
