@@ -1,0 +1,293 @@
+#!/usr/bin/env python3
+"""Benchmark of one greedy verify + KV realign step (EqSpec) on one MI355X.
+
+A step is one call of the fused ``specdec_step`` (verify kernel, then the
+realign kernel with the position ids / mask fused in) over one batch of
+synthetic input already resident in HBM.  The default workload is the
+Vicuna-7B-shaped batch (B=8, k=5, V=32000 bf16 logits; KV L=32, H=32, D=128
+bf16; prompts U[128,1024]; out-of-place realign).
+
+Prints ONE JSON line on stdout: steps/s, ms/step, the realign kernel's
+achieved HBM bandwidth against the 8 TB/s peak (timed with HIP events the
+library records on the launch stream), the HBM traffic measured by rocprofv3
+counters when the committed summary matches the current kernel source, and
+the CPU oracle timed on a bounded sample of the same step.
+
+  python bench.py [--steps K] [--warmup W] [--workload NAME] [--variant oop|inplace]
+  python bench.py --copy-calibration GIB   # plain device copy, for counter scaling
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+from pathlib import Path
+
+import numpy as np
+
+ROOT = Path(__file__).resolve().parent
+sys.path.insert(0, str(ROOT))
+
+PEAK_HBM_GBS = 8000.0
+METRIC = "verify+realign steps/s and achieved HBM GB/s (% peak), B=8 7B-shaped KV"
+KERNEL_SRC = ROOT / "paper_2510_22876_amd" / "csrc" / "specdec_kernels.hip"
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_source_hash() -> str:
+    return hashlib.sha256(KERNEL_SRC.read_bytes()).hexdigest()[:16]
+
+
+def describe(w, variant):
+    p = w.prompt
+    pr = f"U[{p[1]},{p[2]}]" if p[0] == "uniform" else (f"log-U[{p[1]},{p[2]}]" if p[0] == "loguniform" else str(p))
+    return (f"{w.name}: B={w.B} k={w.k} V={w.V} {w.logit_dtype} logits; KV L={w.L} H={w.H} D={w.D} bf16; "
+            f"prompts {pr}; accept {w.accept[0]}; {'out-of-place' if variant == 'oop' else 'in-place'} realign")
+
+
+def step_bytes(w, pad_in, W_in, n_acc, w_new, variant):
+    """Algorithmic bytes of one step: what the method must read and write."""
+    C = w.column_bytes
+    W0 = W_in - (w.k + 1)
+    lens = (W0 - pad_in.astype(np.int64)) + n_acc.astype(np.int64) + 1
+    pad_out = w_new - lens
+    shift = pad_out - pad_in
+    if variant == "oop":
+        realign = int(lens.sum()) * C + w.B * w_new * C
+    else:
+        moved = shift != 0
+        realign = int(2 * lens[moved].sum()) * C + int(np.clip(shift, 0, None).sum()) * C
+    posmask = w.B * (w_new + w.k + 1) * (8 + 1)
+    verify = w.B * (w.k + 1) * w.V * w.logit_bytes + 4 * w.B * w.k + 4 * w.B \
+        + 4 * w.B * (w.k + 1) + 3 * 4 * w.B + 4
+    return dict(realign=realign, posmask=posmask, verify=verify)
+
+
+def read_traffic_summary(workload: str, variant: str):
+    """HBM bytes per realign launch from the committed rocprofv3 counter summary,
+    if it was taken on the current kernel source."""
+    path = ROOT / "profiles" / f"realign_{variant}_{workload}_hbm_counters.md"
+    if not path.exists():
+        return None, "no counter summary"
+    text = path.read_text()
+    m_hash = re.search(r"kernel_source_sha256_16:\s*([0-9a-f]+)", text)
+    m_bytes = re.search(r"hbm_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    if not m_hash or not m_bytes:
+        return None, "summary unreadable"
+    if m_hash.group(1) != kernel_source_hash():
+        return None, "kernel changed since the counters were taken"
+    return float(m_bytes.group(1)), path.name
+
+
+def cpu_baseline(w, logits, draft, pad_in, W_in, src, budget_s: float):
+    """The oracle as it stands, single-threaded on the host, on a bounded
+    sample: verification over every logit row, the KV realignment of whole
+    layer slabs (cycling over up to two layers until ``budget_s`` seconds of
+    work), and position ids / mask; scaled to one whole step."""
+    import oracle
+    k = w.k
+    lg = logits.cpu()
+    dr = draft.cpu().numpy()
+    t0 = time.perf_counter()
+    v = oracle.verify(lg, w.logit_dtype, dr, pad_in, W_in)
+    t_verify = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    oracle.posmask(v["pad_out"], v["w_new"], k)
+    t_pm = time.perf_counter() - t0
+    nl = min(w.L, 2)
+    slabs = [src[l:l + 1, :, :, :, :W_in, :].contiguous() for l in range(nl)]
+    import torch
+    host = [s.view(torch.int16).cpu().numpy().view(np.uint16) for s in slabs]
+    runs = 0
+    t_real = 0.0
+    while t_real < budget_s or runs == 0:
+        h = host[runs % nl]
+        t0 = time.perf_counter()
+        oracle.realign_kv(h, k, W_in, pad_in, v["n_acc"], v["w_new"])
+        t_real += time.perf_counter() - t0
+        runs += 1
+    per_layer = t_real / runs
+    est = t_verify + per_layer * w.L + t_pm
+    return dict(value=1.0 / est, unit="steps/s", cores=1, kind="oracle",
+                sample=(f"oracle verify over all {w.B * (w.k + 1)} logit rows ({t_verify * 1e3:.1f} ms), "
+                        f"KV realign of {runs} one-layer slabs cycling over layers 0..{nl - 1} "
+                        f"({per_layer * 1e3:.1f} ms per layer, x{w.L} layers), pos/mask ({t_pm * 1e3:.2f} ms); "
+                        f"single-threaded, scaled to one whole step ({est:.2f} s)"))
+
+
+def copy_calibration(gib: float):
+    import torch
+    n = int(gib * (1 << 30))
+    a = torch.empty(n, dtype=torch.uint8, device="cuda")
+    b = torch.empty(n, dtype=torch.uint8, device="cuda")
+    a.fill_(1)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s.record()
+    reps = 10
+    for _ in range(reps):
+        b.copy_(a)
+    e.record()
+    torch.cuda.synchronize()
+    ms = s.elapsed_time(e) / reps
+    print(json.dumps({"copy_bytes_each_way": n, "ms_per_copy": ms, "GBps_read_plus_write": 2 * n / ms / 1e6}))
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="vicuna7b")
+    ap.add_argument("--variant", default="oop", choices=["oop", "inplace"])
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--cpu-baseline-seconds", type=float, default=10.0,
+                    help="seconds of oracle realign work for the CPU baseline (0: skip)")
+    ap.add_argument("--copy-calibration", type=float, default=0.0,
+                    help="run a plain device copy of this many GiB each way and exit")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py measures one GPU: this step runs on a single MI355X and has no multi-GPU "
+              f"path (asked for --gpus {args.gpus}, WORLD_SIZE={world}).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    if args.copy_calibration > 0:
+        copy_calibration(args.copy_calibration)
+        return
+
+    from paper_2510_22876_amd import specdec as sd
+    from paper_2510_22876_amd import workloads as wl
+
+    w = wl.WORKLOADS[args.workload]
+    variant = args.variant
+    n, W_in, pad_in, cap = wl.initial_geometry(w, args.seed)
+    log(f"[bench] workload {describe(w, variant)}; W_in={W_in} cap={cap}")
+    logits, draft, *_ = wl.logits_and_drafts(w, args.seed, 0, device="cuda")
+    src = wl.make_kv(w, pad_in, W_in, cap, args.seed, device="cuda")
+    pristine = None
+    if variant == "oop":
+        dst = torch.empty_like(src)
+    else:
+        dst = src
+        pristine = src.clone()
+    pm_cap = W_in + w.k + 1
+    bufs = sd.StepBuffers(w.B, w.k, pm_cap)
+    pad_t = torch.as_tensor(pad_in, device="cuda")
+
+    def step():
+        sd.specdec_step(logits, draft, pad_t, W_in, src, dst, bufs.tokens, bufs.n_acc, bufs.bonus, bufs.pad_out,
+                        bufs.w_new, bufs.pos, bufs.mask, bufs.workspace, bufs.dev_status)
+
+    def restore():
+        src.copy_(pristine)
+
+    for _ in range(args.warmup):
+        if pristine is not None:
+            restore()
+        step()
+    torch.cuda.synchronize()
+    n_acc = bufs.n_acc.cpu().numpy()
+    w_new = int(bufs.w_new.cpu()[0])
+    if int(bufs.dev_status.cpu()[0]) != 0:
+        raise RuntimeError("device flagged invalid values")
+
+    K = args.steps
+    sd.timing_reset()
+    sd.timing_enable(True)
+    if pristine is None:
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(K):
+            step()
+        torch.cuda.synchronize()
+        elapsed = time.perf_counter() - t0
+    else:
+        # in place is not idempotent: restore the input before each step,
+        # outside the timed intervals (events bracket each step)
+        elapsed = 0.0
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        for _ in range(K):
+            restore()
+            s.record()
+            step()
+            e.record()
+            torch.cuda.synchronize()
+            elapsed += s.elapsed_time(e) / 1e3
+    sd.timing_enable(False)
+    realign_ms, realign_n = sd.timing_query(sd.KERNEL_REALIGN)
+    verify_ms, verify_n = sd.timing_query(sd.KERNEL_VERIFY)
+    assert realign_n == K and verify_n == K
+
+    by = step_bytes(w, pad_in, W_in, n_acc, w_new, variant)
+    realign_avg_ms = realign_ms / realign_n
+    verify_avg_ms = verify_ms / verify_n
+    realign_bytes = by["realign"] + by["posmask"]
+    achieved = realign_bytes / (realign_avg_ms * 1e-3) / 1e9
+    ms_per_step = elapsed / K * 1e3
+    step_gbs = (realign_bytes + by["verify"]) / (ms_per_step * 1e-3) / 1e9
+    traffic, traffic_src = read_traffic_summary(w.name, variant)
+    log(f"[bench] n_acc={n_acc.tolist()} w_new={w_new} realign {realign_avg_ms:.4f} ms "
+        f"({realign_bytes / 1e9:.3f} GB, {achieved:.0f} GB/s), verify {verify_avg_ms:.4f} ms "
+        f"({by['verify'] / 1e6:.2f} MB), step {ms_per_step:.4f} ms ({step_gbs:.0f} GB/s); traffic: {traffic_src}")
+
+    cpu = None
+    if args.cpu_baseline_seconds > 0:
+        cpu = cpu_baseline(w, logits, draft, pad_in, W_in, pristine if pristine is not None else src,
+                           args.cpu_baseline_seconds)
+        log(f"[bench] cpu baseline: {cpu['value']:.4f} steps/s ({cpu['sample']})")
+
+    line = {
+        "metric": METRIC,
+        "value": K / elapsed,
+        "unit": "steps/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": describe(w, variant),
+            "B": w.B, "k": w.k, "V": w.V, "L": w.L, "H": w.H, "D": w.D, "W_in": W_in, "w_new": w_new,
+            "variant": variant, "seed": args.seed,
+            "step_GBps": round(step_gbs, 1),
+            "step_bytes": realign_bytes + by["verify"],
+            "verify_ms": round(verify_avg_ms, 5),
+            "realign_ms": round(realign_avg_ms, 5),
+        },
+        "roofline": {
+            "bound": "hbm",
+            "kernel": "realign_" + variant + " (+ fused pos/mask)",
+            "achieved": round(achieved, 1),
+            "peak": PEAK_HBM_GBS,
+            "unit": "GB/s",
+            "frac": round(achieved / PEAK_HBM_GBS, 4),
+            "traffic": traffic,
+            "algorithmic_bytes": realign_bytes,
+        },
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

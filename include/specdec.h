@@ -1,0 +1,206 @@
+/*
+ * specdec.h — C ABI of libspecdec.so: one step of greedy batch speculative
+ * decoding under the EqSpec method (arXiv 2510.22876) on AMD MI355X (gfx950).
+ *
+ * One step = greedy batch verification (Algorithm 3, BatchVerify) followed by
+ * unpad-append-repad realignment of a left-padded contiguous KV cache
+ * (Section 3.1, Eq. (1) and Eq. (2); Theorem B.1) and the rebuild of position
+ * ids and the attention mask (invariant I2), so that rectangular alignment
+ * (I1) and position / KV-cache correspondence (I2) hold after the step.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Every pointer argument that names a tensor is a DEVICE pointer (memory
+ *   from hipMalloc or a torch CUDA/HIP tensor) unless it says "host".  The
+ *   caller owns every buffer; the library never allocates, frees or keeps a
+ *   pointer after the call returns.
+ * - `stream` is a hipStream_t passed as void* (NULL = the null stream).  All
+ *   work is enqueued on it and the call returns without waiting, except where
+ *   a host output is requested.
+ * - Return value: a specdec_status_t.  Problems the host can see (NULL
+ *   pointers, sizes out of range, misalignment, overlapping buffers, a short
+ *   workspace) are reported before anything is enqueued; nothing is written
+ *   then.  SPECDEC_ERR_HIP reports a failed HIP call.  specdec_last_error()
+ *   gives the message of the last failure on the calling thread.
+ * - Device-resident values (pad_in, n_acc, w_new, pad_out) cannot be checked
+ *   by the host.  Kernels check them before any memory access they steer; a
+ *   row whose values are out of range is left untouched and a bit is set in
+ *   the optional `dev_status` word (device uint32, may be NULL; bits are
+ *   OR-ed in and never cleared by the library).
+ *
+ * Terms: B rows, k draft tokens per row, V vocabulary entries.  W_in is the
+ * width of the cache handed to the step, counted in cache columns and
+ * including the k+1 columns of the verify window; L = W_in - (k+1) is the
+ * width of the cache before the window.  Row i holds c_i = L - pad_in[i]
+ * cached entries in columns [pad_in[i], L) and the entries of the verify
+ * window [pending token, d_1 .. d_k] in columns [L, W_in).  Logit row r of
+ * sequence i scores the token that follows window slot r.
+ */
+#ifndef SPECDEC_H
+#define SPECDEC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SPECDEC_ABI_VERSION 1
+
+typedef enum {
+  SPECDEC_OK = 0,
+  SPECDEC_ERR_INVALID_ARGUMENT = 1, /* NULL pointer, size out of range, overlap   */
+  SPECDEC_ERR_UNSUPPORTED = 2,      /* dtype, alignment or head size not handled */
+  SPECDEC_ERR_HIP = 3,              /* a HIP runtime call failed                 */
+  SPECDEC_ERR_WORKSPACE = 4         /* workspace missing or too small            */
+} specdec_status_t;
+
+typedef enum { SPECDEC_F32 = 0, SPECDEC_BF16 = 1, SPECDEC_F16 = 2 } specdec_dtype_t;
+
+/* Bits OR-ed into *dev_status by the kernels. */
+#define SPECDEC_DEV_BAD_PAD_IN 0x1u  /* pad_in[i] outside [0, L]                        */
+#define SPECDEC_DEV_BAD_ACCEPT 0x2u  /* n_acc[i] outside [0, k]                         */
+#define SPECDEC_DEV_BAD_WIDTH 0x4u   /* w_new outside [1, W_in] or shorter than a row   */
+#define SPECDEC_DEV_BAD_PAD_OUT 0x8u /* pad_out[i] outside [0, w_new] or pos/mask short */
+
+/* Limits checked by the host. */
+#define SPECDEC_MAX_B 65536
+#define SPECDEC_MAX_K 64
+#define SPECDEC_MAX_ROWS 1048576      /* B*(k+1)                                   */
+#define SPECDEC_MAX_WIDTH 16777216    /* W_in, cap and pm_cap                      */
+#define SPECDEC_MAX_D 4096
+
+/* A bf16 KV cache [L][2][B][H][cap][D], contiguous, D fastest.  One
+ * (layer, K/V, row, head) "span" is cap*D contiguous elements.  `data` is a
+ * device pointer, 16-byte aligned; D must be a multiple of 8 (rows of 16-byte
+ * vectors). */
+typedef struct specdec_kv {
+  void* data;
+  int32_t L, B, H, D;
+  int64_t cap;
+} specdec_kv_t;
+
+/* ABI version of the loaded library (SPECDEC_ABI_VERSION at build time). */
+int32_t specdec_abi_version(void);
+
+/* Message of the last failure on the calling thread ("" if none).  The
+ * string stays valid until the next call on this thread. */
+const char* specdec_last_error(void);
+
+/* Bytes of device workspace specdec_verify_greedy / specdec_step need for a
+ * batch of B rows and k drafts (0 on invalid sizes). */
+size_t specdec_workspace_bytes(int32_t B, int32_t k);
+
+/* Zero a workspace on `stream` (with a kernel, so it can sit inside captured
+ * graphs).  A workspace must be zero before its first use; every successful
+ * verify leaves it zero again.  One workspace serves one in-flight call:
+ * calls that share a workspace must be ordered (same stream). */
+specdec_status_t specdec_workspace_init(void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Greedy batch verification (Algorithm 3) and the new width and paddings
+ * (Eq. (1), Eq. (2)).
+ *
+ *   logits    [B][k+1][V] of `dtype` (SPECDEC_F32 / _BF16 / _F16), contiguous,
+ *             aligned to its element size.
+ *   draft     int32 [B][k]: the draft tokens d_1..d_k of each row.
+ *   pad_in    int32 [B]: left padding of each row, 0 <= pad_in[i] <= L.
+ *   tokens    int32 [B][k+1] out: tokens[i][r] = lowest index of the maximum of
+ *             logits[i][r][:] (-0.0 == +0.0; a NaN ranks above every number,
+ *             the first NaN wins).
+ *   n_acc     int32 [B] out: number of accepted drafts, the first r < k with
+ *             draft[i][r] != tokens[i][r], else k.
+ *   bonus     int32 [B] out (may be NULL): tokens[i][n_acc[i]], the target's
+ *             correction / bonus token (never a draft token).
+ *   pad_out   int32 [B] out: new left padding w_new - (c_i + n_acc[i] + 1);
+ *             -1 for a row whose pad_in is out of range.
+ *   w_new     int32 [1] out: new shared width L' = max_i (c_i + n_acc[i] + 1)
+ *             over rows with a valid pad_in (0 if none).  L' <= W_in.
+ *   workspace device memory of specdec_workspace_bytes(B, k) bytes, zero
+ *             before the call (see specdec_workspace_init), 8-byte aligned.
+ * B = 0 is a no-op.  Limits: 1 <= V < 2^31, 0 <= k <= SPECDEC_MAX_K,
+ * B <= SPECDEC_MAX_B, B*(k+1) <= SPECDEC_MAX_ROWS, k+1 <= W_in <= SPECDEC_MAX_WIDTH.
+ */
+specdec_status_t specdec_verify_greedy(const void* logits, int32_t dtype, const int32_t* draft,
+                                       const int32_t* pad_in, int32_t B, int32_t k, int32_t V,
+                                       int32_t W_in, int32_t* tokens, int32_t* n_acc,
+                                       int32_t* bonus, int32_t* pad_out, int32_t* w_new,
+                                       void* workspace, size_t workspace_bytes,
+                                       uint32_t* dev_status, void* stream);
+
+/*
+ * Unpad-append-repad of the KV cache (Section 3.1; Theorem B.1's relocation).
+ *
+ * For every (layer, K/V, row i, head) span, with c_i = L - pad_in[i],
+ * a_i = n_acc[i] + 1 and p'_i = w_new - (c_i + a_i): destination columns
+ * [0, p'_i) become +0.0 and destination column j in [p'_i, w_new) receives
+ * source column j - (p'_i - pad_in[i]), bit for bit.  Source columns kept are
+ * [pad_in[i], L + a_i); window columns of rejected drafts are dropped.
+ * Destination columns [w_new, cap) are left as they are.
+ *
+ *   src, dst  KV descriptors with equal L, B, H, D; src->cap >= W_in,
+ *             dst->cap >= W_in (w_new <= W_in always holds).
+ *             dst->data == src->data (same cap): in place.  In place requires
+ *             the input's pad columns [0, pad_in[i]) to be +0.0 (they are
+ *             not rewritten); it moves only rows whose padding changes.
+ *             Otherwise the two caches must not overlap.
+ *   pad_in, n_acc  int32 [B] (device); w_new int32 [1] (device): the outputs
+ *             of specdec_verify_greedy for this step.
+ */
+specdec_status_t specdec_realign_kv(const specdec_kv_t* src, const specdec_kv_t* dst, int32_t k,
+                                    int32_t W_in, const int32_t* pad_in, const int32_t* n_acc,
+                                    const int32_t* w_new, uint32_t* dev_status, void* stream);
+
+/*
+ * Position ids and attention mask of invariant I2 for the realigned batch.
+ *
+ * For columns j in [0, w_new + k + 1) (the realigned cache plus the next
+ * verify window): mask[i][j] = (j >= pad_out[i]), pos[i][j] =
+ * max(0, #content columns q <= j - 1) = max(0, j - pad_out[i]).  Columns
+ * [w_new + k + 1, pm_cap) are left as they are.
+ *
+ *   pad_out   int32 [B], w_new int32 [1] (device).
+ *   pos       int64 [B][pm_cap] out, 8-byte aligned; mask uint8 [B][pm_cap] out.
+ *   pm_cap    row stride of pos and mask; must be >= w_new + k + 1 (checked on
+ *             the device; rows that do not fit are skipped and flagged).
+ */
+specdec_status_t specdec_build_posmask(const int32_t* pad_out, const int32_t* w_new, int32_t B,
+                                       int32_t k, int64_t* pos, uint8_t* mask, int64_t pm_cap,
+                                       uint32_t* dev_status, void* stream);
+
+/*
+ * The whole step on one stream: specdec_verify_greedy, then the realignment
+ * and the position ids / mask (one fused launch).  Arguments as above;
+ * pm_cap must be >= W_in + k + 1.  If `w_new_host` (host int32*) is not
+ * NULL, the stream is synchronised and L' is copied there.
+ */
+specdec_status_t specdec_step(const void* logits, int32_t dtype, const int32_t* draft,
+                              const int32_t* pad_in, int32_t B, int32_t k, int32_t V,
+                              int32_t W_in, const specdec_kv_t* src, const specdec_kv_t* dst,
+                              int32_t* tokens, int32_t* n_acc, int32_t* bonus, int32_t* pad_out,
+                              int32_t* w_new, int64_t* pos, uint8_t* mask, int64_t pm_cap,
+                              void* workspace, size_t workspace_bytes, uint32_t* dev_status,
+                              int32_t* w_new_host, void* stream);
+
+/*
+ * Kernel timers (for measurement; off by default).  While enabled, the
+ * library records a pair of HIP events on the launch stream around each of
+ * its kernel launches.  specdec_timing_query waits for the recorded events,
+ * adds their durations to the totals of `kernel`
+ * (0 = verify, 1 = realign (with the fused position ids / mask in
+ * specdec_step), 2 = position ids / mask alone) and returns the totals since
+ * the last reset.
+ */
+#define SPECDEC_KERNEL_VERIFY 0
+#define SPECDEC_KERNEL_REALIGN 1
+#define SPECDEC_KERNEL_POSMASK 2
+specdec_status_t specdec_timing_enable(int32_t on);
+specdec_status_t specdec_timing_reset(void);
+specdec_status_t specdec_timing_query(int32_t kernel, double* total_ms, int64_t* launches);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SPECDEC_H */

@@ -1,0 +1,390 @@
+// C-ABI entry points of libspecdec.so (declared in include/specdec.h):
+// argument validation on the host, then kernel launches on the caller's
+// stream.  Validation never touches the GPU, so every error path below can be
+// exercised without a device.
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "specdec.h"
+#include "specdec_internal.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+specdec_status_t fail(specdec_status_t code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  std::vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return code;
+}
+
+specdec_status_t ok() {
+  g_last_error.clear();
+  return SPECDEC_OK;
+}
+
+specdec_status_t hip_fail(hipError_t e, const char* what) {
+  return fail(SPECDEC_ERR_HIP, "%s: %s (%d)", what, hipGetErrorString(e), static_cast<int>(e));
+}
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+int logit_bytes(int32_t dtype) {
+  switch (dtype) {
+    case SPECDEC_F32: return 4;
+    case SPECDEC_BF16: return 2;
+    case SPECDEC_F16: return 2;
+    default: return 0;
+  }
+}
+
+// ---- kernel timers -------------------------------------------------------------
+
+struct TimedLaunch {
+  int kernel;
+  hipEvent_t begin, end;
+};
+
+struct Timers {
+  std::mutex mu;
+  bool on = false;
+  std::vector<TimedLaunch> pending;
+  std::vector<hipEvent_t> pool;
+  double total_ms[3] = {0, 0, 0};
+  int64_t launches[3] = {0, 0, 0};
+};
+
+Timers& timers() {
+  static Timers t;
+  return t;
+}
+
+hipEvent_t take_event(Timers& t) {
+  if (!t.pool.empty()) {
+    hipEvent_t e = t.pool.back();
+    t.pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+// Runs `launch` on `stream`, bracketed by timer events when timing is on.
+template <typename F>
+hipError_t timed(int kernel, hipStream_t stream, F&& launch) {
+  Timers& t = timers();
+  hipEvent_t b = nullptr, e = nullptr;
+  {
+    std::lock_guard<std::mutex> lk(t.mu);
+    if (t.on) {
+      b = take_event(t);
+      e = take_event(t);
+    }
+  }
+  if (b && e) {
+    hipError_t r = hipEventRecord(b, stream);
+    if (r != hipSuccess) return r;
+  }
+  hipError_t r = launch();
+  if (r != hipSuccess) return r;
+  if (b && e) {
+    r = hipEventRecord(e, stream);
+    if (r != hipSuccess) return r;
+    std::lock_guard<std::mutex> lk(t.mu);
+    t.pending.push_back({kernel, b, e});
+  }
+  return hipSuccess;
+}
+
+// ---- validation -------------------------------------------------------------------
+
+specdec_status_t check_verify_args(const void* logits, int32_t dtype, const int32_t* draft,
+                                   const int32_t* pad_in, int32_t B, int32_t k, int32_t V, int32_t W_in,
+                                   const int32_t* tokens, const int32_t* n_acc, const int32_t* bonus,
+                                   const int32_t* pad_out, const int32_t* w_new, const void* workspace,
+                                   size_t workspace_bytes) {
+  if (B < 0 || B > SPECDEC_MAX_B) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "B=%d outside [0,%d]", B, SPECDEC_MAX_B);
+  if (k < 0 || k > SPECDEC_MAX_K) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "k=%d outside [0,%d]", k, SPECDEC_MAX_K);
+  if (V < 1) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "V=%d must be >= 1", V);
+  if (W_in < k + 1 || W_in > SPECDEC_MAX_WIDTH)
+    return fail(SPECDEC_ERR_INVALID_ARGUMENT, "W_in=%d outside [k+1=%d, %d]", W_in, k + 1, SPECDEC_MAX_WIDTH);
+  const int eb = logit_bytes(dtype);
+  if (eb == 0) return fail(SPECDEC_ERR_UNSUPPORTED, "logit dtype %d not supported", dtype);
+  const int64_t rows = static_cast<int64_t>(B) * (k + 1);
+  if (rows > SPECDEC_MAX_ROWS) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "B*(k+1)=%lld exceeds %d", (long long)rows, SPECDEC_MAX_ROWS);
+  if (B == 0) return SPECDEC_OK;
+  if (!logits || !pad_in || !tokens || !n_acc || !pad_out || !w_new || (k > 0 && !draft))
+    return fail(SPECDEC_ERR_INVALID_ARGUMENT, "NULL tensor pointer (logits, draft, pad_in, tokens, n_acc, pad_out, w_new)");
+  if (!aligned(logits, eb)) return fail(SPECDEC_ERR_UNSUPPORTED, "logits not aligned to %d bytes", eb);
+  const void* i32s[] = {draft, pad_in, tokens, n_acc, bonus, pad_out, w_new};
+  for (const void* p : i32s)
+    if (p && !aligned(p, 4)) return fail(SPECDEC_ERR_UNSUPPORTED, "int32 tensor not 4-byte aligned");
+  const int64_t chunk = specdec::verify_chunk_elems(rows, V);
+  const int64_t blocks = rows * ((V + chunk - 1) / chunk);
+  if (blocks > 0x7FFFFFFFLL) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "logits too large for one launch");
+  const size_t need = specdec_workspace_bytes(B, k);
+  if (!workspace) return fail(SPECDEC_ERR_WORKSPACE, "workspace is NULL (need %zu bytes)", need);
+  if (!aligned(workspace, 8)) return fail(SPECDEC_ERR_WORKSPACE, "workspace not 8-byte aligned");
+  if (workspace_bytes < need)
+    return fail(SPECDEC_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", workspace_bytes, need);
+  return SPECDEC_OK;
+}
+
+specdec_status_t check_kv(const specdec_kv_t* kv, const char* name) {
+  if (!kv) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "%s descriptor is NULL", name);
+  if (kv->L < 0 || kv->B < 0 || kv->H < 0) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "%s has a negative dimension", name);
+  if (kv->D <= 0 || kv->D > SPECDEC_MAX_D) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "%s D=%d outside [1,%d]", name, kv->D, SPECDEC_MAX_D);
+  if (kv->D % 8 != 0) return fail(SPECDEC_ERR_UNSUPPORTED, "%s D=%d: rows of D bf16 must be whole 16-byte vectors", name, kv->D);
+  if (kv->cap < 0 || kv->cap > SPECDEC_MAX_WIDTH) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "%s cap=%lld out of range", name, (long long)kv->cap);
+  const int64_t spans = static_cast<int64_t>(kv->L) * 2 * kv->B * kv->H;
+  if (spans > 0x7FFFFFFFLL) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "%s has too many spans", name);
+  if (spans > 0 && kv->cap > 0) {
+    if (!kv->data) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "%s data is NULL", name);
+    if (!aligned(kv->data, 16)) return fail(SPECDEC_ERR_UNSUPPORTED, "%s data not 16-byte aligned", name);
+  }
+  return SPECDEC_OK;
+}
+
+int64_t kv_bytes(const specdec_kv_t* kv) {
+  return static_cast<int64_t>(kv->L) * 2 * kv->B * kv->H * kv->cap * kv->D * 2;
+}
+
+specdec_status_t check_realign_args(const specdec_kv_t* src, const specdec_kv_t* dst, int32_t k, int32_t W_in,
+                                    const int32_t* pad_in, const int32_t* n_acc, const int32_t* w_new,
+                                    bool* in_place) {
+  specdec_status_t s = check_kv(src, "src");
+  if (s) return s;
+  s = check_kv(dst, "dst");
+  if (s) return s;
+  if (k < 0 || k > SPECDEC_MAX_K) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "k=%d outside [0,%d]", k, SPECDEC_MAX_K);
+  if (W_in < k + 1 || W_in > SPECDEC_MAX_WIDTH)
+    return fail(SPECDEC_ERR_INVALID_ARGUMENT, "W_in=%d outside [k+1=%d, %d]", W_in, k + 1, SPECDEC_MAX_WIDTH);
+  if (src->L != dst->L || src->B != dst->B || src->H != dst->H || src->D != dst->D)
+    return fail(SPECDEC_ERR_INVALID_ARGUMENT, "src and dst shapes differ");
+  const int64_t spans = static_cast<int64_t>(src->L) * 2 * src->B * src->H;
+  *in_place = false;
+  if (spans == 0) return SPECDEC_OK;
+  if (src->cap < W_in) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "src cap=%lld < W_in=%d", (long long)src->cap, W_in);
+  if (dst->cap < W_in) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "dst cap=%lld < W_in=%d", (long long)dst->cap, W_in);
+  if (!pad_in || !n_acc || !w_new) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "NULL pad_in / n_acc / w_new");
+  if (!aligned(pad_in, 4) || !aligned(n_acc, 4) || !aligned(w_new, 4))
+    return fail(SPECDEC_ERR_UNSUPPORTED, "int32 tensor not 4-byte aligned");
+  const uintptr_t s0 = reinterpret_cast<uintptr_t>(src->data), d0 = reinterpret_cast<uintptr_t>(dst->data);
+  const uintptr_t s1 = s0 + static_cast<uintptr_t>(kv_bytes(src)), d1 = d0 + static_cast<uintptr_t>(kv_bytes(dst));
+  if (s0 == d0) {
+    if (src->cap != dst->cap) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "in place needs src cap == dst cap");
+    *in_place = true;
+  } else if (s0 < d1 && d0 < s1) {
+    return fail(SPECDEC_ERR_INVALID_ARGUMENT, "src and dst overlap without being the same cache");
+  }
+  const int64_t blocks = specdec::realign_grid_blocks(spans, W_in, src->D, *in_place);
+  if (blocks > 0x70000000LL) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "cache too large for one launch");
+  return SPECDEC_OK;
+}
+
+specdec_status_t check_posmask_args(const int32_t* pad_out, const int32_t* w_new, int32_t B, int32_t k,
+                                    const int64_t* pos, const uint8_t* mask, int64_t pm_cap) {
+  if (B < 0 || B > SPECDEC_MAX_B) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "B=%d outside [0,%d]", B, SPECDEC_MAX_B);
+  if (k < 0 || k > SPECDEC_MAX_K) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "k=%d outside [0,%d]", k, SPECDEC_MAX_K);
+  if (pm_cap < k + 1 || pm_cap > SPECDEC_MAX_WIDTH + SPECDEC_MAX_K + 1)
+    return fail(SPECDEC_ERR_INVALID_ARGUMENT, "pm_cap=%lld out of range", (long long)pm_cap);
+  if (B == 0) return SPECDEC_OK;
+  if (!pad_out || !w_new || !pos || !mask) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "NULL pad_out / w_new / pos / mask");
+  if (!aligned(pos, 8)) return fail(SPECDEC_ERR_UNSUPPORTED, "pos not 8-byte aligned");
+  if (!aligned(pad_out, 4) || !aligned(w_new, 4)) return fail(SPECDEC_ERR_UNSUPPORTED, "int32 tensor not 4-byte aligned");
+  return SPECDEC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t specdec_abi_version(void) { return SPECDEC_ABI_VERSION; }
+
+const char* specdec_last_error(void) { return g_last_error.c_str(); }
+
+size_t specdec_workspace_bytes(int32_t B, int32_t k) {
+  if (B < 0 || B > SPECDEC_MAX_B || k < 0 || k > SPECDEC_MAX_K) return 0;
+  return specdec::kWsHeaderBytes + static_cast<size_t>(B) * static_cast<size_t>(k + 1) * 8u;
+}
+
+specdec_status_t specdec_workspace_init(void* workspace, size_t workspace_bytes, void* stream) {
+  if (workspace_bytes == 0) return ok();
+  if (!workspace) return fail(SPECDEC_ERR_WORKSPACE, "workspace is NULL");
+  hipError_t e = specdec::launch_zero(workspace, workspace_bytes, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "workspace clear");
+  return ok();
+}
+
+specdec_status_t specdec_verify_greedy(const void* logits, int32_t dtype, const int32_t* draft,
+                                       const int32_t* pad_in, int32_t B, int32_t k, int32_t V, int32_t W_in,
+                                       int32_t* tokens, int32_t* n_acc, int32_t* bonus, int32_t* pad_out,
+                                       int32_t* w_new, void* workspace, size_t workspace_bytes,
+                                       uint32_t* dev_status, void* stream) {
+  specdec_status_t s = check_verify_args(logits, dtype, draft, pad_in, B, k, V, W_in, tokens, n_acc, bonus,
+                                         pad_out, w_new, workspace, workspace_bytes);
+  if (s) return s;
+  if (B == 0) return ok();
+  if (dev_status && !aligned(dev_status, 4)) return fail(SPECDEC_ERR_UNSUPPORTED, "dev_status not 4-byte aligned");
+  specdec::VerifyLaunch p{logits, dtype, draft, pad_in, B, k, V, W_in, tokens, n_acc,
+                          bonus, pad_out, w_new, workspace, dev_status};
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  hipError_t e = timed(SPECDEC_KERNEL_VERIFY, st, [&] { return specdec::launch_verify(p, st); });
+  if (e != hipSuccess) return hip_fail(e, "verify launch");
+  return ok();
+}
+
+specdec_status_t specdec_realign_kv(const specdec_kv_t* src, const specdec_kv_t* dst, int32_t k, int32_t W_in,
+                                    const int32_t* pad_in, const int32_t* n_acc, const int32_t* w_new,
+                                    uint32_t* dev_status, void* stream) {
+  bool in_place = false;
+  specdec_status_t s = check_realign_args(src, dst, k, W_in, pad_in, n_acc, w_new, &in_place);
+  if (s) return s;
+  if (static_cast<int64_t>(src->L) * src->B * src->H == 0) return ok();
+  if (dev_status && !aligned(dev_status, 4)) return fail(SPECDEC_ERR_UNSUPPORTED, "dev_status not 4-byte aligned");
+  specdec::RealignLaunch p{};
+  p.src = src->data;
+  p.dst = dst->data;
+  p.src_cap = src->cap;
+  p.dst_cap = dst->cap;
+  p.L = src->L;
+  p.B = src->B;
+  p.H = src->H;
+  p.D = src->D;
+  p.k = k;
+  p.W_in = W_in;
+  p.pad_in = pad_in;
+  p.n_acc = n_acc;
+  p.w_new = w_new;
+  p.dev_status = dev_status;
+  p.in_place = in_place;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  hipError_t e = timed(SPECDEC_KERNEL_REALIGN, st, [&] { return specdec::launch_realign(p, st); });
+  if (e != hipSuccess) return hip_fail(e, "realign launch");
+  return ok();
+}
+
+specdec_status_t specdec_build_posmask(const int32_t* pad_out, const int32_t* w_new, int32_t B, int32_t k,
+                                       int64_t* pos, uint8_t* mask, int64_t pm_cap, uint32_t* dev_status,
+                                       void* stream) {
+  specdec_status_t s = check_posmask_args(pad_out, w_new, B, k, pos, mask, pm_cap);
+  if (s) return s;
+  if (B == 0) return ok();
+  if (dev_status && !aligned(dev_status, 4)) return fail(SPECDEC_ERR_UNSUPPORTED, "dev_status not 4-byte aligned");
+  specdec::PosmaskLaunch p{pad_out, w_new, B, k, pos, mask, pm_cap, pm_cap, dev_status};
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  hipError_t e = timed(SPECDEC_KERNEL_POSMASK, st, [&] { return specdec::launch_posmask(p, st); });
+  if (e != hipSuccess) return hip_fail(e, "posmask launch");
+  return ok();
+}
+
+specdec_status_t specdec_step(const void* logits, int32_t dtype, const int32_t* draft, const int32_t* pad_in,
+                              int32_t B, int32_t k, int32_t V, int32_t W_in, const specdec_kv_t* src,
+                              const specdec_kv_t* dst, int32_t* tokens, int32_t* n_acc, int32_t* bonus,
+                              int32_t* pad_out, int32_t* w_new, int64_t* pos, uint8_t* mask, int64_t pm_cap,
+                              void* workspace, size_t workspace_bytes, uint32_t* dev_status, int32_t* w_new_host,
+                              void* stream) {
+  specdec_status_t s = check_verify_args(logits, dtype, draft, pad_in, B, k, V, W_in, tokens, n_acc, bonus,
+                                         pad_out, w_new, workspace, workspace_bytes);
+  if (s) return s;
+  bool in_place = false;
+  s = check_realign_args(src, dst, k, W_in, pad_in, n_acc, w_new, &in_place);
+  if (s) return s;
+  if (src->B != B) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "cache rows B=%d differ from logits rows B=%d", src->B, B);
+  s = check_posmask_args(pad_out, w_new, B, k, pos, mask, pm_cap);
+  if (s) return s;
+  if (B > 0 && pm_cap < static_cast<int64_t>(W_in) + k + 1)
+    return fail(SPECDEC_ERR_INVALID_ARGUMENT, "pm_cap=%lld < W_in+k+1=%d", (long long)pm_cap, W_in + k + 1);
+  if (dev_status && !aligned(dev_status, 4)) return fail(SPECDEC_ERR_UNSUPPORTED, "dev_status not 4-byte aligned");
+  if (B == 0) return ok();
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  specdec::VerifyLaunch vp{logits, dtype, draft, pad_in, B, k, V, W_in, tokens, n_acc,
+                           bonus, pad_out, w_new, workspace, dev_status};
+  hipError_t e = timed(SPECDEC_KERNEL_VERIFY, st, [&] { return specdec::launch_verify(vp, st); });
+  if (e != hipSuccess) return hip_fail(e, "verify launch");
+  specdec::RealignLaunch rp{};
+  rp.src = src->data;
+  rp.dst = dst->data;
+  rp.src_cap = src->cap;
+  rp.dst_cap = dst->cap;
+  rp.L = src->L;
+  rp.B = src->B;
+  rp.H = src->H;
+  rp.D = src->D;
+  rp.k = k;
+  rp.W_in = W_in;
+  rp.pad_in = pad_in;
+  rp.n_acc = n_acc;
+  rp.w_new = w_new;
+  rp.dev_status = dev_status;
+  rp.in_place = in_place;
+  rp.pos = pos;
+  rp.mask = mask;
+  rp.pm_cap = pm_cap;
+  rp.pad_out = pad_out;
+  e = timed(SPECDEC_KERNEL_REALIGN, st, [&] { return specdec::launch_realign(rp, st); });
+  if (e != hipSuccess) return hip_fail(e, "realign launch");
+  if (w_new_host) {
+    e = hipMemcpyAsync(w_new_host, w_new, sizeof(int32_t), hipMemcpyDeviceToHost, st);
+    if (e != hipSuccess) return hip_fail(e, "w_new copy");
+    e = hipStreamSynchronize(st);
+    if (e != hipSuccess) return hip_fail(e, "stream synchronize");
+  }
+  return ok();
+}
+
+specdec_status_t specdec_timing_enable(int32_t on) {
+  Timers& t = timers();
+  std::lock_guard<std::mutex> lk(t.mu);
+  t.on = on != 0;
+  return ok();
+}
+
+specdec_status_t specdec_timing_reset(void) {
+  Timers& t = timers();
+  std::lock_guard<std::mutex> lk(t.mu);
+  for (const TimedLaunch& p : t.pending) {
+    (void)hipEventSynchronize(p.end);
+    t.pool.push_back(p.begin);
+    t.pool.push_back(p.end);
+  }
+  t.pending.clear();
+  for (int i = 0; i < 3; ++i) {
+    t.total_ms[i] = 0;
+    t.launches[i] = 0;
+  }
+  return ok();
+}
+
+specdec_status_t specdec_timing_query(int32_t kernel, double* total_ms, int64_t* launches) {
+  if (kernel < 0 || kernel > 2) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "unknown kernel id %d", kernel);
+  Timers& t = timers();
+  std::lock_guard<std::mutex> lk(t.mu);
+  for (const TimedLaunch& p : t.pending) {
+    hipError_t e = hipEventSynchronize(p.end);
+    if (e != hipSuccess) return hip_fail(e, "timer event synchronize");
+    float ms = 0.f;
+    e = hipEventElapsedTime(&ms, p.begin, p.end);
+    if (e != hipSuccess) return hip_fail(e, "timer elapsed time");
+    t.total_ms[p.kernel] += ms;
+    t.launches[p.kernel] += 1;
+    t.pool.push_back(p.begin);
+    t.pool.push_back(p.end);
+  }
+  t.pending.clear();
+  if (total_ms) *total_ms = t.total_ms[kernel];
+  if (launches) *launches = t.launches[kernel];
+  return ok();
+}
+
+}  // extern "C"

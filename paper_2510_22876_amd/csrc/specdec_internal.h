@@ -1,0 +1,68 @@
+// Internal launch interface between the C-ABI layer (specdec_api.cpp) and the
+// HIP kernels (specdec_kernels.hip).  Not installed; not part of the ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace specdec {
+
+constexpr int kThreads = 256;          // every kernel: 4 wavefronts of 64
+constexpr size_t kWsHeaderBytes = 256; // completion counter, padded to a cache line pair
+
+struct VerifyLaunch {
+  const void* logits;
+  int dtype;                 // 0 f32, 1 bf16, 2 f16
+  const int32_t* draft;
+  const int32_t* pad_in;
+  int32_t B, k, V, W_in;
+  int32_t* tokens;
+  int32_t* n_acc;
+  int32_t* bonus;            // may be null
+  int32_t* pad_out;
+  int32_t* w_new;
+  void* workspace;           // [counter | pad][keys: B*(k+1) uint64]
+  uint32_t* dev_status;      // may be null
+};
+
+struct RealignLaunch {
+  const void* src;
+  void* dst;
+  int64_t src_cap, dst_cap;
+  int32_t L, B, H, D;
+  int32_t k, W_in;
+  const int32_t* pad_in;
+  const int32_t* n_acc;
+  const int32_t* w_new;
+  uint32_t* dev_status;
+  bool in_place;
+  // fused position ids / mask (pos == nullptr: none)
+  int64_t* pos;
+  uint8_t* mask;
+  int64_t pm_cap;
+  const int32_t* pad_out;    // verify's pad_out; used only by the fused pos/mask blocks
+};
+
+struct PosmaskLaunch {
+  const int32_t* pad_out;
+  const int32_t* w_new;
+  int32_t B, k;
+  int64_t* pos;
+  uint8_t* mask;
+  int64_t pm_cap;
+  int64_t col_bound;         // upper bound of w_new + k + 1 known on the host
+  uint32_t* dev_status;
+};
+
+// Verify chunking chosen on the host: elements of one logit row per workgroup.
+int64_t verify_chunk_elems(int64_t rows, int64_t V);
+
+// Workgroups of the realign grid (without the fused position-id blocks).
+int64_t realign_grid_blocks(int64_t nspans, int64_t W_in, int32_t D, bool in_place);
+
+hipError_t launch_verify(const VerifyLaunch& p, hipStream_t stream);
+hipError_t launch_realign(const RealignLaunch& p, hipStream_t stream);
+hipError_t launch_posmask(const PosmaskLaunch& p, hipStream_t stream);
+hipError_t launch_zero(void* ptr, size_t bytes, hipStream_t stream);
+
+}  // namespace specdec

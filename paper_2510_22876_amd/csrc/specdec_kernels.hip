@@ -1,0 +1,599 @@
+// HIP kernels for one greedy verify + KV realign step (EqSpec, arXiv 2510.22876)
+// on MI355X (gfx950, wave64).
+//
+//   verify_kernel      vocab-wide argmax of every logit row (Algorithm 3), split
+//                      over workgroups per row; the last workgroup to finish
+//                      runs the prefix-match scan, the bonus token and the new
+//                      width / paddings (Eq. (1), Eq. (2)).
+//   realign_oop        out-of-place unpad-append-repad of the bf16 KV cache:
+//                      one workgroup per 16 KB chunk of a (layer, K/V, row,
+//                      head) span, 128-bit loads and stores.
+//   realign_inplace    in-place variant: one workgroup walks a whole span in
+//                      the direction of its shift, a barrier between the reads
+//                      and the writes of each chunk.
+//   posmask blocks     position ids / mask of invariant I2, appended to either
+//                      realign grid (or launched alone).
+//
+// Everything here is bandwidth-bound data movement plus integer compares: no
+// matrix cores.
+#include "specdec_internal.h"
+
+namespace specdec {
+namespace {
+
+constexpr uint32_t kBadPadIn = 0x1u, kBadAccept = 0x2u, kBadWidth = 0x4u, kBadPadOut = 0x8u;
+constexpr int kWaves = kThreads / 64;
+constexpr int kPmColsPerBlock = 4 * kThreads;
+
+// ---------------------------------------------------------------------------
+// argmax keys
+//
+// A logit is mapped to an unsigned key whose integer order is the order of
+// the values: -0.0 and +0.0 share a key, every NaN gets the largest key (a NaN
+// ranks above every number).  Within a thread elements are visited in
+// increasing index order and only a strictly larger key replaces the best,
+// so the lowest index wins among equal keys; across threads the pair is
+// packed as (key << 32) | ~index, whose maximum again prefers the lowest
+// index.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ uint32_t key_f32(uint32_t u) {
+  const uint32_t mag = u & 0x7FFFFFFFu;
+  if (mag > 0x7F800000u) return 0xFFFFFFFFu;
+  if (mag == 0u) return 0x80000000u;
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+template <uint32_t kNanMag>  // 0x7F80 for bf16, 0x7C00 for f16
+__device__ __forceinline__ uint32_t key_16(uint32_t h) {
+  const uint32_t mag = h & 0x7FFFu;
+  if (mag > kNanMag) return 0xFFFFu;
+  if (mag == 0u) return 0x8000u;
+  return (h & 0x8000u) ? (~h & 0xFFFFu) : (h | 0x8000u);
+}
+
+struct Best {
+  uint32_t key = 0u;
+  int32_t idx = 0;
+  __device__ __forceinline__ void take(uint32_t k, int32_t i) {
+    if (k > key) {
+      key = k;
+      idx = i;
+    }
+  }
+};
+
+template <int DT>
+struct Logit;
+
+template <>
+struct Logit<0> {  // f32
+  static constexpr int kBytes = 4;
+  __device__ static uint32_t key_at(const char* row, int64_t i) {
+    return key_f32(*reinterpret_cast<const uint32_t*>(row + 4 * i));
+  }
+  __device__ static void take_vec(Best& b, const uint4& q, int32_t e) {
+    b.take(key_f32(q.x), e);
+    b.take(key_f32(q.y), e + 1);
+    b.take(key_f32(q.z), e + 2);
+    b.take(key_f32(q.w), e + 3);
+  }
+};
+
+template <uint32_t kNanMag>
+struct Logit16 {
+  static constexpr int kBytes = 2;
+  __device__ static uint32_t key_at(const char* row, int64_t i) {
+    return key_16<kNanMag>(*reinterpret_cast<const uint16_t*>(row + 2 * i));
+  }
+  __device__ static void take_word(Best& b, uint32_t w, int32_t e) {
+    b.take(key_16<kNanMag>(w & 0xFFFFu), e);
+    b.take(key_16<kNanMag>(w >> 16), e + 1);
+  }
+  __device__ static void take_vec(Best& b, const uint4& q, int32_t e) {
+    take_word(b, q.x, e);
+    take_word(b, q.y, e + 2);
+    take_word(b, q.z, e + 4);
+    take_word(b, q.w, e + 6);
+  }
+};
+template <>
+struct Logit<1> : Logit16<0x7F80u> {};  // bf16
+template <>
+struct Logit<2> : Logit16<0x7C00u> {};  // f16
+
+__device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    const uint64_t o = __shfl_xor(v, off);
+    v = o > v ? o : v;
+  }
+  return v;
+}
+
+__device__ __forceinline__ int32_t wave_max_i32(int32_t v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    const int32_t o = __shfl_xor(v, off);
+    v = o > v ? o : v;
+  }
+  return v;
+}
+
+struct VerifyArgs {
+  const char* logits;
+  const int32_t* draft;
+  const int32_t* pad_in;
+  int32_t B, k, V, W_in;
+  int32_t* tokens;
+  int32_t* n_acc;
+  int32_t* bonus;
+  int32_t* pad_out;
+  int32_t* w_new;
+  uint32_t* counter;
+  unsigned long long* keys;
+  uint32_t* dev_status;
+  int64_t chunk_elems;
+  int32_t chunks;        // workgroups per logit row
+  uint32_t total_blocks;
+};
+
+// Scan logit elements [beg, end) of one row; 16-byte vectors over the aligned
+// interior, single elements for the unaligned head and the tail.
+template <int DT>
+__device__ __forceinline__ void scan_range(const char* row, int64_t beg, int64_t end, Best& b) {
+  using T = Logit<DT>;
+  constexpr int kPerVec = 16 / T::kBytes;
+  constexpr int kUnroll = 4;
+  const int tid = threadIdx.x;
+  const uintptr_t addr = reinterpret_cast<uintptr_t>(row) + static_cast<uintptr_t>(beg) * T::kBytes;
+  int64_t head = static_cast<int64_t>((16u - (addr & 15u)) & 15u) / T::kBytes;
+  if (head > end - beg) head = end - beg;
+  const int64_t a0 = beg + head;
+  const int64_t nvec = (end - a0) / kPerVec;
+  const int64_t a1 = a0 + nvec * kPerVec;
+  if (tid < head) b.take(T::key_at(row, beg + tid), static_cast<int32_t>(beg + tid));
+  const uint4* vp = reinterpret_cast<const uint4*>(row + a0 * T::kBytes);
+  for (int64_t v0 = 0; v0 < nvec; v0 += kThreads * kUnroll) {
+    uint4 q[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const int64_t v = v0 + u * kThreads + tid;
+      q[u] = v < nvec ? vp[v] : make_uint4(0u, 0u, 0u, 0u);
+    }
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const int64_t v = v0 + u * kThreads + tid;
+      if (v < nvec) T::take_vec(b, q[u], static_cast<int32_t>(a0 + v * kPerVec));
+    }
+  }
+  if (tid < end - a1) b.take(T::key_at(row, a1 + tid), static_cast<int32_t>(a1 + tid));
+}
+
+// Prefix-match scan, bonus token and new width, run by the last workgroup.
+__device__ void verify_finalize(const VerifyArgs& a) {
+  __shared__ int32_t wmax[kWaves];
+  const int32_t L = a.W_in - (a.k + 1);
+  const int kp1 = a.k + 1;
+  int32_t local = 0;
+  for (int i = threadIdx.x; i < a.B; i += kThreads) {
+    const int32_t p = a.pad_in[i];
+    const bool ok = p >= 0 && p <= L;
+    int32_t nacc = a.k, bon = -1;
+    bool found = false;
+    for (int r = 0; r < kp1; ++r) {
+      unsigned long long* slot = a.keys + static_cast<int64_t>(i) * kp1 + r;
+      const unsigned long long key = __hip_atomic_load(slot, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(slot, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      const int32_t pred = static_cast<int32_t>(~static_cast<uint32_t>(key & 0xFFFFFFFFull));
+      a.tokens[static_cast<int64_t>(i) * kp1 + r] = pred;
+      if (!found && (r == a.k || a.draft[static_cast<int64_t>(i) * a.k + r] != pred)) {
+        nacc = r;
+        bon = pred;
+        found = true;
+      }
+    }
+    a.n_acc[i] = nacc;
+    if (a.bonus) a.bonus[i] = bon;
+    if (ok) {
+      const int32_t len = (L - p) + nacc + 1;
+      local = len > local ? len : local;
+    } else if (a.dev_status) {
+      atomicOr(a.dev_status, kBadPadIn);
+    }
+  }
+  local = wave_max_i32(local);
+  if ((threadIdx.x & 63) == 0) wmax[threadIdx.x >> 6] = local;
+  __syncthreads();
+  int32_t w = wmax[0];
+#pragma unroll
+  for (int q = 1; q < kWaves; ++q) w = wmax[q] > w ? wmax[q] : w;
+  for (int i = threadIdx.x; i < a.B; i += kThreads) {
+    const int32_t p = a.pad_in[i];
+    const bool ok = p >= 0 && p <= L;
+    a.pad_out[i] = ok ? w - ((L - p) + a.n_acc[i] + 1) : -1;
+  }
+  if (threadIdx.x == 0) {
+    a.w_new[0] = w;
+    __hip_atomic_store(a.counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
+template <int DT>
+__global__ __launch_bounds__(kThreads) void verify_kernel(VerifyArgs a) {
+  __shared__ unsigned long long wkey[kWaves];
+  __shared__ int is_last;
+  const int64_t row = blockIdx.x / a.chunks;
+  const int64_t chunk = blockIdx.x - row * a.chunks;
+  const int64_t beg = chunk * a.chunk_elems;
+  int64_t end = beg + a.chunk_elems;
+  if (end > a.V) end = a.V;
+  const char* rowp = a.logits + row * static_cast<int64_t>(a.V) * Logit<DT>::kBytes;
+
+  Best b;
+  scan_range<DT>(rowp, beg, end, b);
+  unsigned long long key =
+      (static_cast<unsigned long long>(b.key) << 32) | static_cast<uint32_t>(~static_cast<uint32_t>(b.idx));
+  key = wave_max_u64(key);
+  if ((threadIdx.x & 63) == 0) wkey[threadIdx.x >> 6] = key;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    unsigned long long k2 = wkey[0];
+#pragma unroll
+    for (int q = 1; q < kWaves; ++q) k2 = wkey[q] > k2 ? wkey[q] : k2;
+    atomicMax(a.keys + row, k2);
+    __threadfence();
+    const uint32_t prev = atomicAdd(a.counter, 1u);
+    is_last = (prev == a.total_blocks - 1u);
+  }
+  __syncthreads();
+  if (!is_last) return;
+  __threadfence();
+  verify_finalize(a);
+}
+
+// ---------------------------------------------------------------------------
+// realign
+// ---------------------------------------------------------------------------
+struct RealignArgs {
+  const uint4* src;
+  uint4* dst;
+  int64_t src_span_vecs, dst_span_vecs;  // cap * D / 8
+  int32_t vpc;                           // 16-byte vectors per column: D / 8
+  int32_t B, H, k, W_in;
+  const int32_t* pad_in;
+  const int32_t* n_acc;
+  const int32_t* w_new;
+  uint32_t* dev_status;
+  int64_t chunks;                        // workgroups per span (out of place)
+  int64_t realign_blocks;
+  // position ids / mask blocks after the realign blocks
+  int64_t* pos;
+  uint8_t* mask;
+  const int32_t* pad_out;
+  int64_t pm_cap;
+  int64_t pm_col_blocks;
+};
+
+struct RowGeom {
+  int32_t pad_in, pad_out, len, w;
+};
+
+__device__ __forceinline__ uint32_t row_geometry(const RealignArgs& a, int row, RowGeom& g) {
+  const int32_t L = a.W_in - (a.k + 1);
+  const int32_t w = a.w_new[0];
+  const int32_t p = a.pad_in[row];
+  const int32_t n = a.n_acc[row];
+  uint32_t err = 0u;
+  if (p < 0 || p > L) err |= kBadPadIn;
+  if (n < 0 || n > a.k) err |= kBadAccept;
+  if (err) return err;
+  const int32_t len = (L - p) + n + 1;
+  if (w < 1 || w > a.W_in || len > w) return kBadWidth;
+  g.pad_in = p;
+  g.pad_out = w - len;
+  g.len = len;
+  g.w = w;
+  return 0u;
+}
+
+__device__ void posmask_block(int64_t blk, int64_t* pos, uint8_t* mask,
+                              const int32_t* pad_out, const int32_t* w_new, int32_t k, int64_t pm_cap,
+                              int64_t col_blocks, uint32_t* dev_status) {
+  const int64_t row = blk / col_blocks;
+  const int64_t cb = blk - row * col_blocks;
+  const int32_t w = w_new[0];
+  const int32_t po = pad_out[row];
+  const int64_t width = static_cast<int64_t>(w) + k + 1;
+  if (w < 0 || po < 0 || po > w || width > pm_cap) {
+    if (cb == 0 && threadIdx.x == 0 && dev_status) atomicOr(dev_status, kBadPadOut);
+    return;
+  }
+  int64_t* prow = pos + row * pm_cap;
+  uint8_t* mrow = mask + row * pm_cap;
+#pragma unroll
+  for (int q = 0; q < kPmColsPerBlock / kThreads; ++q) {
+    const int64_t j = cb * kPmColsPerBlock + q * kThreads + threadIdx.x;
+    if (j < width) {
+      const bool content = j >= po;
+      prow[j] = content ? j - po : 0;
+      mrow[j] = content ? 1 : 0;
+    }
+  }
+}
+
+// Register values of the current thread are live; forces the compiler to
+// wait for the loads that produce them before this point.
+__device__ __forceinline__ void hold(const uint4& v) {
+  asm volatile("" ::"v"(v.x), "v"(v.y), "v"(v.z), "v"(v.w));
+}
+
+template <int kUnroll>
+__global__ __launch_bounds__(kThreads) void realign_oop_kernel(RealignArgs a) {
+  const int64_t b = blockIdx.x;
+  if (b >= a.realign_blocks) {
+    posmask_block(b - a.realign_blocks, a.pos, a.mask, a.pad_out, a.w_new, a.k, a.pm_cap, a.pm_col_blocks,
+                  a.dev_status);
+    return;
+  }
+  const int64_t span = b / a.chunks;
+  const int64_t chunk = b - span * a.chunks;
+  const int row = static_cast<int>((span / a.H) % a.B);
+  RowGeom g;
+  const uint32_t err = row_geometry(a, row, g);
+  if (err) {
+    if (chunk == 0 && span == static_cast<int64_t>(row) * a.H && threadIdx.x == 0 && a.dev_status)
+      atomicOr(a.dev_status, err);
+    return;
+  }
+  constexpr int64_t kChunk = static_cast<int64_t>(kThreads) * kUnroll;
+  const int64_t vpc = a.vpc;
+  const int64_t total = static_cast<int64_t>(g.w) * vpc;       // output vectors of the span
+  const int64_t c0 = chunk * kChunk;
+  if (c0 >= total) return;
+  const int64_t zero_end = static_cast<int64_t>(g.pad_out) * vpc;
+  const int64_t shift = static_cast<int64_t>(g.pad_out - g.pad_in) * vpc;
+  const uint4* s = a.src + span * a.src_span_vecs;
+  uint4* d = a.dst + span * a.dst_span_vecs;
+  const int t = threadIdx.x;
+  uint4 v[kUnroll];
+  if (c0 >= zero_end && c0 + kChunk <= total) {
+    // the whole chunk is copied content
+#pragma unroll
+    for (int j = 0; j < kUnroll; ++j) v[j] = s[c0 - shift + j * kThreads + t];
+#pragma unroll
+    for (int j = 0; j < kUnroll; ++j) d[c0 + j * kThreads + t] = v[j];
+  } else if (c0 + kChunk <= zero_end) {
+    // the whole chunk is new padding
+#pragma unroll
+    for (int j = 0; j < kUnroll; ++j) d[c0 + j * kThreads + t] = make_uint4(0u, 0u, 0u, 0u);
+  } else {
+    // padding / content boundary or the ragged end of the span; source
+    // indices are clamped into the kept range so every load is in bounds
+    const int64_t lo = zero_end - shift, hi = total - 1 - shift;
+#pragma unroll
+    for (int j = 0; j < kUnroll; ++j) {
+      int64_t si = c0 + j * kThreads + t - shift;
+      si = si < lo ? lo : (si > hi ? hi : si);
+      v[j] = s[si];
+    }
+#pragma unroll
+    for (int j = 0; j < kUnroll; ++j) {
+      const int64_t u = c0 + j * kThreads + t;
+      if (u < total) d[u] = u >= zero_end ? v[j] : make_uint4(0u, 0u, 0u, 0u);
+    }
+  }
+}
+
+// Moves vectors [lo, lo + kChunk) (clipped to [0, n)) of one row's kept
+// entries from `from + u` to `to + u` within the same span.  All reads of the
+// chunk complete before any write to it.
+template <int kUnroll>
+__device__ __forceinline__ void move_chunk(uint4* base, int64_t from, int64_t to, int64_t lo, int64_t n) {
+  constexpr int64_t kChunk = static_cast<int64_t>(kThreads) * kUnroll;
+  const int t = threadIdx.x;
+  uint4 v[kUnroll];
+  if (lo >= 0 && lo + kChunk <= n) {
+#pragma unroll
+    for (int j = 0; j < kUnroll; ++j) v[j] = base[from + lo + j * kThreads + t];
+#pragma unroll
+    for (int j = 0; j < kUnroll; ++j) hold(v[j]);
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < kUnroll; ++j) base[to + lo + j * kThreads + t] = v[j];
+  } else {
+#pragma unroll
+    for (int j = 0; j < kUnroll; ++j) {
+      int64_t u = lo + j * kThreads + t;
+      u = u < 0 ? 0 : (u >= n ? n - 1 : u);
+      v[j] = base[from + u];
+    }
+#pragma unroll
+    for (int j = 0; j < kUnroll; ++j) hold(v[j]);
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < kUnroll; ++j) {
+      const int64_t u = lo + j * kThreads + t;
+      if (u >= 0 && u < n) base[to + u] = v[j];
+    }
+  }
+}
+
+template <int kUnroll>
+__global__ __launch_bounds__(kThreads) void realign_inplace_kernel(RealignArgs a) {
+  const int64_t b = blockIdx.x;
+  if (b >= a.realign_blocks) {
+    posmask_block(b - a.realign_blocks, a.pos, a.mask, a.pad_out, a.w_new, a.k, a.pm_cap, a.pm_col_blocks,
+                  a.dev_status);
+    return;
+  }
+  const int64_t span = b;
+  const int row = static_cast<int>((span / a.H) % a.B);
+  RowGeom g;
+  const uint32_t err = row_geometry(a, row, g);
+  if (err) {
+    if (span == static_cast<int64_t>(row) * a.H && threadIdx.x == 0 && a.dev_status)
+      atomicOr(a.dev_status, err);
+    return;
+  }
+  const int32_t s = g.pad_out - g.pad_in;
+  if (s == 0) return;  // no shift: the row is already in place (uniform acceptance)
+  const int64_t vpc = a.vpc;
+  uint4* base = a.dst + span * a.dst_span_vecs;
+  const int64_t n = static_cast<int64_t>(g.len) * vpc;
+  const int64_t from = static_cast<int64_t>(g.pad_in) * vpc;
+  const int64_t to = static_cast<int64_t>(g.pad_out) * vpc;
+  constexpr int64_t kChunk = static_cast<int64_t>(kThreads) * kUnroll;
+  if (s > 0) {
+    // moving towards higher addresses: walk from the top, so a chunk's
+    // destination never covers source vectors that are still to be read
+    for (int64_t hi = n; hi > 0; hi -= kChunk) move_chunk<kUnroll>(base, from, to, hi - kChunk, n);
+    // the vacated columns [pad_in, pad_out) become padding; every read of
+    // them completed before the last barrier
+    for (int64_t u = threadIdx.x; u < to - from; u += kThreads) base[from + u] = make_uint4(0u, 0u, 0u, 0u);
+  } else {
+    // moving towards lower addresses: walk from the bottom; columns
+    // [0, pad_out) already hold padding (+0.0)
+    for (int64_t lo = 0; lo < n; lo += kChunk) move_chunk<kUnroll>(base, from, to, lo, n);
+  }
+}
+
+__global__ __launch_bounds__(kThreads) void posmask_kernel(int64_t* pos, uint8_t* mask,
+                                                           const int32_t* pad_out, const int32_t* w_new,
+                                                           int32_t k, int64_t pm_cap, int64_t col_blocks,
+                                                           uint32_t* dev_status) {
+  posmask_block(blockIdx.x, pos, mask, pad_out, w_new, k, pm_cap, col_blocks, dev_status);
+}
+
+__global__ __launch_bounds__(kThreads) void zero_kernel(uint4* p16, int64_t n16, uint8_t* tail, int64_t ntail) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x;
+  if (i < n16) p16[i] = make_uint4(0u, 0u, 0u, 0u);
+  if (i < ntail) tail[i] = 0;
+}
+
+constexpr int kOopUnroll = 4;      // 16 KB of a span per workgroup
+constexpr int kInplaceUnroll = 8;  // 32 KB per chunk of the in-place walk
+
+}  // namespace
+
+int64_t verify_chunk_elems(int64_t rows, int64_t V) {
+  // about 2048 workgroups in total, each scanning 2048..16384 elements
+  const int64_t per = (rows * V + 2047) / 2048;
+  int64_t c = ((per + 2047) / 2048) * 2048;
+  if (c < 2048) c = 2048;
+  if (c > 16384) c = 16384;
+  if (c > V) c = V;
+  return c;
+}
+
+hipError_t launch_verify(const VerifyLaunch& p, hipStream_t stream) {
+  VerifyArgs a;
+  a.logits = static_cast<const char*>(p.logits);
+  a.draft = p.draft;
+  a.pad_in = p.pad_in;
+  a.B = p.B;
+  a.k = p.k;
+  a.V = p.V;
+  a.W_in = p.W_in;
+  a.tokens = p.tokens;
+  a.n_acc = p.n_acc;
+  a.bonus = p.bonus;
+  a.pad_out = p.pad_out;
+  a.w_new = p.w_new;
+  a.counter = static_cast<uint32_t*>(p.workspace);
+  a.keys = reinterpret_cast<unsigned long long*>(static_cast<char*>(p.workspace) + kWsHeaderBytes);
+  a.dev_status = p.dev_status;
+  const int64_t rows = static_cast<int64_t>(p.B) * (p.k + 1);
+  a.chunk_elems = verify_chunk_elems(rows, p.V);
+  a.chunks = static_cast<int32_t>((p.V + a.chunk_elems - 1) / a.chunk_elems);
+  const int64_t blocks = rows * a.chunks;
+  a.total_blocks = static_cast<uint32_t>(blocks);
+  const dim3 grid(static_cast<uint32_t>(blocks)), block(kThreads);
+  switch (p.dtype) {
+    case 0: hipLaunchKernelGGL(verify_kernel<0>, grid, block, 0, stream, a); break;
+    case 1: hipLaunchKernelGGL(verify_kernel<1>, grid, block, 0, stream, a); break;
+    default: hipLaunchKernelGGL(verify_kernel<2>, grid, block, 0, stream, a); break;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_realign(const RealignLaunch& p, hipStream_t stream) {
+  RealignArgs a;
+  a.src = static_cast<const uint4*>(p.src);
+  a.dst = static_cast<uint4*>(p.dst);
+  a.vpc = p.D / 8;
+  a.src_span_vecs = p.src_cap * a.vpc;
+  a.dst_span_vecs = p.dst_cap * a.vpc;
+  a.B = p.B;
+  a.H = p.H;
+  a.k = p.k;
+  a.W_in = p.W_in;
+  a.pad_in = p.pad_in;
+  a.n_acc = p.n_acc;
+  a.w_new = p.w_new;
+  a.dev_status = p.dev_status;
+  const int64_t nspans = static_cast<int64_t>(p.L) * 2 * p.B * p.H;
+  a.pos = p.pos;
+  a.mask = p.mask;
+  a.pad_out = p.pad_out;
+  a.pm_cap = p.pm_cap;
+  int64_t pm_blocks = 0;
+  if (p.pos) {
+    const int64_t bound = static_cast<int64_t>(p.W_in) + p.k + 1;
+    a.pm_col_blocks = (bound + kPmColsPerBlock - 1) / kPmColsPerBlock;
+    pm_blocks = a.pm_col_blocks * p.B;
+  } else {
+    a.pm_col_blocks = 1;
+  }
+  if (p.in_place) {
+    a.chunks = 1;
+    a.realign_blocks = nspans;
+    const dim3 grid(static_cast<uint32_t>(nspans + pm_blocks)), block(kThreads);
+    if (nspans + pm_blocks == 0) return hipSuccess;
+    hipLaunchKernelGGL(realign_inplace_kernel<kInplaceUnroll>, grid, block, 0, stream, a);
+  } else {
+    const int64_t per_block = static_cast<int64_t>(kThreads) * kOopUnroll;
+    a.chunks = (static_cast<int64_t>(p.W_in) * a.vpc + per_block - 1) / per_block;
+    a.realign_blocks = nspans * a.chunks;
+    const int64_t blocks = a.realign_blocks + pm_blocks;
+    if (blocks == 0) return hipSuccess;
+    const dim3 grid(static_cast<uint32_t>(blocks)), block(kThreads);
+    hipLaunchKernelGGL(realign_oop_kernel<kOopUnroll>, grid, block, 0, stream, a);
+  }
+  return hipGetLastError();
+}
+
+int64_t realign_grid_blocks(int64_t nspans, int64_t W_in, int32_t D, bool in_place) {
+  if (in_place) return nspans;
+  const int64_t per_block = static_cast<int64_t>(kThreads) * kOopUnroll;
+  return nspans * ((W_in * (D / 8) + per_block - 1) / per_block);
+}
+
+hipError_t launch_posmask(const PosmaskLaunch& p, hipStream_t stream) {
+  const int64_t col_blocks = (p.col_bound + kPmColsPerBlock - 1) / kPmColsPerBlock;
+  const int64_t blocks = col_blocks * p.B;
+  if (blocks == 0) return hipSuccess;
+  hipLaunchKernelGGL(posmask_kernel, dim3(static_cast<uint32_t>(blocks)), dim3(kThreads), 0, stream, p.pos,
+                     p.mask, p.pad_out, p.w_new, p.k, p.pm_cap, col_blocks, p.dev_status);
+  return hipGetLastError();
+}
+
+hipError_t launch_zero(void* ptr, size_t bytes, hipStream_t stream) {
+  const uintptr_t base = reinterpret_cast<uintptr_t>(ptr);
+  // 16-byte stores over the aligned body, byte stores for the rest (the
+  // workspace is 8-byte aligned; the rare unaligned prefix is byte-cleared)
+  if ((base & 15u) != 0u || bytes < 16) {
+    const int64_t n = static_cast<int64_t>(bytes);
+    if (n == 0) return hipSuccess;
+    hipLaunchKernelGGL(zero_kernel, dim3(static_cast<uint32_t>((n + kThreads - 1) / kThreads)), dim3(kThreads), 0,
+                       stream, static_cast<uint4*>(nullptr), int64_t{0}, static_cast<uint8_t*>(ptr), n);
+    return hipGetLastError();
+  }
+  const int64_t n16 = static_cast<int64_t>(bytes / 16);
+  const int64_t ntail = static_cast<int64_t>(bytes % 16);
+  const int64_t n = n16 > ntail ? n16 : ntail;
+  hipLaunchKernelGGL(zero_kernel, dim3(static_cast<uint32_t>((n + kThreads - 1) / kThreads)), dim3(kThreads), 0,
+                     stream, static_cast<uint4*>(ptr), n16, static_cast<uint8_t*>(ptr) + n16 * 16, ntail);
+  return hipGetLastError();
+}
+
+}  // namespace specdec

@@ -59,19 +59,37 @@ def check_posmask(pos, mask, pad_out, w_new, k):
             raise InvariantError(f"row {i}: content positions are not 0,1,2,...")
 
 
-def expected_tags(l, kv, row, H, D, w_new, pad_out, prod_step):
+def expected_tags(l, kv, row, H, D, w_new, pad_out, prod_step, device="cpu"):
     """bf16 bit patterns [H][w_new][D] that row ``row`` of slab (l, kv) must
     hold: +0.0 on pads, the tag of (producing step, l, kv, row, h, p, d) on
-    content column pad_out + p."""
+    content column pad_out + p.  Returns numpy uint16 on the CPU, an int16
+    tensor on another device."""
     p0 = int(pad_out)
     n = w_new - p0
-    out = torch.zeros((H, w_new, D), dtype=torch.int16)
+    out = torch.zeros((H, w_new, D), dtype=torch.int16, device=device)
     if n > 0:
-        steps = torch.as_tensor(np.asarray(prod_step[:n]), dtype=torch.int64).view(1, n, 1)
-        tags = kv_tag(steps, l, kv, row, torch.arange(H).view(H, 1, 1),
-                      torch.arange(n).view(1, n, 1), torch.arange(D).view(1, 1, D))
+        steps = torch.as_tensor(np.asarray(prod_step[:n]), dtype=torch.int64, device=device).view(1, n, 1)
+        tags = kv_tag(steps, l, kv, row, torch.arange(H, device=device).view(H, 1, 1),
+                      torch.arange(n, device=device).view(1, n, 1), torch.arange(D, device=device).view(1, 1, D),
+                      device=device)
         out[:, p0:, :] = tags
-    return out.numpy().view(np.uint16)
+    if device == "cpu":
+        return out.numpy().view(np.uint16)
+    return out
+
+
+def check_tagged_kv_device(kv: torch.Tensor, pad_out, w_new, prod_steps):
+    """check_tagged_kv for a bf16 cache that stays on its device."""
+    L, _, B, H, cap, D = kv.shape
+    for l in range(L):
+        for k2 in range(2):
+            for i in range(B):
+                exp = expected_tags(l, k2, i, H, D, w_new, pad_out[i], prod_steps[i], device=kv.device)
+                got = kv[l, k2, i, :, :w_new, :].view(torch.int16)
+                if not torch.equal(got, exp):
+                    bad = (got != exp).nonzero()[0].tolist()
+                    raise InvariantError(f"cache clause broken at layer {l} kv {k2} row {i} head/col {bad} "
+                                         f"(pad_out {pad_out[i]})")
 
 
 def check_tagged_kv(kv_bits, pad_out, w_new, prod_steps, layers=None, rows=None):

@@ -1,0 +1,155 @@
+"""The C-ABI library loads, exports every function include/specdec.h declares,
+and rejects bad arguments on the host before anything reaches a GPU.
+
+No compute call is made here.  The error-path cases pass dummy pointer values
+that the library never dereferences, because each case fails validation; they
+are skipped when a GPU is visible, so that a validation regression can never
+send such a pointer to a kernel.
+"""
+import ctypes
+import re
+from pathlib import Path
+
+import pytest
+
+ROOT = Path(__file__).resolve().parent.parent
+HEADER = (ROOT / "include" / "specdec.h").read_text()
+
+
+def _declared_functions():
+    body = re.sub(r"/\*.*?\*/", "", HEADER, flags=re.S)
+    return sorted(set(re.findall(r"\b(specdec_\w+)\s*\(", body)))
+
+
+@pytest.fixture(scope="module")
+def sd():
+    from paper_2510_22876_amd import specdec
+    return specdec
+
+
+def test_library_exports_every_declared_function(sd):
+    declared = _declared_functions()
+    assert "specdec_step" in declared and "specdec_verify_greedy" in declared
+    assert "specdec_realign_kv" in declared and "specdec_build_posmask" in declared
+    for name in declared:
+        assert hasattr(sd.lib, name), f"{name} declared in specdec.h but not exported"
+    assert sorted(sd.EXPORTED) == declared
+
+
+def test_abi_version_matches_header(sd):
+    m = re.search(r"#define SPECDEC_ABI_VERSION (\d+)", HEADER)
+    assert sd.abi_version() == int(m.group(1))
+
+
+def test_workspace_bytes(sd):
+    assert sd.workspace_bytes(8, 5) == 256 + 8 * 6 * 8
+    assert sd.workspace_bytes(0, 0) == 256
+    assert sd.workspace_bytes(-1, 2) == 0
+    assert sd.workspace_bytes(4, 65) == 0
+
+
+def _no_gpu():
+    import torch
+    if torch.cuda.is_available():
+        pytest.skip("error paths with dummy pointers run on CPU-only hosts")
+
+
+# A dummy, well-aligned address; never dereferenced (every case fails validation).
+A = 0x10000
+P = ctypes.c_void_p
+
+
+def _verify(sd, **over):
+    args = dict(logits=A, dtype=1, draft=A, pad_in=A, B=2, k=3, V=100, W_in=10, tokens=A, n_acc=A,
+                bonus=A, pad_out=A, w_new=A, ws=A, ws_bytes=sd.workspace_bytes(2, 3), status=None, stream=None)
+    args.update(over)
+    return sd.lib.specdec_verify_greedy(*args.values())
+
+
+@pytest.mark.parametrize("over,code", [
+    (dict(B=-1), 1), (dict(B=70000), 1), (dict(k=-1), 1), (dict(k=65), 1), (dict(V=0), 1),
+    (dict(W_in=3), 1), (dict(W_in=1 << 25), 1), (dict(dtype=7), 2), (dict(logits=None), 1),
+    (dict(draft=None), 1), (dict(pad_in=None), 1), (dict(tokens=None), 1), (dict(n_acc=None), 1),
+    (dict(pad_out=None), 1), (dict(w_new=None), 1), (dict(logits=A + 1), 2), (dict(dtype=0, logits=A + 2), 2),
+    (dict(tokens=A + 2), 2), (dict(ws=None), 4), (dict(ws=A + 4), 4), (dict(ws_bytes=16), 4),
+    (dict(B=65536, k=63), 1),
+])
+def test_verify_rejects(sd, over, code):
+    _no_gpu()
+    assert _verify(sd, **over) == code
+    assert sd.lib.specdec_last_error().decode() != ""
+
+
+def test_verify_empty_batch_is_a_noop(sd):
+    _no_gpu()
+    assert _verify(sd, B=0, logits=None, draft=None, pad_in=None, tokens=None, n_acc=None, pad_out=None,
+                   w_new=None, ws=None) == 0
+
+
+def _kv(sd, data=A, L=2, B=2, H=2, D=16, cap=64):
+    return sd.KV(data, L, B, H, D, cap)
+
+
+def _realign(sd, src=None, dst=None, k=3, W_in=10, pad_in=A, n_acc=A, w_new=A):
+    src = src if src is not None else _kv(sd)
+    dst = dst if dst is not None else _kv(sd, data=A + (1 << 30))
+    return sd.lib.specdec_realign_kv(ctypes.byref(src), ctypes.byref(dst), k, W_in, pad_in, n_acc, w_new,
+                                     None, None)
+
+
+def test_realign_rejects(sd):
+    _no_gpu()
+    K = lambda **kw: _kv(sd, **kw)
+    assert sd.lib.specdec_realign_kv(None, ctypes.byref(K()), 3, 10, A, A, A, None, None) == 1
+    assert _realign(sd, src=K(D=12)) == 2                         # D*2 not a multiple of 16
+    assert _realign(sd, src=K(D=0)) == 1
+    assert _realign(sd, src=K(data=A + 8)) == 2                  # not 16-byte aligned
+    assert _realign(sd, src=K(data=None)) == 1
+    assert _realign(sd, src=K(cap=9)) == 1                       # src cap < W_in
+    assert _realign(sd, dst=K(data=A + (1 << 30), cap=9)) == 1   # dst cap < W_in
+    assert _realign(sd, dst=K(data=A + (1 << 30), H=3)) == 1     # shapes differ
+    assert _realign(sd, dst=K(data=A + 4096)) == 1               # partial overlap
+    assert _realign(sd, dst=K(data=A, cap=65)) == 1              # same base, different cap
+    assert _realign(sd, k=-1) == 1
+    assert _realign(sd, W_in=3) == 1
+    assert _realign(sd, pad_in=None) == 1
+    assert _realign(sd, w_new=A + 2) == 2
+
+
+def test_realign_empty_cache_is_a_noop(sd):
+    _no_gpu()
+    assert _realign(sd, src=_kv(sd, L=0), dst=_kv(sd, data=A + (1 << 30), L=0)) == 0
+
+
+def test_posmask_rejects(sd):
+    _no_gpu()
+    f = sd.lib.specdec_build_posmask
+    assert f(A, A, 2, 3, A, A, 3, None, None) == 1         # pm_cap < k+1
+    assert f(None, A, 2, 3, A, A, 64, None, None) == 1
+    assert f(A, A, 2, 3, A + 4, A, 64, None, None) == 2    # pos not 8-byte aligned
+    assert f(A, A, -1, 3, A, A, 64, None, None) == 1
+    assert f(None, None, 0, 3, None, None, 64, None, None) == 0   # empty batch
+
+
+def test_step_rejects(sd):
+    _no_gpu()
+    src, dst = _kv(sd), _kv(sd, data=A + (1 << 30))
+    ws = sd.workspace_bytes(2, 3)
+
+    def step(B=2, pm_cap=64, src=src, dst=dst, ws_bytes=ws):
+        return sd.lib.specdec_step(A, 1, A, A, B, 3, 100, 10, ctypes.byref(src), ctypes.byref(dst), A, A, A, A, A,
+                                   A, A, pm_cap, A, ws_bytes, None, None, None)
+    assert step(pm_cap=13) == 1                  # pm_cap < W_in + k + 1
+    assert step(src=_kv(sd, B=3), dst=_kv(sd, data=A + (1 << 30), B=3)) == 1   # cache rows differ
+    assert step(ws_bytes=8) == 4
+
+
+def test_timing_query_rejects_unknown_kernel(sd):
+    assert sd.lib.specdec_timing_query(7, None, None) == 1
+    assert sd.lib.specdec_timing_enable(0) == 0
+
+
+def test_workspace_init_argument_checks(sd):
+    _no_gpu()
+    assert sd.lib.specdec_workspace_init(None, 0, None) == 0
+    assert sd.lib.specdec_workspace_init(None, 16, None) == 4
