@@ -43,6 +43,7 @@ class StepResult:
     dst: torch.Tensor
     out: dict                     # device outputs copied to host
     pm_cap: int
+    variant: str = "oop"
     extra: dict = field(default_factory=dict)
 
 
@@ -95,7 +96,8 @@ def run_gpu(w: wl.Workload, seed: int = 0, variant: str = "oop", api: str = "ste
     out = dict(tokens=o.tokens.cpu().numpy(), n_acc=o.n_acc.cpu().numpy(), bonus=o.bonus.cpu().numpy(),
                pad_out=o.pad_out.cpu().numpy(), w_new=int(o.w_new.cpu()[0]), pos=o.pos.cpu().numpy(),
                mask=o.mask.cpu().numpy(), dev_status=int(o.dev_status.cpu()[0]))
-    return StepResult(w, W_in, cap, np.asarray(pad_in, np.int32), logits, draft, before, dst, out, pm_cap)
+    return StepResult(w, W_in, cap, np.asarray(pad_in, np.int32), logits, draft, before, dst, out, pm_cap,
+                      variant=variant)
 
 
 def check_verify_vs_oracle(r: StepResult):

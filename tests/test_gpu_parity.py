@@ -36,7 +36,7 @@ def _full_check(r):
     check_kv_full_vs_oracle(r, v)
     check_posmask_vs_oracle(r, v)
     check_relocation_on_device(r, r.out["pad_out"], r.out["n_acc"], r.out["w_new"])
-    if r.dst is not r.src:
+    if r.variant == "oop":
         # out of place: columns [w_new, cap) of the destination are untouched
         tail = i16(r.dst[..., r.out["w_new"]:, :])
         assert bool((tail == SENT_KV).all()), "destination written beyond w_new"
