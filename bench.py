@@ -187,7 +187,7 @@ def main():
         dst = src
         pristine = src.clone()
     pm_cap = W_in + w.k + 1
-    bufs = sd.StepBuffers(w.B, w.k, pm_cap)
+    bufs = sd.StepBuffers(w.B, w.k, w.V, pm_cap)
     pad_t = torch.as_tensor(pad_in, device="cuda")
 
     def step():

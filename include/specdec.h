@@ -89,13 +89,15 @@ int32_t specdec_abi_version(void);
 const char* specdec_last_error(void);
 
 /* Bytes of device workspace specdec_verify_greedy / specdec_step need for a
- * batch of B rows and k drafts (0 on invalid sizes). */
-size_t specdec_workspace_bytes(int32_t B, int32_t k);
+ * batch of B rows, k drafts and a vocabulary of V (0 on invalid sizes).  The
+ * workspace holds per-workgroup partial maxima of the argmax; it needs no
+ * initialisation and its contents after a call are unspecified.  One
+ * workspace serves one in-flight call: calls that share a workspace must be
+ * ordered (same stream). */
+size_t specdec_workspace_bytes(int32_t B, int32_t k, int32_t V);
 
-/* Zero a workspace on `stream` (with a kernel, so it can sit inside captured
- * graphs).  A workspace must be zero before its first use; every successful
- * verify leaves it zero again.  One workspace serves one in-flight call:
- * calls that share a workspace must be ordered (same stream). */
+/* Zero a workspace on `stream` with a kernel (never needed for correctness;
+ * provided for callers that want deterministic scratch contents). */
 specdec_status_t specdec_workspace_init(void* workspace, size_t workspace_bytes, void* stream);
 
 /*
@@ -117,8 +119,8 @@ specdec_status_t specdec_workspace_init(void* workspace, size_t workspace_bytes,
  *             -1 for a row whose pad_in is out of range.
  *   w_new     int32 [1] out: new shared width L' = max_i (c_i + n_acc[i] + 1)
  *             over rows with a valid pad_in (0 if none).  L' <= W_in.
- *   workspace device memory of specdec_workspace_bytes(B, k) bytes, zero
- *             before the call (see specdec_workspace_init), 8-byte aligned.
+ *   workspace device memory of specdec_workspace_bytes(B, k, V) bytes,
+ *             8-byte aligned.
  * B = 0 is a no-op.  Limits: 1 <= V < 2^31, 0 <= k <= SPECDEC_MAX_K,
  * B <= SPECDEC_MAX_B, B*(k+1) <= SPECDEC_MAX_ROWS, k+1 <= W_in <= SPECDEC_MAX_WIDTH.
  */

@@ -131,8 +131,8 @@ specdec_status_t check_verify_args(const void* logits, int32_t dtype, const int3
     if (p && !aligned(p, 4)) return fail(SPECDEC_ERR_UNSUPPORTED, "int32 tensor not 4-byte aligned");
   const int64_t chunk = specdec::verify_chunk_elems(rows, V);
   const int64_t blocks = rows * ((V + chunk - 1) / chunk);
-  if (blocks > 0x7FFFFFFFLL) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "logits too large for one launch");
-  const size_t need = specdec_workspace_bytes(B, k);
+  if (blocks * specdec::kThreads > 0xFFFFFFFFLL) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "logits too large for one launch");
+  const size_t need = specdec_workspace_bytes(B, k, V);
   if (!workspace) return fail(SPECDEC_ERR_WORKSPACE, "workspace is NULL (need %zu bytes)", need);
   if (!aligned(workspace, 8)) return fail(SPECDEC_ERR_WORKSPACE, "workspace not 8-byte aligned");
   if (workspace_bytes < need)
@@ -187,8 +187,7 @@ specdec_status_t check_realign_args(const specdec_kv_t* src, const specdec_kv_t*
   } else if (s0 < d1 && d0 < s1) {
     return fail(SPECDEC_ERR_INVALID_ARGUMENT, "src and dst overlap without being the same cache");
   }
-  const int64_t blocks = specdec::realign_grid_blocks(spans, W_in, src->D, *in_place);
-  if (blocks > 0x70000000LL) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "cache too large for one launch");
+  if (spans > 0xFFFFFFFFLL) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "too many spans");
   return SPECDEC_OK;
 }
 
@@ -213,9 +212,10 @@ int32_t specdec_abi_version(void) { return SPECDEC_ABI_VERSION; }
 
 const char* specdec_last_error(void) { return g_last_error.c_str(); }
 
-size_t specdec_workspace_bytes(int32_t B, int32_t k) {
-  if (B < 0 || B > SPECDEC_MAX_B || k < 0 || k > SPECDEC_MAX_K) return 0;
-  return specdec::kWsHeaderBytes + static_cast<size_t>(B) * static_cast<size_t>(k + 1) * 8u;
+size_t specdec_workspace_bytes(int32_t B, int32_t k, int32_t V) {
+  if (B < 0 || B > SPECDEC_MAX_B || k < 0 || k > SPECDEC_MAX_K || V < 1) return 0;
+  const int64_t rows = static_cast<int64_t>(B) * (k + 1);
+  return specdec::kWsHeaderBytes + static_cast<size_t>(rows * specdec::verify_chunks(rows, V)) * 8u;
 }
 
 specdec_status_t specdec_workspace_init(void* workspace, size_t workspace_bytes, void* stream) {

@@ -8,7 +8,8 @@
 namespace specdec {
 
 constexpr int kThreads = 256;          // every kernel: 4 wavefronts of 64
-constexpr size_t kWsHeaderBytes = 256; // completion counter, padded to a cache line pair
+constexpr size_t kWsHeaderBytes = 256; // reserved, keeps the partial maxima 256-byte aligned
+constexpr int64_t kMaxVerifyChunks = 64;  // workgroups per logit row in the verify scan
 
 struct VerifyLaunch {
   const void* logits;
@@ -21,7 +22,7 @@ struct VerifyLaunch {
   int32_t* bonus;            // may be null
   int32_t* pad_out;
   int32_t* w_new;
-  void* workspace;           // [counter | pad][keys: B*(k+1) uint64]
+  void* workspace;           // [header][partial maxima: B*(k+1)*chunks uint64]
   uint32_t* dev_status;      // may be null
 };
 
@@ -54,8 +55,10 @@ struct PosmaskLaunch {
   uint32_t* dev_status;
 };
 
-// Verify chunking chosen on the host: elements of one logit row per workgroup.
+// Verify chunking chosen on the host: elements of one logit row per
+// workgroup, and workgroups per row.
 int64_t verify_chunk_elems(int64_t rows, int64_t V);
+int64_t verify_chunks(int64_t rows, int64_t V);
 
 // Workgroups of the realign grid (without the fused position-id blocks).
 int64_t realign_grid_blocks(int64_t nspans, int64_t W_in, int32_t D, bool in_place);

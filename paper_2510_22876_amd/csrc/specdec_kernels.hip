@@ -1,10 +1,14 @@
 // HIP kernels for one greedy verify + KV realign step (EqSpec, arXiv 2510.22876)
 // on MI355X (gfx950, wave64).
 //
-//   verify_kernel      vocab-wide argmax of every logit row (Algorithm 3), split
-//                      over workgroups per row; the last workgroup to finish
-//                      runs the prefix-match scan, the bonus token and the new
-//                      width / paddings (Eq. (1), Eq. (2)).
+//   verify_partial     vocab-wide argmax of every logit row (Algorithm 3), split
+//                      over workgroups per row; each workgroup stores its
+//                      packed (key, index) maximum in its own workspace slot.
+//   verify_finalize    one workgroup: reduces the slots of each row, then the
+//                      prefix-match scan, the bonus token and the new width /
+//                      paddings (Eq. (1), Eq. (2)).  Two launches instead of a
+//                      last-workgroup-done counter: a device-scope fence and
+//                      atomic per workgroup costs more than a kernel boundary.
 //   realign_oop        out-of-place unpad-append-repad of the bf16 KV cache:
 //                      one workgroup per 16 KB chunk of a (layer, K/V, row,
 //                      head) span, 128-bit loads and stores.
@@ -16,6 +20,8 @@
 //
 // Everything here is bandwidth-bound data movement plus integer compares: no
 // matrix cores.
+#include <cstdlib>
+
 #include "specdec_internal.h"
 
 namespace specdec {
@@ -129,12 +135,10 @@ struct VerifyArgs {
   int32_t* bonus;
   int32_t* pad_out;
   int32_t* w_new;
-  uint32_t* counter;
-  unsigned long long* keys;
+  unsigned long long* partial;  // [B*(k+1)][chunks] packed maxima
   uint32_t* dev_status;
   int64_t chunk_elems;
-  int32_t chunks;        // workgroups per logit row
-  uint32_t total_blocks;
+  int32_t chunks;               // workgroups per logit row
 };
 
 // Scan logit elements [beg, end) of one row; 16-byte vectors over the aligned
@@ -169,59 +173,9 @@ __device__ __forceinline__ void scan_range(const char* row, int64_t beg, int64_t
   if (tid < end - a1) b.take(T::key_at(row, a1 + tid), static_cast<int32_t>(a1 + tid));
 }
 
-// Prefix-match scan, bonus token and new width, run by the last workgroup.
-__device__ void verify_finalize(const VerifyArgs& a) {
-  __shared__ int32_t wmax[kWaves];
-  const int32_t L = a.W_in - (a.k + 1);
-  const int kp1 = a.k + 1;
-  int32_t local = 0;
-  for (int i = threadIdx.x; i < a.B; i += kThreads) {
-    const int32_t p = a.pad_in[i];
-    const bool ok = p >= 0 && p <= L;
-    int32_t nacc = a.k, bon = -1;
-    bool found = false;
-    for (int r = 0; r < kp1; ++r) {
-      unsigned long long* slot = a.keys + static_cast<int64_t>(i) * kp1 + r;
-      const unsigned long long key = __hip_atomic_load(slot, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      __hip_atomic_store(slot, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      const int32_t pred = static_cast<int32_t>(~static_cast<uint32_t>(key & 0xFFFFFFFFull));
-      a.tokens[static_cast<int64_t>(i) * kp1 + r] = pred;
-      if (!found && (r == a.k || a.draft[static_cast<int64_t>(i) * a.k + r] != pred)) {
-        nacc = r;
-        bon = pred;
-        found = true;
-      }
-    }
-    a.n_acc[i] = nacc;
-    if (a.bonus) a.bonus[i] = bon;
-    if (ok) {
-      const int32_t len = (L - p) + nacc + 1;
-      local = len > local ? len : local;
-    } else if (a.dev_status) {
-      atomicOr(a.dev_status, kBadPadIn);
-    }
-  }
-  local = wave_max_i32(local);
-  if ((threadIdx.x & 63) == 0) wmax[threadIdx.x >> 6] = local;
-  __syncthreads();
-  int32_t w = wmax[0];
-#pragma unroll
-  for (int q = 1; q < kWaves; ++q) w = wmax[q] > w ? wmax[q] : w;
-  for (int i = threadIdx.x; i < a.B; i += kThreads) {
-    const int32_t p = a.pad_in[i];
-    const bool ok = p >= 0 && p <= L;
-    a.pad_out[i] = ok ? w - ((L - p) + a.n_acc[i] + 1) : -1;
-  }
-  if (threadIdx.x == 0) {
-    a.w_new[0] = w;
-    __hip_atomic_store(a.counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  }
-}
-
 template <int DT>
-__global__ __launch_bounds__(kThreads) void verify_kernel(VerifyArgs a) {
+__global__ __launch_bounds__(kThreads) void verify_partial_kernel(VerifyArgs a) {
   __shared__ unsigned long long wkey[kWaves];
-  __shared__ int is_last;
   const int64_t row = blockIdx.x / a.chunks;
   const int64_t chunk = blockIdx.x - row * a.chunks;
   const int64_t beg = chunk * a.chunk_elems;
@@ -240,23 +194,111 @@ __global__ __launch_bounds__(kThreads) void verify_kernel(VerifyArgs a) {
     unsigned long long k2 = wkey[0];
 #pragma unroll
     for (int q = 1; q < kWaves; ++q) k2 = wkey[q] > k2 ? wkey[q] : k2;
-    atomicMax(a.keys + row, k2);
-    __threadfence();
-    const uint32_t prev = atomicAdd(a.counter, 1u);
-    is_last = (prev == a.total_blocks - 1u);
+    a.partial[blockIdx.x] = k2;
   }
+}
+
+// One workgroup of kFinalizeThreads: row maxima, then per sequence the
+// prefix-match scan, the bonus token and its new length; then the width and
+// the paddings.
+constexpr int kFinalizeThreads = 1024;
+
+__global__ __launch_bounds__(kFinalizeThreads) void verify_finalize_kernel(VerifyArgs a) {
+  __shared__ int32_t wmax[kFinalizeThreads / 64];
+  const int32_t L = a.W_in - (a.k + 1);
+  const int kp1 = a.k + 1;
+  const int64_t rows = static_cast<int64_t>(a.B) * kp1;
+  // row maxima -> predicted tokens
+  for (int64_t r = threadIdx.x; r < rows; r += kFinalizeThreads) {
+    const unsigned long long* p = a.partial + r * a.chunks;
+    unsigned long long m = p[0];
+    for (int c = 1; c < a.chunks; ++c) m = p[c] > m ? p[c] : m;
+    a.tokens[r] = static_cast<int32_t>(~static_cast<uint32_t>(m & 0xFFFFFFFFull));
+  }
+  __syncthreads();  // tokens written by this workgroup are visible to it
+  int32_t local = 0;
+  for (int i = threadIdx.x; i < a.B; i += kFinalizeThreads) {
+    const int32_t p = a.pad_in[i];
+    const bool ok = p >= 0 && p <= L;
+    const int32_t* tok = a.tokens + static_cast<int64_t>(i) * kp1;
+    const int32_t* dr = a.draft + static_cast<int64_t>(i) * a.k;
+    int32_t nacc = a.k;
+    for (int r = 0; r < a.k; ++r)
+      if (dr[r] != tok[r]) {
+        nacc = r;
+        break;
+      }
+    a.n_acc[i] = nacc;
+    if (a.bonus) a.bonus[i] = tok[nacc];
+    if (ok) {
+      const int32_t len = (L - p) + nacc + 1;
+      local = len > local ? len : local;
+    } else if (a.dev_status) {
+      atomicOr(a.dev_status, kBadPadIn);
+    }
+  }
+  local = wave_max_i32(local);
+  if ((threadIdx.x & 63) == 0) wmax[threadIdx.x >> 6] = local;
   __syncthreads();
-  if (!is_last) return;
-  __threadfence();
-  verify_finalize(a);
+  int32_t w = wmax[0];
+#pragma unroll
+  for (int q = 1; q < kFinalizeThreads / 64; ++q) w = wmax[q] > w ? wmax[q] : w;
+  for (int i = threadIdx.x; i < a.B; i += kFinalizeThreads) {
+    const int32_t p = a.pad_in[i];
+    const bool ok = p >= 0 && p <= L;
+    a.pad_out[i] = ok ? w - ((L - p) + a.n_acc[i] + 1) : -1;
+  }
+  if (threadIdx.x == 0) a.w_new[0] = w;
 }
 
 // ---------------------------------------------------------------------------
 // realign
+//
+// Tunables (compile-time; the defaults were chosen by sweeping on MI355X):
+//   *_VEC  16-byte vectors per lane per chunk
+//   *_TPB  threads per workgroup (a multiple of 64)
+//   *_NT   nontemporal hints (the cache is streamed once): bit 0 on loads,
+//          bit 1 on stores
+// The out-of-place grid walks each span in chunks of TPB*VEC vectors; within
+// a chunk every wavefront moves one contiguous run of 64*VEC vectors, so the
+// set of DRAM rows touched at any moment stays compact.
 // ---------------------------------------------------------------------------
+#ifndef SPECDEC_OOP_VEC
+#define SPECDEC_OOP_VEC 2
+#endif
+#ifndef SPECDEC_OOP_TPB
+#define SPECDEC_OOP_TPB 64
+#endif
+#ifndef SPECDEC_OOP_NT
+#define SPECDEC_OOP_NT 3
+#endif
+#ifndef SPECDEC_INPLACE_VEC
+#define SPECDEC_INPLACE_VEC 8
+#endif
+#ifndef SPECDEC_INPLACE_TPB
+#define SPECDEC_INPLACE_TPB 512
+#endif
+#ifndef SPECDEC_INPLACE_NT
+#define SPECDEC_INPLACE_NT 3
+#endif
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+template <bool kNt>
+__device__ __forceinline__ u32x4 ld16(const u32x4* p) {
+  if constexpr (kNt) return __builtin_nontemporal_load(p);
+  else return *p;
+}
+
+template <bool kNt>
+__device__ __forceinline__ void st16(u32x4* p, u32x4 v) {
+  if constexpr (kNt) __builtin_nontemporal_store(v, p);
+  else *p = v;
+}
+
 struct RealignArgs {
-  const uint4* src;
-  uint4* dst;
+  const u32x4* src;
+  u32x4* dst;
   int64_t src_span_vecs, dst_span_vecs;  // cap * D / 8
   int32_t vpc;                           // 16-byte vectors per column: D / 8
   int32_t B, H, k, W_in;
@@ -264,14 +306,15 @@ struct RealignArgs {
   const int32_t* n_acc;
   const int32_t* w_new;
   uint32_t* dev_status;
-  int64_t chunks;                        // workgroups per span (out of place)
-  int64_t realign_blocks;
+  uint32_t chunks;                       // workgroups per span (out of place)
+  uint32_t realign_blocks;               // realign workgroups in this launch
+  uint32_t span_base;                    // first span of this launch
   // position ids / mask blocks after the realign blocks
   int64_t* pos;
   uint8_t* mask;
   const int32_t* pad_out;
   int64_t pm_cap;
-  int64_t pm_col_blocks;
+  uint32_t pm_col_blocks;
 };
 
 struct RowGeom {
@@ -296,11 +339,13 @@ __device__ __forceinline__ uint32_t row_geometry(const RealignArgs& a, int row, 
   return 0u;
 }
 
-__device__ void posmask_block(int64_t blk, int64_t* pos, uint8_t* mask,
-                              const int32_t* pad_out, const int32_t* w_new, int32_t k, int64_t pm_cap,
-                              int64_t col_blocks, uint32_t* dev_status) {
-  const int64_t row = blk / col_blocks;
-  const int64_t cb = blk - row * col_blocks;
+// Position ids and mask for 4*kTpb columns of one row.
+template <int kTpb>
+__device__ void posmask_block(uint32_t blk, int64_t* pos, uint8_t* mask, const int32_t* pad_out,
+                              const int32_t* w_new, int32_t k, int64_t pm_cap, uint32_t col_blocks,
+                              uint32_t* dev_status) {
+  const uint32_t row = blk / col_blocks;
+  const uint32_t cb = blk - row * col_blocks;
   const int32_t w = w_new[0];
   const int32_t po = pad_out[row];
   const int64_t width = static_cast<int64_t>(w) + k + 1;
@@ -308,11 +353,11 @@ __device__ void posmask_block(int64_t blk, int64_t* pos, uint8_t* mask,
     if (cb == 0 && threadIdx.x == 0 && dev_status) atomicOr(dev_status, kBadPadOut);
     return;
   }
-  int64_t* prow = pos + row * pm_cap;
-  uint8_t* mrow = mask + row * pm_cap;
+  int64_t* prow = pos + static_cast<int64_t>(row) * pm_cap;
+  uint8_t* mrow = mask + static_cast<int64_t>(row) * pm_cap;
 #pragma unroll
-  for (int q = 0; q < kPmColsPerBlock / kThreads; ++q) {
-    const int64_t j = cb * kPmColsPerBlock + q * kThreads + threadIdx.x;
+  for (int q = 0; q < 4; ++q) {
+    const int64_t j = static_cast<int64_t>(cb) * (4 * kTpb) + q * kTpb + threadIdx.x;
     if (j < width) {
       const bool content = j >= po;
       prow[j] = content ? j - po : 0;
@@ -321,147 +366,150 @@ __device__ void posmask_block(int64_t blk, int64_t* pos, uint8_t* mask,
   }
 }
 
-// Register values of the current thread are live; forces the compiler to
-// wait for the loads that produce them before this point.
-__device__ __forceinline__ void hold(const uint4& v) {
-  asm volatile("" ::"v"(v.x), "v"(v.y), "v"(v.z), "v"(v.w));
-}
-
-template <int kUnroll>
-__global__ __launch_bounds__(kThreads) void realign_oop_kernel(RealignArgs a) {
-  const int64_t b = blockIdx.x;
+template <int kVec, int kTpb, int kNt>
+__global__ __launch_bounds__(kTpb) void realign_oop_kernel(RealignArgs a) {
+  const uint32_t b = blockIdx.x;
   if (b >= a.realign_blocks) {
-    posmask_block(b - a.realign_blocks, a.pos, a.mask, a.pad_out, a.w_new, a.k, a.pm_cap, a.pm_col_blocks,
-                  a.dev_status);
+    posmask_block<kTpb>(b - a.realign_blocks, a.pos, a.mask, a.pad_out, a.w_new, a.k, a.pm_cap, a.pm_col_blocks,
+                        a.dev_status);
     return;
   }
-  const int64_t span = b / a.chunks;
-  const int64_t chunk = b - span * a.chunks;
-  const int row = static_cast<int>((span / a.H) % a.B);
+  const uint32_t rel = b / a.chunks;
+  const uint32_t chunk = b - rel * a.chunks;
+  const uint32_t span = a.span_base + rel;
+  const int row = static_cast<int>((span / static_cast<uint32_t>(a.H)) % static_cast<uint32_t>(a.B));
   RowGeom g;
   const uint32_t err = row_geometry(a, row, g);
   if (err) {
-    if (chunk == 0 && span == static_cast<int64_t>(row) * a.H && threadIdx.x == 0 && a.dev_status)
+    if (chunk == 0 && span == static_cast<uint32_t>(row) * a.H && threadIdx.x == 0 && a.dev_status)
       atomicOr(a.dev_status, err);
     return;
   }
-  constexpr int64_t kChunk = static_cast<int64_t>(kThreads) * kUnroll;
+  constexpr int64_t kChunk = static_cast<int64_t>(kTpb) * kVec;
   const int64_t vpc = a.vpc;
   const int64_t total = static_cast<int64_t>(g.w) * vpc;       // output vectors of the span
-  const int64_t c0 = chunk * kChunk;
+  const int64_t c0 = static_cast<int64_t>(chunk) * kChunk;
   if (c0 >= total) return;
   const int64_t zero_end = static_cast<int64_t>(g.pad_out) * vpc;
   const int64_t shift = static_cast<int64_t>(g.pad_out - g.pad_in) * vpc;
-  const uint4* s = a.src + span * a.src_span_vecs;
-  uint4* d = a.dst + span * a.dst_span_vecs;
-  const int t = threadIdx.x;
-  uint4 v[kUnroll];
+  const u32x4* s = a.src + static_cast<int64_t>(span) * a.src_span_vecs;
+  u32x4* d = a.dst + static_cast<int64_t>(span) * a.dst_span_vecs;
+  // vector j of this lane: c0 + (wave * kVec + j) * 64 + lane
+  const int64_t t0 = c0 + static_cast<int64_t>(threadIdx.x >> 6) * (64 * kVec) + (threadIdx.x & 63);
+  const u32x4 zero = {0u, 0u, 0u, 0u};
+  u32x4 v[kVec];
   if (c0 >= zero_end && c0 + kChunk <= total) {
     // the whole chunk is copied content
 #pragma unroll
-    for (int j = 0; j < kUnroll; ++j) v[j] = s[c0 - shift + j * kThreads + t];
+    for (int j = 0; j < kVec; ++j) v[j] = ld16<(kNt & 1) != 0>(s + (t0 + j * 64 - shift));
 #pragma unroll
-    for (int j = 0; j < kUnroll; ++j) d[c0 + j * kThreads + t] = v[j];
+    for (int j = 0; j < kVec; ++j) st16<(kNt & 2) != 0>(d + (t0 + j * 64), v[j]);
   } else if (c0 + kChunk <= zero_end) {
     // the whole chunk is new padding
 #pragma unroll
-    for (int j = 0; j < kUnroll; ++j) d[c0 + j * kThreads + t] = make_uint4(0u, 0u, 0u, 0u);
+    for (int j = 0; j < kVec; ++j) st16<(kNt & 2) != 0>(d + (t0 + j * 64), zero);
   } else {
     // padding / content boundary or the ragged end of the span; source
     // indices are clamped into the kept range so every load is in bounds
     const int64_t lo = zero_end - shift, hi = total - 1 - shift;
 #pragma unroll
-    for (int j = 0; j < kUnroll; ++j) {
-      int64_t si = c0 + j * kThreads + t - shift;
+    for (int j = 0; j < kVec; ++j) {
+      int64_t si = t0 + j * 64 - shift;
       si = si < lo ? lo : (si > hi ? hi : si);
-      v[j] = s[si];
+      v[j] = ld16<(kNt & 1) != 0>(s + si);
     }
 #pragma unroll
-    for (int j = 0; j < kUnroll; ++j) {
-      const int64_t u = c0 + j * kThreads + t;
-      if (u < total) d[u] = u >= zero_end ? v[j] : make_uint4(0u, 0u, 0u, 0u);
+    for (int j = 0; j < kVec; ++j) {
+      const int64_t u = t0 + j * 64;
+      if (u < total) st16<(kNt & 2) != 0>(d + u, u >= zero_end ? v[j] : zero);
     }
   }
 }
 
-// Moves vectors [lo, lo + kChunk) (clipped to [0, n)) of one row's kept
+// Register values of the current thread are live; forces the compiler to
+// wait for the loads that produce them before this point.
+__device__ __forceinline__ void hold(const u32x4& v) {
+  asm volatile("" ::"v"(v.x), "v"(v.y), "v"(v.z), "v"(v.w));
+}
+
+// Moves vectors [lo, lo + kTpb*kVec) (clipped to [0, n)) of one row's kept
 // entries from `from + u` to `to + u` within the same span.  All reads of the
 // chunk complete before any write to it.
-template <int kUnroll>
-__device__ __forceinline__ void move_chunk(uint4* base, int64_t from, int64_t to, int64_t lo, int64_t n) {
-  constexpr int64_t kChunk = static_cast<int64_t>(kThreads) * kUnroll;
-  const int t = threadIdx.x;
-  uint4 v[kUnroll];
+template <int kVec, int kTpb, int kNt>
+__device__ __forceinline__ void move_chunk(u32x4* base, int64_t from, int64_t to, int64_t lo, int64_t n) {
+  constexpr int64_t kChunk = static_cast<int64_t>(kTpb) * kVec;
+  const int64_t t0 = static_cast<int64_t>(threadIdx.x >> 6) * (64 * kVec) + (threadIdx.x & 63);
+  u32x4 v[kVec];
   if (lo >= 0 && lo + kChunk <= n) {
 #pragma unroll
-    for (int j = 0; j < kUnroll; ++j) v[j] = base[from + lo + j * kThreads + t];
+    for (int j = 0; j < kVec; ++j) v[j] = ld16<(kNt & 1) != 0>(base + (from + lo + t0 + j * 64));
 #pragma unroll
-    for (int j = 0; j < kUnroll; ++j) hold(v[j]);
+    for (int j = 0; j < kVec; ++j) hold(v[j]);
     __syncthreads();
 #pragma unroll
-    for (int j = 0; j < kUnroll; ++j) base[to + lo + j * kThreads + t] = v[j];
+    for (int j = 0; j < kVec; ++j) st16<(kNt & 2) != 0>(base + (to + lo + t0 + j * 64), v[j]);
   } else {
 #pragma unroll
-    for (int j = 0; j < kUnroll; ++j) {
-      int64_t u = lo + j * kThreads + t;
+    for (int j = 0; j < kVec; ++j) {
+      int64_t u = lo + t0 + j * 64;
       u = u < 0 ? 0 : (u >= n ? n - 1 : u);
-      v[j] = base[from + u];
+      v[j] = ld16<(kNt & 1) != 0>(base + (from + u));
     }
 #pragma unroll
-    for (int j = 0; j < kUnroll; ++j) hold(v[j]);
+    for (int j = 0; j < kVec; ++j) hold(v[j]);
     __syncthreads();
 #pragma unroll
-    for (int j = 0; j < kUnroll; ++j) {
-      const int64_t u = lo + j * kThreads + t;
-      if (u >= 0 && u < n) base[to + u] = v[j];
+    for (int j = 0; j < kVec; ++j) {
+      const int64_t u = lo + t0 + j * 64;
+      if (u >= 0 && u < n) st16<(kNt & 2) != 0>(base + (to + u), v[j]);
     }
   }
 }
 
-template <int kUnroll>
-__global__ __launch_bounds__(kThreads) void realign_inplace_kernel(RealignArgs a) {
-  const int64_t b = blockIdx.x;
+template <int kVec, int kTpb, int kNt>
+__global__ __launch_bounds__(kTpb) void realign_inplace_kernel(RealignArgs a) {
+  const uint32_t b = blockIdx.x;
   if (b >= a.realign_blocks) {
-    posmask_block(b - a.realign_blocks, a.pos, a.mask, a.pad_out, a.w_new, a.k, a.pm_cap, a.pm_col_blocks,
-                  a.dev_status);
+    posmask_block<kTpb>(b - a.realign_blocks, a.pos, a.mask, a.pad_out, a.w_new, a.k, a.pm_cap, a.pm_col_blocks,
+                        a.dev_status);
     return;
   }
-  const int64_t span = b;
-  const int row = static_cast<int>((span / a.H) % a.B);
+  const uint32_t span = a.span_base + b;
+  const int row = static_cast<int>((span / static_cast<uint32_t>(a.H)) % static_cast<uint32_t>(a.B));
   RowGeom g;
   const uint32_t err = row_geometry(a, row, g);
   if (err) {
-    if (span == static_cast<int64_t>(row) * a.H && threadIdx.x == 0 && a.dev_status)
-      atomicOr(a.dev_status, err);
+    if (span == static_cast<uint32_t>(row) * a.H && threadIdx.x == 0 && a.dev_status) atomicOr(a.dev_status, err);
     return;
   }
   const int32_t s = g.pad_out - g.pad_in;
   if (s == 0) return;  // no shift: the row is already in place (uniform acceptance)
   const int64_t vpc = a.vpc;
-  uint4* base = a.dst + span * a.dst_span_vecs;
+  u32x4* base = a.dst + static_cast<int64_t>(span) * a.dst_span_vecs;
   const int64_t n = static_cast<int64_t>(g.len) * vpc;
   const int64_t from = static_cast<int64_t>(g.pad_in) * vpc;
   const int64_t to = static_cast<int64_t>(g.pad_out) * vpc;
-  constexpr int64_t kChunk = static_cast<int64_t>(kThreads) * kUnroll;
+  constexpr int64_t kChunk = static_cast<int64_t>(kTpb) * kVec;
   if (s > 0) {
     // moving towards higher addresses: walk from the top, so a chunk's
     // destination never covers source vectors that are still to be read
-    for (int64_t hi = n; hi > 0; hi -= kChunk) move_chunk<kUnroll>(base, from, to, hi - kChunk, n);
+    for (int64_t hi = n; hi > 0; hi -= kChunk) move_chunk<kVec, kTpb, kNt>(base, from, to, hi - kChunk, n);
     // the vacated columns [pad_in, pad_out) become padding; every read of
     // them completed before the last barrier
-    for (int64_t u = threadIdx.x; u < to - from; u += kThreads) base[from + u] = make_uint4(0u, 0u, 0u, 0u);
+    const u32x4 zero = {0u, 0u, 0u, 0u};
+    for (int64_t u = threadIdx.x; u < to - from; u += kTpb) st16<(kNt & 2) != 0>(base + (from + u), zero);
   } else {
     // moving towards lower addresses: walk from the bottom; columns
     // [0, pad_out) already hold padding (+0.0)
-    for (int64_t lo = 0; lo < n; lo += kChunk) move_chunk<kUnroll>(base, from, to, lo, n);
+    for (int64_t lo = 0; lo < n; lo += kChunk) move_chunk<kVec, kTpb, kNt>(base, from, to, lo, n);
   }
 }
 
 __global__ __launch_bounds__(kThreads) void posmask_kernel(int64_t* pos, uint8_t* mask,
                                                            const int32_t* pad_out, const int32_t* w_new,
-                                                           int32_t k, int64_t pm_cap, int64_t col_blocks,
+                                                           int32_t k, int64_t pm_cap, uint32_t col_blocks,
                                                            uint32_t* dev_status) {
-  posmask_block(blockIdx.x, pos, mask, pad_out, w_new, k, pm_cap, col_blocks, dev_status);
+  posmask_block<kThreads>(blockIdx.x, pos, mask, pad_out, w_new, k, pm_cap, col_blocks, dev_status);
 }
 
 __global__ __launch_bounds__(kThreads) void zero_kernel(uint4* p16, int64_t n16, uint8_t* tail, int64_t ntail) {
@@ -470,19 +518,29 @@ __global__ __launch_bounds__(kThreads) void zero_kernel(uint4* p16, int64_t n16,
   if (i < ntail) tail[i] = 0;
 }
 
-constexpr int kOopUnroll = 4;      // 16 KB of a span per workgroup
-constexpr int kInplaceUnroll = 8;  // 32 KB per chunk of the in-place walk
+constexpr int kOopVec = SPECDEC_OOP_VEC, kOopTpb = SPECDEC_OOP_TPB, kOopNt = SPECDEC_OOP_NT;
+constexpr int kInVec = SPECDEC_INPLACE_VEC, kInTpb = SPECDEC_INPLACE_TPB, kInNt = SPECDEC_INPLACE_NT;
+static_assert(kOopTpb % 64 == 0 && kInTpb % 64 == 0, "workgroups are whole wavefronts");
 
 }  // namespace
 
 int64_t verify_chunk_elems(int64_t rows, int64_t V) {
-  // about 2048 workgroups in total, each scanning 2048..16384 elements
+  // about 2048 workgroups in total, each scanning 2048..16384 elements, and
+  // at most kMaxVerifyChunks workgroups per row
   const int64_t per = (rows * V + 2047) / 2048;
   int64_t c = ((per + 2047) / 2048) * 2048;
   if (c < 2048) c = 2048;
   if (c > 16384) c = 16384;
+  int64_t min_c = (V + kMaxVerifyChunks - 1) / kMaxVerifyChunks;
+  min_c = ((min_c + 7) / 8) * 8;
+  if (c < min_c) c = min_c;
   if (c > V) c = V;
   return c;
+}
+
+int64_t verify_chunks(int64_t rows, int64_t V) {
+  const int64_t c = verify_chunk_elems(rows, V);
+  return (V + c - 1) / c;
 }
 
 hipError_t launch_verify(const VerifyLaunch& p, hipStream_t stream) {
@@ -499,27 +557,28 @@ hipError_t launch_verify(const VerifyLaunch& p, hipStream_t stream) {
   a.bonus = p.bonus;
   a.pad_out = p.pad_out;
   a.w_new = p.w_new;
-  a.counter = static_cast<uint32_t*>(p.workspace);
-  a.keys = reinterpret_cast<unsigned long long*>(static_cast<char*>(p.workspace) + kWsHeaderBytes);
+  a.partial = reinterpret_cast<unsigned long long*>(static_cast<char*>(p.workspace) + kWsHeaderBytes);
   a.dev_status = p.dev_status;
   const int64_t rows = static_cast<int64_t>(p.B) * (p.k + 1);
   a.chunk_elems = verify_chunk_elems(rows, p.V);
   a.chunks = static_cast<int32_t>((p.V + a.chunk_elems - 1) / a.chunk_elems);
   const int64_t blocks = rows * a.chunks;
-  a.total_blocks = static_cast<uint32_t>(blocks);
   const dim3 grid(static_cast<uint32_t>(blocks)), block(kThreads);
   switch (p.dtype) {
-    case 0: hipLaunchKernelGGL(verify_kernel<0>, grid, block, 0, stream, a); break;
-    case 1: hipLaunchKernelGGL(verify_kernel<1>, grid, block, 0, stream, a); break;
-    default: hipLaunchKernelGGL(verify_kernel<2>, grid, block, 0, stream, a); break;
+    case 0: hipLaunchKernelGGL(verify_partial_kernel<0>, grid, block, 0, stream, a); break;
+    case 1: hipLaunchKernelGGL(verify_partial_kernel<1>, grid, block, 0, stream, a); break;
+    default: hipLaunchKernelGGL(verify_partial_kernel<2>, grid, block, 0, stream, a); break;
   }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(verify_finalize_kernel, dim3(1), dim3(kFinalizeThreads), 0, stream, a);
   return hipGetLastError();
 }
 
 hipError_t launch_realign(const RealignLaunch& p, hipStream_t stream) {
   RealignArgs a;
-  a.src = static_cast<const uint4*>(p.src);
-  a.dst = static_cast<uint4*>(p.dst);
+  a.src = static_cast<const u32x4*>(p.src);
+  a.dst = static_cast<u32x4*>(p.dst);
   a.vpc = p.D / 8;
   a.src_span_vecs = p.src_cap * a.vpc;
   a.dst_span_vecs = p.dst_cap * a.vpc;
@@ -536,35 +595,50 @@ hipError_t launch_realign(const RealignLaunch& p, hipStream_t stream) {
   a.mask = p.mask;
   a.pad_out = p.pad_out;
   a.pm_cap = p.pm_cap;
+  const int tpb = p.in_place ? kInTpb : kOopTpb;
   int64_t pm_blocks = 0;
+  a.pm_col_blocks = 1;
   if (p.pos) {
     const int64_t bound = static_cast<int64_t>(p.W_in) + p.k + 1;
-    a.pm_col_blocks = (bound + kPmColsPerBlock - 1) / kPmColsPerBlock;
-    pm_blocks = a.pm_col_blocks * p.B;
-  } else {
-    a.pm_col_blocks = 1;
+    a.pm_col_blocks = static_cast<uint32_t>((bound + 4 * tpb - 1) / (4 * tpb));
+    pm_blocks = static_cast<int64_t>(a.pm_col_blocks) * p.B;
   }
-  if (p.in_place) {
-    a.chunks = 1;
-    a.realign_blocks = nspans;
-    const dim3 grid(static_cast<uint32_t>(nspans + pm_blocks)), block(kThreads);
-    if (nspans + pm_blocks == 0) return hipSuccess;
-    hipLaunchKernelGGL(realign_inplace_kernel<kInplaceUnroll>, grid, block, 0, stream, a);
-  } else {
-    const int64_t per_block = static_cast<int64_t>(kThreads) * kOopUnroll;
-    a.chunks = (static_cast<int64_t>(p.W_in) * a.vpc + per_block - 1) / per_block;
-    a.realign_blocks = nspans * a.chunks;
-    const int64_t blocks = a.realign_blocks + pm_blocks;
-    if (blocks == 0) return hipSuccess;
-    const dim3 grid(static_cast<uint32_t>(blocks)), block(kThreads);
-    hipLaunchKernelGGL(realign_oop_kernel<kOopUnroll>, grid, block, 0, stream, a);
+  const int64_t chunks = p.in_place ? 1 : realign_grid_blocks(1, p.W_in, p.D, false);
+  a.chunks = static_cast<uint32_t>(chunks);
+  // one dispatch holds fewer than 2^32 work-items: split the spans over
+  // several launches when the cache is larger than that (the environment
+  // variable SPECDEC_MAX_LAUNCH_ITEMS lowers the cap, to exercise the split)
+  int64_t max_items = 0xFFFFFFFFLL;
+  if (const char* env = std::getenv("SPECDEC_MAX_LAUNCH_ITEMS")) {
+    const long long v = std::atoll(env);
+    if (v > 0 && v < max_items) max_items = v;
   }
-  return hipGetLastError();
+  const int64_t max_blocks = (max_items / tpb) - pm_blocks;
+  const int64_t spans_per_launch = max_blocks / chunks;
+  if (spans_per_launch < 1) return hipErrorInvalidConfiguration;
+  const dim3 block(tpb);
+  for (int64_t s0 = 0; s0 < nspans || (nspans == 0 && s0 == 0); s0 += spans_per_launch) {
+    const int64_t ns = nspans - s0 < spans_per_launch ? nspans - s0 : spans_per_launch;
+    const bool last = s0 + ns >= nspans;
+    a.span_base = static_cast<uint32_t>(s0);
+    a.realign_blocks = static_cast<uint32_t>(ns * chunks);
+    const int64_t blocks = ns * chunks + (last ? pm_blocks : 0);
+    if (blocks == 0) break;
+    const dim3 grid(static_cast<uint32_t>(blocks));
+    if (p.in_place)
+      hipLaunchKernelGGL((realign_inplace_kernel<kInVec, kInTpb, kInNt>), grid, block, 0, stream, a);
+    else
+      hipLaunchKernelGGL((realign_oop_kernel<kOopVec, kOopTpb, kOopNt>), grid, block, 0, stream, a);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    if (nspans == 0) break;
+  }
+  return hipSuccess;
 }
 
 int64_t realign_grid_blocks(int64_t nspans, int64_t W_in, int32_t D, bool in_place) {
   if (in_place) return nspans;
-  const int64_t per_block = static_cast<int64_t>(kThreads) * kOopUnroll;
+  const int64_t per_block = static_cast<int64_t>(kOopTpb) * kOopVec;
   return nspans * ((W_in * (D / 8) + per_block - 1) / per_block);
 }
 
@@ -573,7 +647,7 @@ hipError_t launch_posmask(const PosmaskLaunch& p, hipStream_t stream) {
   const int64_t blocks = col_blocks * p.B;
   if (blocks == 0) return hipSuccess;
   hipLaunchKernelGGL(posmask_kernel, dim3(static_cast<uint32_t>(blocks)), dim3(kThreads), 0, stream, p.pos,
-                     p.mask, p.pad_out, p.w_new, p.k, p.pm_cap, col_blocks, p.dev_status);
+                     p.mask, p.pad_out, p.w_new, p.k, p.pm_cap, static_cast<uint32_t>(col_blocks), p.dev_status);
   return hipGetLastError();
 }
 

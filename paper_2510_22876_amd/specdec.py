@@ -39,15 +39,15 @@ class KV(ctypes.Structure):
                 ("H", ctypes.c_int32), ("D", ctypes.c_int32), ("cap", ctypes.c_int64)]
 
 
-def _load() -> ctypes.CDLL:
-    if not _LIB_PATH.exists():
-        raise ImportError(f"{_LIB_PATH} is not built; run `python -m paper_2510_22876_amd.build`")
-    lib = ctypes.CDLL(str(_LIB_PATH))
+def _load(path: Path = _LIB_PATH) -> ctypes.CDLL:
+    if not Path(path).exists():
+        raise ImportError(f"{path} is not built; run `python -m paper_2510_22876_amd.build`")
+    lib = ctypes.CDLL(str(path))
     P, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
     pKV = ctypes.POINTER(KV)
     lib.specdec_abi_version.restype = i32
     lib.specdec_last_error.restype = ctypes.c_char_p
-    lib.specdec_workspace_bytes.argtypes = [i32, i32]
+    lib.specdec_workspace_bytes.argtypes = [i32, i32, i32]
     lib.specdec_workspace_bytes.restype = sz
     lib.specdec_workspace_init.argtypes = [P, sz, P]
     lib.specdec_verify_greedy.argtypes = [P, i32, P, P, i32, i32, i32, i32, P, P, P, P, P, P, sz, P, P]
@@ -120,16 +120,15 @@ def abi_version() -> int:
     return lib.specdec_abi_version()
 
 
-def workspace_bytes(B: int, k: int) -> int:
-    return lib.specdec_workspace_bytes(B, k)
+def workspace_bytes(B: int, k: int, V: int) -> int:
+    return lib.specdec_workspace_bytes(B, k, V)
 
 
-def alloc_workspace(B: int, k: int, device="cuda") -> torch.Tensor:
-    """A zeroed workspace tensor for specdec_verify_greedy / specdec_step."""
-    n = workspace_bytes(B, k)
-    ws = torch.empty((n + 7) // 8, dtype=torch.int64, device=device)
-    specdec_workspace_init(ws, n)
-    return ws
+def alloc_workspace(B: int, k: int, V: int, device="cuda") -> torch.Tensor:
+    """A workspace tensor for specdec_verify_greedy / specdec_step (needs no
+    initialisation)."""
+    n = workspace_bytes(B, k, V)
+    return torch.empty((n + 7) // 8, dtype=torch.int64, device=device)
 
 
 def specdec_workspace_init(workspace: torch.Tensor, nbytes: int | None = None, stream=None) -> None:
@@ -150,7 +149,7 @@ def _check_verify(logits, draft, pad_in, tokens, n_acc, bonus, pad_out, w_new, w
     _req("pad_out", pad_out, (B,), i32)
     _req("w_new", w_new, (1,), i32)
     _req("dev_status", dev_status, (1,), i32, optional=True)
-    if workspace.numel() * workspace.element_size() < workspace_bytes(B, kp1 - 1) or not workspace.is_cuda:
+    if workspace.numel() * workspace.element_size() < workspace_bytes(B, kp1 - 1, V) or not workspace.is_cuda:
         raise ValueError("workspace too small")
 
 
@@ -223,9 +222,10 @@ def timing_query(kernel: int) -> tuple[float, int]:
 
 
 class StepBuffers:
-    """Device outputs of one step for B rows, k drafts and a pos/mask stride."""
+    """Device outputs of one step for B rows, k drafts, a vocabulary of V and a
+    pos/mask stride."""
 
-    def __init__(self, B: int, k: int, pm_cap: int, device="cuda"):
+    def __init__(self, B: int, k: int, V: int, pm_cap: int, device="cuda"):
         i32 = dict(dtype=torch.int32, device=device)
         self.tokens = torch.empty((B, k + 1), **i32)
         self.n_acc = torch.empty(B, **i32)
@@ -235,4 +235,4 @@ class StepBuffers:
         self.pos = torch.empty((B, pm_cap), dtype=torch.int64, device=device)
         self.mask = torch.empty((B, pm_cap), dtype=torch.uint8, device=device)
         self.dev_status = torch.zeros(1, **i32)
-        self.workspace = alloc_workspace(B, k, device)
+        self.workspace = alloc_workspace(B, k, V, device)

@@ -47,9 +47,9 @@ class StepResult:
     extra: dict = field(default_factory=dict)
 
 
-def alloc_outputs(B, k, pm_cap, device="cuda"):
+def alloc_outputs(B, k, V, pm_cap, device="cuda"):
     from paper_2510_22876_amd import specdec as sd
-    bufs = sd.StepBuffers(B, k, pm_cap, device)
+    bufs = sd.StepBuffers(B, k, V, pm_cap, device)
     for t in (bufs.tokens, bufs.n_acc, bufs.bonus, bufs.pad_out, bufs.w_new):
         t.fill_(-99)
     bufs.pos.fill_(SENT_POS)
@@ -82,7 +82,7 @@ def run_gpu(w: wl.Workload, seed: int = 0, variant: str = "oop", api: str = "ste
         dst = src
         before = src.clone() if keep_src else None
     pm_cap = W_in + w.k + 1 + 3
-    o = alloc_outputs(w.B, w.k, pm_cap)
+    o = alloc_outputs(w.B, w.k, w.V, pm_cap)
     pad_t = torch.as_tensor(np.asarray(pad_in, np.int32), device="cuda")
     if api == "step":
         sd.specdec_step(logits, draft, pad_t, W_in, src, dst, o.tokens, o.n_acc, o.bonus, o.pad_out,

@@ -42,10 +42,14 @@ def test_abi_version_matches_header(sd):
 
 
 def test_workspace_bytes(sd):
-    assert sd.workspace_bytes(8, 5) == 256 + 8 * 6 * 8
-    assert sd.workspace_bytes(0, 0) == 256
-    assert sd.workspace_bytes(-1, 2) == 0
-    assert sd.workspace_bytes(4, 65) == 0
+    # 48 rows of 32000: 16 workgroups of 2048 elements per row
+    assert sd.workspace_bytes(8, 5, 32000) == 256 + 8 * 6 * 16 * 8
+    assert sd.workspace_bytes(0, 0, 10) == 256
+    assert sd.workspace_bytes(-1, 2, 10) == 0
+    assert sd.workspace_bytes(4, 65, 10) == 0
+    assert sd.workspace_bytes(4, 2, 0) == 0
+    # never more than 64 workgroups per row
+    assert sd.workspace_bytes(1, 0, 2 ** 31 - 1) == 256 + 64 * 8
 
 
 def _no_gpu():
@@ -61,7 +65,7 @@ P = ctypes.c_void_p
 
 def _verify(sd, **over):
     args = dict(logits=A, dtype=1, draft=A, pad_in=A, B=2, k=3, V=100, W_in=10, tokens=A, n_acc=A,
-                bonus=A, pad_out=A, w_new=A, ws=A, ws_bytes=sd.workspace_bytes(2, 3), status=None, stream=None)
+                bonus=A, pad_out=A, w_new=A, ws=A, ws_bytes=sd.workspace_bytes(2, 3, 100), status=None, stream=None)
     args.update(over)
     return sd.lib.specdec_verify_greedy(*args.values())
 
@@ -134,7 +138,7 @@ def test_posmask_rejects(sd):
 def test_step_rejects(sd):
     _no_gpu()
     src, dst = _kv(sd), _kv(sd, data=A + (1 << 30))
-    ws = sd.workspace_bytes(2, 3)
+    ws = sd.workspace_bytes(2, 3, 100)
 
     def step(B=2, pm_cap=64, src=src, dst=dst, ws_bytes=ws):
         return sd.lib.specdec_step(A, 1, A, A, B, 3, 100, 10, ctypes.byref(src), ctypes.byref(dst), A, A, A, A, A,

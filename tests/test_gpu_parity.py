@@ -137,7 +137,7 @@ def test_unaligned_logits_pointer():
 
 def test_empty_batch_is_a_noop():
     from paper_2510_22876_amd import specdec as sd
-    o = alloc_outputs(1, 2, 10)
+    o = alloc_outputs(1, 2, 50, 10)
     e = torch.empty((0, 3, 50), dtype=torch.bfloat16, device="cuda")
     d = torch.empty((0, 2), dtype=torch.int32, device="cuda")
     z = torch.empty(0, dtype=torch.int32, device="cuda")
@@ -148,14 +148,15 @@ def test_empty_batch_is_a_noop():
 
 
 def test_workspace_reused_across_calls():
-    """The completion counter and per-row keys reset themselves after each
-    verify: consecutive calls on one workspace with different inputs all agree
-    with the oracle."""
+    """Consecutive calls on one workspace (filled with garbage first) with
+    different inputs all agree with the oracle: the workspace needs no
+    initialisation."""
     from paper_2510_22876_amd import specdec as sd
     w = SMALL["vicuna7b_small"]
-    o = alloc_outputs(w.B, w.k, 2000)
+    o = alloc_outputs(w.B, w.k, w.V, 2000)
     n, W_in, pad_in, cap = wl.initial_geometry(w)
     pad_t = torch.as_tensor(pad_in, device="cuda")
+    o.workspace.fill_(0x5A5A5A5A5A5A5A5A)
     for seed in range(5):
         logits, draft, *_ = wl.logits_and_drafts(w, seed, seed, device="cuda")
         say(f"workspace reuse call {seed}")
@@ -166,8 +167,6 @@ def test_workspace_reused_across_calls():
         assert np.array_equal(o.tokens.cpu().numpy(), v["tokens"])
         assert np.array_equal(o.n_acc.cpu().numpy(), v["n_acc"])
         assert int(o.w_new.cpu()[0]) == v["w_new"]
-    ws = o.workspace.view(torch.int64)
-    assert bool((ws == 0).all()), "workspace not left zero"
 
 
 def test_out_of_range_device_values_are_flagged():
@@ -184,7 +183,7 @@ def test_out_of_range_device_values_are_flagged():
     logits, draft, *_ = wl.logits_and_drafts(w, 0, 0, device="cuda")
     src = wl.make_kv(w, pad_in, W_in, cap, device="cuda")
     dst = torch.full_like(i16(src), SENT_KV).view(torch.bfloat16)
-    o = alloc_outputs(w.B, w.k, W_in + w.k + 1)
+    o = alloc_outputs(w.B, w.k, w.V, W_in + w.k + 1)
     sd.specdec_step(logits, draft, torch.as_tensor(bad, device="cuda"), W_in, src, dst, o.tokens, o.n_acc,
                     o.bonus, o.pad_out, o.w_new, o.pos, o.mask, o.workspace, o.dev_status)
     torch.cuda.synchronize()
