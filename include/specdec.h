@@ -186,18 +186,20 @@ specdec_status_t specdec_step(const void* logits, int32_t dtype, const int32_t* 
                               int32_t* w_new_host, void* stream);
 
 /*
- * Kernel timers (for measurement; off by default).  While enabled, the
- * library records a pair of HIP events on the launch stream around each of
- * its kernel launches.  specdec_timing_query waits for the recorded events,
- * adds their durations to the totals of `kernel`
- * (0 = verify, 1 = realign (with the fused position ids / mask in
- * specdec_step), 2 = position ids / mask alone) and returns the totals since
- * the last reset.
+ * Kernel timers (for measurement; off by default).  specdec_timing_enable
+ * takes a mask of kernels (bit 1 << SPECDEC_KERNEL_*; 0 turns the timers
+ * off).  For each selected kernel the library records a pair of HIP events on
+ * the launch stream around its launch (verify: around its two launches).
+ * specdec_timing_query waits for the recorded events, adds their durations to
+ * the totals of `kernel` (0 = verify, 1 = realign, with the fused position ids
+ * / mask in specdec_step, 2 = position ids / mask alone) and returns the
+ * totals since the last reset.
  */
 #define SPECDEC_KERNEL_VERIFY 0
 #define SPECDEC_KERNEL_REALIGN 1
 #define SPECDEC_KERNEL_POSMASK 2
-specdec_status_t specdec_timing_enable(int32_t on);
+#define SPECDEC_TIMING_ALL 7
+specdec_status_t specdec_timing_enable(int32_t kernel_mask);
 specdec_status_t specdec_timing_reset(void);
 specdec_status_t specdec_timing_query(int32_t kernel, double* total_ms, int64_t* launches);
 

@@ -56,7 +56,7 @@ struct TimedLaunch {
 
 struct Timers {
   std::mutex mu;
-  bool on = false;
+  int32_t mask = 0;
   std::vector<TimedLaunch> pending;
   std::vector<hipEvent_t> pool;
   double total_ms[3] = {0, 0, 0};
@@ -86,7 +86,7 @@ hipError_t timed(int kernel, hipStream_t stream, F&& launch) {
   hipEvent_t b = nullptr, e = nullptr;
   {
     std::lock_guard<std::mutex> lk(t.mu);
-    if (t.on) {
+    if (t.mask & (1 << kernel)) {
       b = take_event(t);
       e = take_event(t);
     }
@@ -343,10 +343,12 @@ specdec_status_t specdec_step(const void* logits, int32_t dtype, const int32_t* 
   return ok();
 }
 
-specdec_status_t specdec_timing_enable(int32_t on) {
+specdec_status_t specdec_timing_enable(int32_t kernel_mask) {
+  if (kernel_mask < 0 || kernel_mask > SPECDEC_TIMING_ALL)
+    return fail(SPECDEC_ERR_INVALID_ARGUMENT, "timing mask %d outside [0,%d]", kernel_mask, SPECDEC_TIMING_ALL);
   Timers& t = timers();
   std::lock_guard<std::mutex> lk(t.mu);
-  t.on = on != 0;
+  t.mask = kernel_mask;
   return ok();
 }
 

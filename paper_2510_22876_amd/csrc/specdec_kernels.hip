@@ -255,19 +255,26 @@ __global__ __launch_bounds__(kFinalizeThreads) void verify_finalize_kernel(Verif
 // realign
 //
 // Tunables (compile-time; the defaults were chosen by sweeping on MI355X):
-//   *_VEC  16-byte vectors per lane per chunk
+//   *_VEC  16-byte vectors per lane per chunk (out of place: pieces per
+//          workgroup)
 //   *_TPB  threads per workgroup (a multiple of 64)
+//   OOP_SPLIT  distance in vectors between the pieces of an out-of-place
+//          workgroup
 //   *_NT   nontemporal hints (the cache is streamed once): bit 0 on loads,
 //          bit 1 on stores
-// The out-of-place grid walks each span in chunks of TPB*VEC vectors; within
-// a chunk every wavefront moves one contiguous run of 64*VEC vectors, so the
-// set of DRAM rows touched at any moment stays compact.
+// Small, in-order workgroups keep the set of DRAM rows touched at any moment
+// compact; spreading a workgroup's pieces apart keeps that pattern while
+// halving the number of workgroups, which matters where a workgroup only
+// stores (padding) and the dispatch rate would otherwise bound the kernel.
 // ---------------------------------------------------------------------------
 #ifndef SPECDEC_OOP_VEC
 #define SPECDEC_OOP_VEC 2
 #endif
 #ifndef SPECDEC_OOP_TPB
 #define SPECDEC_OOP_TPB 64
+#endif
+#ifndef SPECDEC_OOP_SPLIT
+#define SPECDEC_OOP_SPLIT 512
 #endif
 #ifndef SPECDEC_OOP_NT
 #define SPECDEC_OOP_NT 3
@@ -321,11 +328,18 @@ struct RowGeom {
   int32_t pad_in, pad_out, len, w;
 };
 
+// Loads a value that no kernel of this launch writes, through the constant
+// address space: a wave-uniform address then becomes a scalar load on the
+// scalar cache path instead of a vector load queued behind the data traffic.
+__device__ __forceinline__ int32_t load_invariant(const int32_t* p) {
+  return *(const __attribute__((address_space(4))) int32_t*)p;
+}
+
 __device__ __forceinline__ uint32_t row_geometry(const RealignArgs& a, int row, RowGeom& g) {
   const int32_t L = a.W_in - (a.k + 1);
-  const int32_t w = a.w_new[0];
-  const int32_t p = a.pad_in[row];
-  const int32_t n = a.n_acc[row];
+  const int32_t w = load_invariant(a.w_new);
+  const int32_t p = load_invariant(a.pad_in + row);
+  const int32_t n = load_invariant(a.n_acc + row);
   uint32_t err = 0u;
   if (p < 0 || p > L) err |= kBadPadIn;
   if (n < 0 || n > a.k) err |= kBadAccept;
@@ -346,8 +360,8 @@ __device__ void posmask_block(uint32_t blk, int64_t* pos, uint8_t* mask, const i
                               uint32_t* dev_status) {
   const uint32_t row = blk / col_blocks;
   const uint32_t cb = blk - row * col_blocks;
-  const int32_t w = w_new[0];
-  const int32_t po = pad_out[row];
+  const int32_t w = load_invariant(w_new);
+  const int32_t po = load_invariant(pad_out + row);
   const int64_t width = static_cast<int64_t>(w) + k + 1;
   if (w < 0 || po < 0 || po > w || width > pm_cap) {
     if (cb == 0 && threadIdx.x == 0 && dev_status) atomicOr(dev_status, kBadPadOut);
@@ -366,8 +380,15 @@ __device__ void posmask_block(uint32_t blk, int64_t* pos, uint8_t* mask, const i
   }
 }
 
-template <int kVec, int kTpb, int kNt>
+// Out of place: every workgroup moves kPieces pieces of kTpb 16-byte vectors
+// (one per lane) of one span's output, the pieces kSplit vectors apart.  The
+// output of a span is cut into groups of kPieces*kSplit vectors; group g is
+// covered by kSplit/kTpb workgroups.  Each piece is new padding (stores only),
+// kept content (a load from the shifted source position and a store), or the
+// boundary between them / the ragged end of the span.
+template <int kPieces, int kTpb, int kSplit, int kNt>
 __global__ __launch_bounds__(kTpb) void realign_oop_kernel(RealignArgs a) {
+  static_assert(kSplit % kTpb == 0, "a group is a whole number of workgroups");
   const uint32_t b = blockIdx.x;
   if (b >= a.realign_blocks) {
     posmask_block<kTpb>(b - a.realign_blocks, a.pos, a.mask, a.pad_out, a.w_new, a.k, a.pm_cap, a.pm_col_blocks,
@@ -375,53 +396,54 @@ __global__ __launch_bounds__(kTpb) void realign_oop_kernel(RealignArgs a) {
     return;
   }
   const uint32_t rel = b / a.chunks;
-  const uint32_t chunk = b - rel * a.chunks;
+  const uint32_t sub = b - rel * a.chunks;            // workgroup within the span
   const uint32_t span = a.span_base + rel;
   const int row = static_cast<int>((span / static_cast<uint32_t>(a.H)) % static_cast<uint32_t>(a.B));
   RowGeom g;
   const uint32_t err = row_geometry(a, row, g);
   if (err) {
-    if (chunk == 0 && span == static_cast<uint32_t>(row) * a.H && threadIdx.x == 0 && a.dev_status)
+    if (sub == 0 && span == static_cast<uint32_t>(row) * a.H && threadIdx.x == 0 && a.dev_status)
       atomicOr(a.dev_status, err);
     return;
   }
-  constexpr int64_t kChunk = static_cast<int64_t>(kTpb) * kVec;
+  constexpr uint32_t kPerGroup = kSplit / kTpb;
+  const uint32_t grp = sub / kPerGroup;
+  const int64_t base = static_cast<int64_t>(grp) * (kPieces * kSplit) + static_cast<int64_t>(sub - grp * kPerGroup) * kTpb;
   const int64_t vpc = a.vpc;
-  const int64_t total = static_cast<int64_t>(g.w) * vpc;       // output vectors of the span
-  const int64_t c0 = static_cast<int64_t>(chunk) * kChunk;
-  if (c0 >= total) return;
+  const int64_t total = static_cast<int64_t>(g.w) * vpc;        // output vectors of the span
+  if (base >= total) return;
   const int64_t zero_end = static_cast<int64_t>(g.pad_out) * vpc;
   const int64_t shift = static_cast<int64_t>(g.pad_out - g.pad_in) * vpc;
   const u32x4* s = a.src + static_cast<int64_t>(span) * a.src_span_vecs;
   u32x4* d = a.dst + static_cast<int64_t>(span) * a.dst_span_vecs;
-  // vector j of this lane: c0 + (wave * kVec + j) * 64 + lane
-  const int64_t t0 = c0 + static_cast<int64_t>(threadIdx.x >> 6) * (64 * kVec) + (threadIdx.x & 63);
+  const int t = threadIdx.x;
   const u32x4 zero = {0u, 0u, 0u, 0u};
-  u32x4 v[kVec];
-  if (c0 >= zero_end && c0 + kChunk <= total) {
-    // the whole chunk is copied content
+  const int64_t lo = zero_end - shift, hi = total - 1 - shift;   // kept source range
+  u32x4 v[kPieces];
 #pragma unroll
-    for (int j = 0; j < kVec; ++j) v[j] = ld16<(kNt & 1) != 0>(s + (t0 + j * 64 - shift));
-#pragma unroll
-    for (int j = 0; j < kVec; ++j) st16<(kNt & 2) != 0>(d + (t0 + j * 64), v[j]);
-  } else if (c0 + kChunk <= zero_end) {
-    // the whole chunk is new padding
-#pragma unroll
-    for (int j = 0; j < kVec; ++j) st16<(kNt & 2) != 0>(d + (t0 + j * 64), zero);
-  } else {
-    // padding / content boundary or the ragged end of the span; source
-    // indices are clamped into the kept range so every load is in bounds
-    const int64_t lo = zero_end - shift, hi = total - 1 - shift;
-#pragma unroll
-    for (int j = 0; j < kVec; ++j) {
-      int64_t si = t0 + j * 64 - shift;
+  for (int j = 0; j < kPieces; ++j) {
+    const int64_t p0 = base + static_cast<int64_t>(j) * kSplit;  // first vector of the piece
+    if (p0 >= zero_end && p0 + kTpb <= total) {
+      v[j] = ld16<(kNt & 1) != 0>(s + (p0 + t - shift));
+    } else if (p0 + kTpb > zero_end && p0 < total) {
+      int64_t si = p0 + t - shift;
       si = si < lo ? lo : (si > hi ? hi : si);
       v[j] = ld16<(kNt & 1) != 0>(s + si);
+    } else {
+      v[j] = zero;
     }
+  }
 #pragma unroll
-    for (int j = 0; j < kVec; ++j) {
-      const int64_t u = t0 + j * 64;
-      if (u < total) st16<(kNt & 2) != 0>(d + u, u >= zero_end ? v[j] : zero);
+  for (int j = 0; j < kPieces; ++j) {
+    const int64_t p0 = base + static_cast<int64_t>(j) * kSplit;
+    if (p0 >= total) break;
+    const int64_t u = p0 + t;
+    if (p0 + kTpb <= zero_end) {
+      st16<(kNt & 2) != 0>(d + u, zero);
+    } else if (p0 >= zero_end && p0 + kTpb <= total) {
+      st16<(kNt & 2) != 0>(d + u, v[j]);
+    } else if (u < total) {
+      st16<(kNt & 2) != 0>(d + u, u >= zero_end ? v[j] : zero);
     }
   }
 }
@@ -519,6 +541,7 @@ __global__ __launch_bounds__(kThreads) void zero_kernel(uint4* p16, int64_t n16,
 }
 
 constexpr int kOopVec = SPECDEC_OOP_VEC, kOopTpb = SPECDEC_OOP_TPB, kOopNt = SPECDEC_OOP_NT;
+constexpr int kOopSplit = SPECDEC_OOP_SPLIT;
 constexpr int kInVec = SPECDEC_INPLACE_VEC, kInTpb = SPECDEC_INPLACE_TPB, kInNt = SPECDEC_INPLACE_NT;
 static_assert(kOopTpb % 64 == 0 && kInTpb % 64 == 0, "workgroups are whole wavefronts");
 
@@ -628,7 +651,7 @@ hipError_t launch_realign(const RealignLaunch& p, hipStream_t stream) {
     if (p.in_place)
       hipLaunchKernelGGL((realign_inplace_kernel<kInVec, kInTpb, kInNt>), grid, block, 0, stream, a);
     else
-      hipLaunchKernelGGL((realign_oop_kernel<kOopVec, kOopTpb, kOopNt>), grid, block, 0, stream, a);
+      hipLaunchKernelGGL((realign_oop_kernel<kOopVec, kOopTpb, kOopSplit, kOopNt>), grid, block, 0, stream, a);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     if (nspans == 0) break;
@@ -638,8 +661,9 @@ hipError_t launch_realign(const RealignLaunch& p, hipStream_t stream) {
 
 int64_t realign_grid_blocks(int64_t nspans, int64_t W_in, int32_t D, bool in_place) {
   if (in_place) return nspans;
-  const int64_t per_block = static_cast<int64_t>(kOopTpb) * kOopVec;
-  return nspans * ((W_in * (D / 8) + per_block - 1) / per_block);
+  const int64_t per_group = static_cast<int64_t>(kOopSplit) * kOopVec;
+  const int64_t groups = (W_in * (D / 8) + per_group - 1) / per_group;
+  return nspans * groups * (kOopSplit / kOopTpb);
 }
 
 hipError_t launch_posmask(const PosmaskLaunch& p, hipStream_t stream) {

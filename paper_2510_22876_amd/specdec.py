@@ -18,6 +18,7 @@ OK, ERR_INVALID_ARGUMENT, ERR_UNSUPPORTED, ERR_HIP, ERR_WORKSPACE = 0, 1, 2, 3, 
 F32, BF16, F16 = 0, 1, 2
 DTYPE_OF = {torch.float32: F32, torch.bfloat16: BF16, torch.float16: F16}
 KERNEL_VERIFY, KERNEL_REALIGN, KERNEL_POSMASK = 0, 1, 2
+TIMING_ALL = 7
 DEV_BAD_PAD_IN, DEV_BAD_ACCEPT, DEV_BAD_WIDTH, DEV_BAD_PAD_OUT = 1, 2, 4, 8
 
 EXPORTED = (
@@ -206,8 +207,10 @@ def specdec_step(logits, draft, pad_in, W_in: int, src, dst, tokens, n_acc, bonu
     return host.value if sync_w_new else None
 
 
-def timing_enable(on: bool = True) -> None:
-    _check(lib.specdec_timing_enable(1 if on else 0))
+def timing_enable(on=True) -> None:
+    """True / False for all kernels, or a mask of (1 << KERNEL_*) bits."""
+    mask = TIMING_ALL if on is True else (0 if on is False else int(on))
+    _check(lib.specdec_timing_enable(mask))
 
 
 def timing_reset() -> None:

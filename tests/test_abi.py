@@ -151,6 +151,8 @@ def test_step_rejects(sd):
 def test_timing_query_rejects_unknown_kernel(sd):
     assert sd.lib.specdec_timing_query(7, None, None) == 1
     assert sd.lib.specdec_timing_enable(0) == 0
+    assert sd.lib.specdec_timing_enable(8) == 1
+    assert sd.lib.specdec_timing_enable(-1) == 1
 
 
 def test_workspace_init_argument_checks(sd):
