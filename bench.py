@@ -1,9 +1,9 @@
 #!/usr/bin/env python3
 """Benchmark of one greedy verify + KV realign step (EqSpec) on one MI355X.
 
-A step is one call of the fused ``specdec_step`` (verify kernel, then the
-realign kernel with the position ids / mask fused in) over one batch of
-synthetic input already resident in HBM.  The default workload is the
+A step is one call of the fused ``specdec_step`` (the two verify kernels,
+then the realign kernel with the position ids / mask and the token row S
+fused in) over one batch of synthetic input already resident in HBM.  The default workload is the
 Vicuna-7B-shaped batch (B=8, k=5, V=32000 bf16 logits; KV L=32, H=32, D=128
 bf16; prompts U[128,1024]; out-of-place realign).
 
@@ -52,7 +52,7 @@ def describe(w, variant):
             f"prompts {pr}; accept {w.accept[0]}; {'out-of-place' if variant == 'oop' else 'in-place'} realign")
 
 
-def step_bytes(w, pad_in, W_in, n_acc, w_new, variant):
+def step_bytes(w, pad_in, W_in, n_acc, w_new, variant, token_row=True):
     """Algorithmic bytes of one step: what the method must read and write."""
     C = w.column_bytes
     W0 = W_in - (w.k + 1)
@@ -65,6 +65,9 @@ def step_bytes(w, pad_in, W_in, n_acc, w_new, variant):
         moved = shift != 0
         realign = int(2 * lens[moved].sum()) * C + int(np.clip(shift, 0, None).sum()) * C
     posmask = w.B * (w_new + w.k + 1) * (8 + 1)
+    if token_row:   # read each row's c_i + 1 tokens and n_acc + 1 predictions, write w_new + 1 columns
+        posmask += 4 * int((lens - n_acc.astype(np.int64)).sum()) + 4 * int((n_acc.astype(np.int64) + 1).sum()) \
+            + 4 * w.B * (w_new + 1)
     verify = w.B * (w.k + 1) * w.V * w.logit_bytes + 4 * w.B * w.k + 4 * w.B \
         + 4 * w.B * (w.k + 1) + 3 * 4 * w.B + 4
     return dict(realign=realign, posmask=posmask, verify=verify)
@@ -86,11 +89,11 @@ def read_traffic_summary(workload: str, variant: str):
     return float(m_bytes.group(1)), path.name
 
 
-def cpu_baseline(w, logits, draft, pad_in, W_in, src, budget_s: float):
+def cpu_baseline(w, logits, draft, pad_in, W_in, src, budget_s: float, s_rows=None):
     """The oracle as it stands, single-threaded on the host, on a bounded
     sample: verification over every logit row, the KV realignment of whole
     layer slabs (cycling over up to two layers until ``budget_s`` seconds of
-    work), and position ids / mask; scaled to one whole step."""
+    work), position ids / mask and the token row; scaled to one whole step."""
     import oracle
     k = w.k
     lg = logits.cpu()
@@ -100,6 +103,8 @@ def cpu_baseline(w, logits, draft, pad_in, W_in, src, budget_s: float):
     t_verify = time.perf_counter() - t0
     t0 = time.perf_counter()
     oracle.posmask(v["pad_out"], v["w_new"], k)
+    if s_rows is not None:
+        oracle.realign_tokens(s_rows, v["tokens"], pad_in, v["n_acc"], v["w_new"], W_in, -1)
     t_pm = time.perf_counter() - t0
     nl = min(w.L, 2)
     slabs = [src[l:l + 1, :, :, :, :W_in, :].contiguous() for l in range(nl)]
@@ -118,7 +123,7 @@ def cpu_baseline(w, logits, draft, pad_in, W_in, src, budget_s: float):
     return dict(value=1.0 / est, unit="steps/s", cores=1, kind="oracle",
                 sample=(f"oracle verify over all {w.B * (w.k + 1)} logit rows ({t_verify * 1e3:.1f} ms), "
                         f"KV realign of {runs} one-layer slabs cycling over layers 0..{nl - 1} "
-                        f"({per_layer * 1e3:.1f} ms per layer, x{w.L} layers), pos/mask ({t_pm * 1e3:.2f} ms); "
+                        f"({per_layer * 1e3:.1f} ms per layer, x{w.L} layers), pos/mask and token row ({t_pm * 1e3:.2f} ms); "
                         f"single-threaded, scaled to one whole step ({est:.2f} s)"))
 
 
@@ -151,6 +156,7 @@ def main():
     ap.add_argument("--workload", default="vicuna7b")
     ap.add_argument("--variant", default="oop", choices=["oop", "inplace"])
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-token-row", action="store_true", help="leave the token row S out of the step")
     ap.add_argument("--cpu-baseline-seconds", type=float, default=10.0,
                     help="seconds of oracle realign work for the CPU baseline (0: skip)")
     ap.add_argument("--kernel-timers", choices=["on", "off"], default="on",
@@ -192,13 +198,22 @@ def main():
     pm_cap = W_in + w.k + 1
     bufs = sd.StepBuffers(w.B, w.k, w.V, pm_cap)
     pad_t = torch.as_tensor(pad_in, device="cuda")
+    token_row = not args.no_token_row
+    s_in = s_out = None
+    if token_row:
+        s_in = wl.make_token_rows(w, pad_in, W_in, W_in + 1, args.seed, -1, device="cuda")
+        s_out = torch.empty_like(s_in) if variant == "oop" else s_in
+    pristine_s = s_in.clone() if (token_row and variant != "oop") else None
 
     def step():
         sd.specdec_step(logits, draft, pad_t, W_in, src, dst, bufs.tokens, bufs.n_acc, bufs.bonus, bufs.pad_out,
-                        bufs.w_new, bufs.pos, bufs.mask, bufs.workspace, bufs.dev_status)
+                        bufs.w_new, bufs.pos, bufs.mask, bufs.workspace, bufs.dev_status, s_in=s_in, s_out=s_out,
+                        pad_id=-1)
 
     def restore():
         src.copy_(pristine)
+        if pristine_s is not None:
+            s_in.copy_(pristine_s)
 
     for _ in range(args.warmup):
         if pristine is not None:
@@ -251,7 +266,7 @@ def main():
         realign_ms, realign_n = sd.timing_query(sd.KERNEL_REALIGN)
     assert realign_n == K and verify_n == K
 
-    by = step_bytes(w, pad_in, W_in, n_acc, w_new, variant)
+    by = step_bytes(w, pad_in, W_in, n_acc, w_new, variant, token_row)
     realign_avg_ms = realign_ms / realign_n
     verify_avg_ms = verify_ms / verify_n
     realign_bytes = by["realign"] + by["posmask"]
@@ -265,8 +280,11 @@ def main():
 
     cpu = None
     if args.cpu_baseline_seconds > 0:
+        s_host = None
+        if token_row:
+            s_host = (pristine_s if pristine_s is not None else s_in).cpu().numpy()
         cpu = cpu_baseline(w, logits, draft, pad_in, W_in, pristine if pristine is not None else src,
-                           args.cpu_baseline_seconds)
+                           args.cpu_baseline_seconds, s_host)
         log(f"[bench] cpu baseline: {cpu['value']:.4f} steps/s ({cpu['sample']})")
 
     line = {
@@ -285,7 +303,7 @@ def main():
         "config": {
             "workload": describe(w, variant),
             "B": w.B, "k": w.k, "V": w.V, "L": w.L, "H": w.H, "D": w.D, "W_in": W_in, "w_new": w_new,
-            "variant": variant, "seed": args.seed,
+            "variant": variant, "seed": args.seed, "token_row": token_row,
             "step_GBps": round(step_gbs, 1),
             "step_bytes": realign_bytes + by["verify"],
             "verify_ms": round(verify_avg_ms, 5),
@@ -293,7 +311,7 @@ def main():
         },
         "roofline": {
             "bound": "hbm",
-            "kernel": "realign_" + variant + " (+ fused pos/mask)",
+            "kernel": "realign_" + variant + " (+ fused pos/mask" + (", token row)" if token_row else ")"),
             "achieved": round(achieved, 1),
             "peak": PEAK_HBM_GBS,
             "unit": "GB/s",

@@ -46,7 +46,7 @@
 extern "C" {
 #endif
 
-#define SPECDEC_ABI_VERSION 1
+#define SPECDEC_ABI_VERSION 2
 
 typedef enum {
   SPECDEC_OK = 0,
@@ -172,16 +172,44 @@ specdec_status_t specdec_build_posmask(const int32_t* pad_out, const int32_t* w_
                                        uint32_t* dev_status, void* stream);
 
 /*
- * The whole step on one stream: specdec_verify_greedy, then the realignment
- * and the position ids / mask (one fused launch).  Arguments as above;
- * pm_cap must be >= W_in + k + 1.  If `w_new_host` (host int32*) is not
- * NULL, the stream is synchronised and L' is copied there.
+ * Realignment of the token row S with the same offsets (Alg. 1, phase 3:
+ * S[i] <- S[i] + A[i] + B[i], then fresh left padding).
+ *
+ * Row i of S before the step holds pad_in[i] pad tokens and then c_i + 1
+ * tokens (the c_i cached tokens and the pending token), L + 1 columns in all.
+ * After the step row i holds pad_out[i] = w_new - (c_i + n_acc[i] + 1) copies
+ * of pad_id, those c_i + 1 tokens, then tokens[i][0 .. n_acc[i]] (the accepted
+ * drafts and the bonus token): w_new + 1 columns.  Columns beyond are left
+ * as they are.
+ *
+ *   s_in      int32 [B][s_in_stride], s_in_stride >= W_in - k (device).
+ *   s_out     int32 [B][s_out_stride], s_out_stride >= W_in + 1 (device);
+ *             s_out == s_in with equal strides: in place (the input's columns
+ *             [0, pad_in[i]) need not hold pad_id); otherwise the two must not
+ *             overlap.
+ *   tokens    int32 [B][k+1], pad_in, n_acc int32 [B], w_new int32 [1]: the
+ *             outputs of specdec_verify_greedy for this step.
+ */
+specdec_status_t specdec_realign_tokens(const int32_t* s_in, int64_t s_in_stride, int32_t* s_out,
+                                        int64_t s_out_stride, const int32_t* tokens,
+                                        const int32_t* pad_in, const int32_t* n_acc,
+                                        const int32_t* w_new, int32_t B, int32_t k, int32_t W_in,
+                                        int32_t pad_id, uint32_t* dev_status, void* stream);
+
+/*
+ * The whole step on one stream: specdec_verify_greedy, then one fused launch
+ * of the cache realignment, the position ids / mask and (when s_in is not
+ * NULL) the token row realignment.  Arguments as above; pm_cap must be
+ * >= W_in + k + 1.  If `w_new_host` (host int32*) is not NULL, the stream is
+ * synchronised and L' is copied there.
  */
 specdec_status_t specdec_step(const void* logits, int32_t dtype, const int32_t* draft,
                               const int32_t* pad_in, int32_t B, int32_t k, int32_t V,
                               int32_t W_in, const specdec_kv_t* src, const specdec_kv_t* dst,
                               int32_t* tokens, int32_t* n_acc, int32_t* bonus, int32_t* pad_out,
                               int32_t* w_new, int64_t* pos, uint8_t* mask, int64_t pm_cap,
+                              const int32_t* s_in, int64_t s_in_stride, int32_t* s_out,
+                              int64_t s_out_stride, int32_t pad_id,
                               void* workspace, size_t workspace_bytes, uint32_t* dev_status,
                               int32_t* w_new_host, void* stream);
 

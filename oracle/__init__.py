@@ -57,6 +57,8 @@ class Oracle:
         lib.oracle_realign_kv.restype = ctypes.c_int
         lib.oracle_posmask.argtypes = [P, i32, i32, i32, P, P, i64]
         lib.oracle_posmask.restype = ctypes.c_int
+        lib.oracle_realign_tokens.argtypes = [P, i64, P, i64, P, P, P, i32, i32, i32, i32, i32]
+        lib.oracle_realign_tokens.restype = ctypes.c_int
         self.lib = lib
 
 
@@ -183,6 +185,26 @@ def posmask(pad_out, w_new: int, k: int, pm_cap: int | None = None, oracle: Orac
     if rc:
         raise OracleError(f"oracle_posmask rejected its arguments (code {rc})")
     return pos, mask
+
+
+def realign_tokens(s_in, tokens, pad_in, n_acc, w_new: int, W_in: int, pad_id: int, out_stride=None,
+                   oracle: Oracle | None = None):
+    """Token row realignment of Alg. 1's phase 3: S[i] <- S[i] + A[i] + B[i], then
+    repadding to width L'+1.  s_in int32 [B][>= L+1]; returns int32
+    [B][out_stride or L'+1] (columns beyond L'+1 are zero)."""
+    si = _c(np.asarray(s_in), np.int32)
+    B = si.shape[0]
+    tk = _c(np.asarray(tokens), np.int32)
+    k = tk.shape[1] - 1
+    stride = out_stride if out_stride is not None else w_new + 1
+    out = np.zeros((B, stride), np.int32)
+    p = _c(np.asarray(pad_in).reshape(B), np.int32)
+    a = _c(np.asarray(n_acc).reshape(B), np.int32)
+    rc = _load(oracle).oracle_realign_tokens(_ptr(si), si.shape[1], _ptr(out), stride, _ptr(tk), _ptr(p), _ptr(a),
+                                             int(w_new), B, k, W_in, int(pad_id))
+    if rc:
+        raise OracleError(f"oracle_realign_tokens rejected its arguments (code {rc})")
+    return out
 
 
 def step(logits, dtype: str, draft, pad_in, kv, W_in: int, dst_cap=None,

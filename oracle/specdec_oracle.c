@@ -232,6 +232,54 @@ int oracle_realign_kv(const uint16_t* src, int64_t src_cap, uint16_t* dst, int64
   return OR_OK;
 }
 
+/* ---- token row realignment (Alg. 1, phase 3) -------------------------------- */
+
+/*
+ * The token row S of each sequence before the step holds p_i pad tokens and
+ * then c_i + 1 tokens: the c_i tokens whose entries are cached and the pending
+ * token (its entry is computed by the verify forward), so its width is L + 1.
+ * Phase 3 appends the accepted drafts and the bonus token (a_i = n_acc + 1
+ * tokens: tokens[i][0..n_acc], the target's predictions, which equal the
+ * accepted drafts) and repads every row to the new width L' + 1.
+ *
+ * s_in   int32 [B][s_in_stride], columns [0, L+1) read
+ * s_out  int32 [B][s_out_stride], columns [0, L'+1) written
+ * tokens int32 [B][k+1] from verification; pad_in, n_acc [B]; w_new = L'.
+ * s_in and s_out must not overlap.
+ */
+int oracle_realign_tokens(const int32_t* s_in, int64_t s_in_stride, int32_t* s_out, int64_t s_out_stride,
+                          const int32_t* tokens, const int32_t* pad_in, const int32_t* n_acc, int32_t w_new,
+                          int32_t B, int32_t k, int32_t W_in, int32_t pad_id) {
+  if (B < 0 || k < 0 || W_in < k + 1) return OR_EINVAL;
+  const int32_t L = W_in - (k + 1);
+  if (s_in_stride < (int64_t)L + 1 || s_out_stride < (int64_t)w_new + 1 || w_new < 0) return OR_EINVAL;
+  int32_t* row = (int32_t*)malloc(sizeof(int32_t) * (size_t)(L + k + 2));
+  if (!row) return OR_ENOMEM;
+  for (int32_t i = 0; i < B; ++i) {
+    if (pad_in[i] < 0 || pad_in[i] > L || n_acc[i] < 0 || n_acc[i] > k) {
+      free(row);
+      return OR_EINVAL;
+    }
+    const int32_t c = L - pad_in[i];
+    const int32_t a = n_acc[i] + 1;
+    if (c + a > w_new) {
+      free(row);
+      return OR_EINVAL;
+    }
+    int64_t n = 0;
+    /* unpad: the sequence's own tokens, the pending token included */
+    for (int32_t j = pad_in[i]; j <= L; ++j) row[n++] = s_in[(int64_t)i * s_in_stride + j];
+    /* append: accepted drafts, then the bonus token */
+    for (int32_t r = 0; r < a; ++r) row[n++] = tokens[(int64_t)i * (k + 1) + r];
+    /* repad to width L' + 1 */
+    const int64_t p_new = (int64_t)w_new + 1 - n;
+    for (int64_t j = 0; j < p_new; ++j) s_out[(int64_t)i * s_out_stride + j] = pad_id;
+    for (int64_t j = 0; j < n; ++j) s_out[(int64_t)i * s_out_stride + p_new + j] = row[j];
+  }
+  free(row);
+  return OR_OK;
+}
+
 /* ---- position ids and attention mask (I2) ---------------------------------- */
 
 /*

@@ -191,6 +191,25 @@ specdec_status_t check_realign_args(const specdec_kv_t* src, const specdec_kv_t*
   return SPECDEC_OK;
 }
 
+specdec_status_t check_token_args(const int32_t* s_in, int64_t s_in_stride, const int32_t* s_out,
+                                  int64_t s_out_stride, int32_t B, int32_t k, int32_t W_in) {
+  if (B == 0) return SPECDEC_OK;
+  if (!s_in || !s_out) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "NULL token row");
+  if (!aligned(s_in, 4) || !aligned(s_out, 4)) return fail(SPECDEC_ERR_UNSUPPORTED, "token row not 4-byte aligned");
+  if (s_in_stride < static_cast<int64_t>(W_in) - k || s_in_stride > SPECDEC_MAX_WIDTH + 1)
+    return fail(SPECDEC_ERR_INVALID_ARGUMENT, "s_in_stride=%lld < W_in-k=%d", (long long)s_in_stride, W_in - k);
+  if (s_out_stride < static_cast<int64_t>(W_in) + 1 || s_out_stride > SPECDEC_MAX_WIDTH + 1)
+    return fail(SPECDEC_ERR_INVALID_ARGUMENT, "s_out_stride=%lld < W_in+1=%d", (long long)s_out_stride, W_in + 1);
+  const uintptr_t a0 = reinterpret_cast<uintptr_t>(s_in), b0 = reinterpret_cast<uintptr_t>(s_out);
+  const uintptr_t a1 = a0 + static_cast<uintptr_t>(B) * s_in_stride * 4, b1 = b0 + static_cast<uintptr_t>(B) * s_out_stride * 4;
+  if (a0 == b0) {
+    if (s_in_stride != s_out_stride) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "in-place token row needs equal strides");
+  } else if (a0 < b1 && b0 < a1) {
+    return fail(SPECDEC_ERR_INVALID_ARGUMENT, "token rows overlap without being the same buffer");
+  }
+  return SPECDEC_OK;
+}
+
 specdec_status_t check_posmask_args(const int32_t* pad_out, const int32_t* w_new, int32_t B, int32_t k,
                                     const int64_t* pos, const uint8_t* mask, int64_t pm_cap) {
   if (B < 0 || B > SPECDEC_MAX_B) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "B=%d outside [0,%d]", B, SPECDEC_MAX_B);
@@ -288,12 +307,48 @@ specdec_status_t specdec_build_posmask(const int32_t* pad_out, const int32_t* w_
   return ok();
 }
 
+specdec_status_t specdec_realign_tokens(const int32_t* s_in, int64_t s_in_stride, int32_t* s_out,
+                                        int64_t s_out_stride, const int32_t* tokens, const int32_t* pad_in,
+                                        const int32_t* n_acc, const int32_t* w_new, int32_t B, int32_t k,
+                                        int32_t W_in, int32_t pad_id, uint32_t* dev_status, void* stream) {
+  if (B < 0 || B > SPECDEC_MAX_B) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "B=%d outside [0,%d]", B, SPECDEC_MAX_B);
+  if (k < 0 || k > SPECDEC_MAX_K) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "k=%d outside [0,%d]", k, SPECDEC_MAX_K);
+  if (W_in < k + 1 || W_in > SPECDEC_MAX_WIDTH)
+    return fail(SPECDEC_ERR_INVALID_ARGUMENT, "W_in=%d outside [k+1=%d, %d]", W_in, k + 1, SPECDEC_MAX_WIDTH);
+  specdec_status_t s = check_token_args(s_in, s_in_stride, s_out, s_out_stride, B, k, W_in);
+  if (s) return s;
+  if (B == 0) return ok();
+  if (!tokens || !pad_in || !n_acc || !w_new) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "NULL tokens / pad_in / n_acc / w_new");
+  if (!aligned(tokens, 4) || !aligned(pad_in, 4) || !aligned(n_acc, 4) || !aligned(w_new, 4))
+    return fail(SPECDEC_ERR_UNSUPPORTED, "int32 tensor not 4-byte aligned");
+  if (dev_status && !aligned(dev_status, 4)) return fail(SPECDEC_ERR_UNSUPPORTED, "dev_status not 4-byte aligned");
+  specdec::RealignLaunch p{};
+  p.B = B;
+  p.k = k;
+  p.W_in = W_in;
+  p.pad_in = pad_in;
+  p.n_acc = n_acc;
+  p.w_new = w_new;
+  p.dev_status = dev_status;
+  p.s_in = s_in;
+  p.s_out = s_out;
+  p.s_in_stride = s_in_stride;
+  p.s_out_stride = s_out_stride;
+  p.tokens = tokens;
+  p.pad_id = pad_id;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  hipError_t e = specdec::launch_tokens(p, st);
+  if (e != hipSuccess) return hip_fail(e, "token row launch");
+  return ok();
+}
+
 specdec_status_t specdec_step(const void* logits, int32_t dtype, const int32_t* draft, const int32_t* pad_in,
                               int32_t B, int32_t k, int32_t V, int32_t W_in, const specdec_kv_t* src,
                               const specdec_kv_t* dst, int32_t* tokens, int32_t* n_acc, int32_t* bonus,
                               int32_t* pad_out, int32_t* w_new, int64_t* pos, uint8_t* mask, int64_t pm_cap,
-                              void* workspace, size_t workspace_bytes, uint32_t* dev_status, int32_t* w_new_host,
-                              void* stream) {
+                              const int32_t* s_in, int64_t s_in_stride, int32_t* s_out, int64_t s_out_stride,
+                              int32_t pad_id, void* workspace, size_t workspace_bytes, uint32_t* dev_status,
+                              int32_t* w_new_host, void* stream) {
   specdec_status_t s = check_verify_args(logits, dtype, draft, pad_in, B, k, V, W_in, tokens, n_acc, bonus,
                                          pad_out, w_new, workspace, workspace_bytes);
   if (s) return s;
@@ -305,6 +360,10 @@ specdec_status_t specdec_step(const void* logits, int32_t dtype, const int32_t* 
   if (s) return s;
   if (B > 0 && pm_cap < static_cast<int64_t>(W_in) + k + 1)
     return fail(SPECDEC_ERR_INVALID_ARGUMENT, "pm_cap=%lld < W_in+k+1=%d", (long long)pm_cap, W_in + k + 1);
+  if (s_in || s_out) {
+    s = check_token_args(s_in, s_in_stride, s_out, s_out_stride, B, k, W_in);
+    if (s) return s;
+  }
   if (dev_status && !aligned(dev_status, 4)) return fail(SPECDEC_ERR_UNSUPPORTED, "dev_status not 4-byte aligned");
   if (B == 0) return ok();
   hipStream_t st = static_cast<hipStream_t>(stream);
@@ -332,6 +391,12 @@ specdec_status_t specdec_step(const void* logits, int32_t dtype, const int32_t* 
   rp.mask = mask;
   rp.pm_cap = pm_cap;
   rp.pad_out = pad_out;
+  rp.s_in = s_in;
+  rp.s_out = s_out;
+  rp.s_in_stride = s_in_stride;
+  rp.s_out_stride = s_out_stride;
+  rp.tokens = tokens;
+  rp.pad_id = pad_id;
   e = timed(SPECDEC_KERNEL_REALIGN, st, [&] { return specdec::launch_realign(rp, st); });
   if (e != hipSuccess) return hip_fail(e, "realign launch");
   if (w_new_host) {

@@ -42,6 +42,12 @@ struct RealignLaunch {
   uint8_t* mask;
   int64_t pm_cap;
   const int32_t* pad_out;    // verify's pad_out; used only by the fused pos/mask blocks
+  // token row S (s_in == nullptr: none); s_out == s_in: in place
+  const int32_t* s_in;
+  int32_t* s_out;
+  int64_t s_in_stride, s_out_stride;
+  const int32_t* tokens;
+  int32_t pad_id;
 };
 
 struct PosmaskLaunch {
@@ -66,6 +72,8 @@ int64_t realign_grid_blocks(int64_t nspans, int64_t W_in, int32_t D, bool in_pla
 hipError_t launch_verify(const VerifyLaunch& p, hipStream_t stream);
 hipError_t launch_realign(const RealignLaunch& p, hipStream_t stream);
 hipError_t launch_posmask(const PosmaskLaunch& p, hipStream_t stream);
+// Token row only (RealignLaunch's cache fields are ignored).
+hipError_t launch_tokens(const RealignLaunch& p, hipStream_t stream);
 hipError_t launch_zero(void* ptr, size_t bytes, hipStream_t stream);
 
 }  // namespace specdec

@@ -316,12 +316,20 @@ struct RealignArgs {
   uint32_t chunks;                       // workgroups per span (out of place)
   uint32_t realign_blocks;               // realign workgroups in this launch
   uint32_t span_base;                    // first span of this launch
-  // position ids / mask blocks after the realign blocks
+  // workgroups before the realign ones: position ids / mask, then the token row
+  uint32_t extra_blocks;
+  uint32_t pm_blocks;
   int64_t* pos;
   uint8_t* mask;
   const int32_t* pad_out;
   int64_t pm_cap;
   uint32_t pm_col_blocks;
+  const int32_t* s_in;                   // token row S [B][s_in_stride]
+  int32_t* s_out;                        // [B][s_out_stride]; == s_in: in place
+  int64_t s_in_stride, s_out_stride;
+  const int32_t* tokens;                 // [B][k+1] predictions from verification
+  int32_t pad_id;
+  uint32_t tok_col_blocks;               // workgroups per token row (1 in place)
 };
 
 struct RowGeom {
@@ -380,6 +388,87 @@ __device__ void posmask_block(uint32_t blk, int64_t* pos, uint8_t* mask, const i
   }
 }
 
+// Token row S of one sequence (Alg. 1, phase 3): the c_i + 1 tokens of the
+// row (its cached tokens and the pending token) move from column pad_in to
+// pad_out, the accepted drafts and the bonus token (the predictions
+// tokens[0..n_acc]) follow them, and columns [0, pad_out) hold pad_id; the
+// new row is L' + 1 wide.  Out of place a workgroup writes 4*kTpb columns of
+// one row; in place one workgroup walks the whole row in the direction of its
+// shift and writes the padding and the appended tokens after a barrier.
+template <int kTpb>
+__device__ void token_block(const RealignArgs& a, uint32_t blk) {
+  const uint32_t row = blk / a.tok_col_blocks;
+  const uint32_t cb = blk - row * a.tok_col_blocks;
+  const int32_t L = a.W_in - (a.k + 1);
+  const int32_t w = load_invariant(a.w_new);
+  const int32_t p = load_invariant(a.pad_in + row);
+  const int32_t n = load_invariant(a.n_acc + row);
+  uint32_t err = 0u;
+  if (p < 0 || p > L) err |= kBadPadIn;
+  if (n < 0 || n > a.k) err |= kBadAccept;
+  const int32_t c = L - p;
+  if (!err && (w < 1 || w > a.W_in || c + n + 1 > w)) err |= kBadWidth;
+  if (err) {
+    if (cb == 0 && threadIdx.x == 0 && a.dev_status) atomicOr(a.dev_status, err);
+    return;
+  }
+  const int64_t po = static_cast<int64_t>(w) - (c + n + 1);   // new padding
+  const int64_t keep_end = po + c + 1;                          // end of the moved tokens
+  const int64_t width = static_cast<int64_t>(w) + 1;
+  const int32_t* src = a.s_in + static_cast<int64_t>(row) * a.s_in_stride;
+  int32_t* dst = a.s_out + static_cast<int64_t>(row) * a.s_out_stride;
+  const int32_t* tk = a.tokens + static_cast<int64_t>(row) * (a.k + 1);
+  if (a.s_in != a.s_out) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int64_t j = static_cast<int64_t>(cb) * (4 * kTpb) + q * kTpb + threadIdx.x;
+      if (j < width) {
+        int32_t v;
+        if (j < po) v = a.pad_id;
+        else if (j < keep_end) v = src[j - po + p];
+        else v = tk[j - keep_end];
+        dst[j] = v;
+      }
+    }
+    return;
+  }
+  // in place
+  const int64_t nt = c + 1;
+  const int64_t shift = po - p;
+  constexpr int64_t kChunk = 4 * kTpb;
+  if (shift != 0) {
+    for (int64_t it = 0; it < nt; it += kChunk) {
+      // right shifts walk from the top, left shifts from the bottom
+      const int64_t lo = shift > 0 ? nt - it - kChunk : it;
+      int32_t v[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        int64_t u = lo + q * kTpb + threadIdx.x;
+        u = u < 0 ? 0 : (u >= nt ? nt - 1 : u);
+        v[q] = dst[p + u];
+      }
+      asm volatile("" ::"v"(v[0]), "v"(v[1]), "v"(v[2]), "v"(v[3]));
+      __syncthreads();
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int64_t u = lo + q * kTpb + threadIdx.x;
+        if (u >= 0 && u < nt) dst[po + u] = v[q];
+      }
+    }
+    __syncthreads();
+  }
+  for (int64_t j = threadIdx.x; j < po; j += kTpb) dst[j] = a.pad_id;
+  for (int64_t j = keep_end + threadIdx.x; j < width; j += kTpb) dst[j] = tk[j - keep_end];
+}
+
+template <int kTpb>
+__device__ __forceinline__ void extra_block(const RealignArgs& a, uint32_t b) {
+  if (b < a.pm_blocks)
+    posmask_block<kTpb>(b, a.pos, a.mask, a.pad_out, a.w_new, a.k, a.pm_cap, a.pm_col_blocks, a.dev_status);
+  else
+    token_block<kTpb>(a, b - a.pm_blocks);
+}
+
 // Out of place: every workgroup moves kPieces pieces of kTpb 16-byte vectors
 // (one per lane) of one span's output, the pieces kSplit vectors apart.  The
 // output of a span is cut into groups of kPieces*kSplit vectors; group g is
@@ -389,12 +478,11 @@ __device__ void posmask_block(uint32_t blk, int64_t* pos, uint8_t* mask, const i
 template <int kPieces, int kTpb, int kSplit, int kNt>
 __global__ __launch_bounds__(kTpb) void realign_oop_kernel(RealignArgs a) {
   static_assert(kSplit % kTpb == 0, "a group is a whole number of workgroups");
-  const uint32_t b = blockIdx.x;
-  if (b >= a.realign_blocks) {
-    posmask_block<kTpb>(b - a.realign_blocks, a.pos, a.mask, a.pad_out, a.w_new, a.k, a.pm_cap, a.pm_col_blocks,
-                        a.dev_status);
+  if (blockIdx.x < a.extra_blocks) {
+    extra_block<kTpb>(a, blockIdx.x);
     return;
   }
+  const uint32_t b = blockIdx.x - a.extra_blocks;
   const uint32_t rel = b / a.chunks;
   const uint32_t sub = b - rel * a.chunks;            // workgroup within the span
   const uint32_t span = a.span_base + rel;
@@ -490,13 +578,11 @@ __device__ __forceinline__ void move_chunk(u32x4* base, int64_t from, int64_t to
 
 template <int kVec, int kTpb, int kNt>
 __global__ __launch_bounds__(kTpb) void realign_inplace_kernel(RealignArgs a) {
-  const uint32_t b = blockIdx.x;
-  if (b >= a.realign_blocks) {
-    posmask_block<kTpb>(b - a.realign_blocks, a.pos, a.mask, a.pad_out, a.w_new, a.k, a.pm_cap, a.pm_col_blocks,
-                        a.dev_status);
+  if (blockIdx.x < a.extra_blocks) {
+    extra_block<kTpb>(a, blockIdx.x);
     return;
   }
-  const uint32_t span = a.span_base + b;
+  const uint32_t span = a.span_base + (blockIdx.x - a.extra_blocks);
   const int row = static_cast<int>((span / static_cast<uint32_t>(a.H)) % static_cast<uint32_t>(a.B));
   RowGeom g;
   const uint32_t err = row_geometry(a, row, g);
@@ -532,6 +618,10 @@ __global__ __launch_bounds__(kThreads) void posmask_kernel(int64_t* pos, uint8_t
                                                            int32_t k, int64_t pm_cap, uint32_t col_blocks,
                                                            uint32_t* dev_status) {
   posmask_block<kThreads>(blockIdx.x, pos, mask, pad_out, w_new, k, pm_cap, col_blocks, dev_status);
+}
+
+__global__ __launch_bounds__(kThreads) void tokens_kernel(RealignArgs a) {
+  token_block<kThreads>(a, blockIdx.x);
 }
 
 __global__ __launch_bounds__(kThreads) void zero_kernel(uint4* p16, int64_t n16, uint8_t* tail, int64_t ntail) {
@@ -598,8 +688,22 @@ hipError_t launch_verify(const VerifyLaunch& p, hipStream_t stream) {
   return hipGetLastError();
 }
 
+static void fill_token_args(RealignArgs& a, const RealignLaunch& p, int tpb) {
+  a.s_in = p.s_in;
+  a.s_out = p.s_out;
+  a.s_in_stride = p.s_in_stride;
+  a.s_out_stride = p.s_out_stride;
+  a.tokens = p.tokens;
+  a.pad_id = p.pad_id;
+  a.tok_col_blocks = 0;
+  if (p.s_in) {
+    const int64_t width = static_cast<int64_t>(p.W_in) + 1;   // L' + 1 <= W_in + 1
+    a.tok_col_blocks = p.s_in == p.s_out ? 1u : static_cast<uint32_t>((width + 4 * tpb - 1) / (4 * tpb));
+  }
+}
+
 hipError_t launch_realign(const RealignLaunch& p, hipStream_t stream) {
-  RealignArgs a;
+  RealignArgs a{};
   a.src = static_cast<const u32x4*>(p.src);
   a.dst = static_cast<u32x4*>(p.dst);
   a.vpc = p.D / 8;
@@ -626,6 +730,9 @@ hipError_t launch_realign(const RealignLaunch& p, hipStream_t stream) {
     a.pm_col_blocks = static_cast<uint32_t>((bound + 4 * tpb - 1) / (4 * tpb));
     pm_blocks = static_cast<int64_t>(a.pm_col_blocks) * p.B;
   }
+  fill_token_args(a, p, tpb);
+  const int64_t tok_blocks = static_cast<int64_t>(a.tok_col_blocks) * p.B;
+  const int64_t extra = pm_blocks + tok_blocks;
   const int64_t chunks = p.in_place ? 1 : realign_grid_blocks(1, p.W_in, p.D, false);
   a.chunks = static_cast<uint32_t>(chunks);
   // one dispatch holds fewer than 2^32 work-items: split the spans over
@@ -636,16 +743,18 @@ hipError_t launch_realign(const RealignLaunch& p, hipStream_t stream) {
     const long long v = std::atoll(env);
     if (v > 0 && v < max_items) max_items = v;
   }
-  const int64_t max_blocks = (max_items / tpb) - pm_blocks;
+  const int64_t max_blocks = (max_items / tpb) - extra;
   const int64_t spans_per_launch = max_blocks / chunks;
   if (spans_per_launch < 1) return hipErrorInvalidConfiguration;
   const dim3 block(tpb);
   for (int64_t s0 = 0; s0 < nspans || (nspans == 0 && s0 == 0); s0 += spans_per_launch) {
     const int64_t ns = nspans - s0 < spans_per_launch ? nspans - s0 : spans_per_launch;
-    const bool last = s0 + ns >= nspans;
+    const bool first = s0 == 0;
     a.span_base = static_cast<uint32_t>(s0);
     a.realign_blocks = static_cast<uint32_t>(ns * chunks);
-    const int64_t blocks = ns * chunks + (last ? pm_blocks : 0);
+    a.extra_blocks = first ? static_cast<uint32_t>(extra) : 0u;
+    a.pm_blocks = first ? static_cast<uint32_t>(pm_blocks) : 0u;
+    const int64_t blocks = ns * chunks + (first ? extra : 0);
     if (blocks == 0) break;
     const dim3 grid(static_cast<uint32_t>(blocks));
     if (p.in_place)
@@ -657,6 +766,22 @@ hipError_t launch_realign(const RealignLaunch& p, hipStream_t stream) {
     if (nspans == 0) break;
   }
   return hipSuccess;
+}
+
+hipError_t launch_tokens(const RealignLaunch& p, hipStream_t stream) {
+  RealignArgs a{};
+  a.B = p.B;
+  a.k = p.k;
+  a.W_in = p.W_in;
+  a.pad_in = p.pad_in;
+  a.n_acc = p.n_acc;
+  a.w_new = p.w_new;
+  a.dev_status = p.dev_status;
+  fill_token_args(a, p, kThreads);
+  const int64_t blocks = static_cast<int64_t>(a.tok_col_blocks) * p.B;
+  if (blocks == 0) return hipSuccess;
+  hipLaunchKernelGGL(tokens_kernel, dim3(static_cast<uint32_t>(blocks)), dim3(kThreads), 0, stream, a);
+  return hipGetLastError();
 }
 
 int64_t realign_grid_blocks(int64_t nspans, int64_t W_in, int32_t D, bool in_place) {

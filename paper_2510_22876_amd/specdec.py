@@ -23,7 +23,8 @@ DEV_BAD_PAD_IN, DEV_BAD_ACCEPT, DEV_BAD_WIDTH, DEV_BAD_PAD_OUT = 1, 2, 4, 8
 
 EXPORTED = (
     "specdec_abi_version", "specdec_last_error", "specdec_workspace_bytes", "specdec_workspace_init",
-    "specdec_verify_greedy", "specdec_realign_kv", "specdec_build_posmask", "specdec_step",
+    "specdec_verify_greedy", "specdec_realign_kv", "specdec_build_posmask", "specdec_realign_tokens",
+    "specdec_step",
     "specdec_timing_enable", "specdec_timing_reset", "specdec_timing_query",
 )
 
@@ -54,12 +55,13 @@ def _load(path: Path = _LIB_PATH) -> ctypes.CDLL:
     lib.specdec_verify_greedy.argtypes = [P, i32, P, P, i32, i32, i32, i32, P, P, P, P, P, P, sz, P, P]
     lib.specdec_realign_kv.argtypes = [pKV, pKV, i32, i32, P, P, P, P, P]
     lib.specdec_build_posmask.argtypes = [P, P, i32, i32, P, P, i64, P, P]
+    lib.specdec_realign_tokens.argtypes = [P, i64, P, i64, P, P, P, P, i32, i32, i32, i32, P, P]
     lib.specdec_step.argtypes = [P, i32, P, P, i32, i32, i32, i32, pKV, pKV, P, P, P, P, P, P, P, i64,
-                                 P, sz, P, P, P]
+                                 P, i64, P, i64, i32, P, sz, P, P, P]
     lib.specdec_timing_enable.argtypes = [i32]
     lib.specdec_timing_query.argtypes = [i32, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)]
     for name in ("specdec_workspace_init", "specdec_verify_greedy", "specdec_realign_kv",
-                 "specdec_build_posmask", "specdec_step", "specdec_timing_enable",
+                 "specdec_build_posmask", "specdec_realign_tokens", "specdec_step", "specdec_timing_enable",
                  "specdec_timing_reset", "specdec_timing_query"):
         getattr(lib, name).restype = ctypes.c_int
     return lib
@@ -187,9 +189,26 @@ def specdec_build_posmask(pad_out, w_new, k: int, pos, mask, dev_status=None, st
                                      _p(dev_status), _stream(stream)))
 
 
+def specdec_realign_tokens(s_in, s_out, tokens, pad_in, n_acc, w_new, W_in: int, pad_id: int,
+                           dev_status=None, stream=None) -> None:
+    B, kp1 = tokens.shape
+    _req("tokens", tokens, (B, kp1), torch.int32)
+    _req("s_in", s_in, (B, s_in.shape[1]), torch.int32)
+    _req("s_out", s_out, (B, s_out.shape[1]), torch.int32)
+    _req("pad_in", pad_in, (B,), torch.int32)
+    _req("n_acc", n_acc, (B,), torch.int32)
+    _req("w_new", w_new, (1,), torch.int32)
+    _req("dev_status", dev_status, (1,), torch.int32, optional=True)
+    _check(lib.specdec_realign_tokens(_p(s_in), s_in.shape[1], _p(s_out), s_out.shape[1], _p(tokens), _p(pad_in),
+                                      _p(n_acc), _p(w_new), B, kp1 - 1, W_in, pad_id, _p(dev_status),
+                                      _stream(stream)))
+
+
 def specdec_step(logits, draft, pad_in, W_in: int, src, dst, tokens, n_acc, bonus, pad_out, w_new,
-                 pos, mask, workspace, dev_status=None, sync_w_new: bool = False, stream=None):
-    """The fused step; returns L' as a Python int when ``sync_w_new``."""
+                 pos, mask, workspace, dev_status=None, sync_w_new: bool = False, stream=None,
+                 s_in=None, s_out=None, pad_id: int = 0):
+    """The fused step (with the token row S when ``s_in`` / ``s_out`` are
+    given); returns L' as a Python int when ``sync_w_new``."""
     B, kp1, V = logits.shape
     _check_verify(logits, draft, pad_in, tokens, n_acc, bonus, pad_out, w_new, workspace, dev_status)
     s = kv_desc(src)
@@ -198,11 +217,18 @@ def specdec_step(logits, draft, pad_in, W_in: int, src, dst, tokens, n_acc, bonu
         raise ValueError("cache rows differ from logit rows")
     _req("pos", pos, (B, pos.shape[1]), torch.int64)
     _req("mask", mask, (B, pos.shape[1]), torch.uint8)
+    if (s_in is None) != (s_out is None):
+        raise ValueError("give both s_in and s_out, or neither")
+    if s_in is not None:
+        _req("s_in", s_in, (B, s_in.shape[1]), torch.int32)
+        _req("s_out", s_out, (B, s_out.shape[1]), torch.int32)
     host = ctypes.c_int32(-1)
     _check(lib.specdec_step(
         _p(logits), DTYPE_OF[logits.dtype], _p(draft), _p(pad_in), B, kp1 - 1, V, W_in,
         ctypes.byref(s), ctypes.byref(d), _p(tokens), _p(n_acc), _p(bonus), _p(pad_out), _p(w_new),
-        _p(pos), _p(mask), pos.shape[1], _p(workspace), workspace.numel() * workspace.element_size(),
+        _p(pos), _p(mask), pos.shape[1], _p(s_in), s_in.shape[1] if s_in is not None else 0, _p(s_out),
+        s_out.shape[1] if s_out is not None else 0, pad_id,
+        _p(workspace), workspace.numel() * workspace.element_size(),
         _p(dev_status), ctypes.byref(host) if sync_w_new else None, _stream(stream)))
     return host.value if sync_w_new else None
 

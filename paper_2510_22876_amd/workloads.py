@@ -30,7 +30,7 @@ import numpy as np
 import torch
 
 # sub-stream tags
-_T_PROMPT, _T_ACCEPT, _T_LOGITS, _T_PLANT, _T_DRAFT, _T_TIES, _T_KV, _T_WINDOW = range(1, 9)
+_T_PROMPT, _T_ACCEPT, _T_LOGITS, _T_PLANT, _T_DRAFT, _T_TIES, _T_KV, _T_WINDOW, _T_TOKENS = range(1, 10)
 
 DT_CODE = {"f32": 0, "bf16": 1, "f16": 2}
 TORCH_DT = {"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}
@@ -310,3 +310,18 @@ def write_window(kvt: torch.Tensor, w: Workload, W0: int, pad: np.ndarray, seed:
                 vals = torch.randn((B, H, k + 1, D), generator=g, device=device,
                                    dtype=torch.float32).to(torch.bfloat16)
             kvt[l, kvi, :, :, W0:W0 + k + 1, :] = vals
+
+
+def make_token_rows(w: Workload, pad_in: np.ndarray, W_in: int, stride: int, seed: int = 0, pad_id: int = -1,
+                    device="cpu") -> torch.Tensor:
+    """Token row S int32 [B][stride]: row i holds pad_in[i] copies of pad_id,
+    then c_i + 1 tokens (its cached tokens and the pending token), L + 1
+    columns in all, L = W_in - (k+1); later columns hold pad_id.  Tokens are
+    uniform in [0, V)."""
+    L = W_in - (w.k + 1)
+    r = _rng(seed, _T_TOKENS)
+    rows = np.full((w.B, stride), pad_id, dtype=np.int32)
+    for i in range(w.B):
+        p = int(pad_in[i])
+        rows[i, p:L + 1] = r.integers(0, max(w.V, 1), size=L + 1 - p)
+    return torch.as_tensor(rows, device=device)

@@ -15,6 +15,8 @@ from tests import checker
 SENT_KV = 0x7FC1        # a bf16 NaN pattern: marks destination columns the step must not touch
 SENT_POS = -7
 SENT_MASK = 0xAB
+SENT_TOK = -555
+PAD_ID = -2
 
 
 def say(*a):
@@ -59,9 +61,11 @@ def alloc_outputs(B, k, V, pm_cap, device="cuda"):
 
 def run_gpu(w: wl.Workload, seed: int = 0, variant: str = "oop", api: str = "step",
             tagged: bool = False, keep_src: bool = True, dst_cap: int | None = None,
-            logits=None, draft=None, pad_in=None, W_in=None, src=None) -> StepResult:
+            logits=None, draft=None, pad_in=None, W_in=None, src=None, tokens: str | None = None,
+            s_rows=None) -> StepResult:
     """One step of the HIP path.  ``api`` = "step" (fused) or "split"
-    (verify, realign and posmask entry points in turn)."""
+    (verify, realign and posmask entry points in turn).  ``tokens`` = "oop" or
+    "inplace" also realigns the token row S (given as ``s_rows`` or drawn)."""
     from paper_2510_22876_amd import specdec as sd
     say(f"workload={w.name} B={w.B} k={w.k} V={w.V} L={w.L} H={w.H} D={w.D} seed={seed} "
         f"variant={variant} api={api} tagged={tagged}")
@@ -84,20 +88,49 @@ def run_gpu(w: wl.Workload, seed: int = 0, variant: str = "oop", api: str = "ste
     pm_cap = W_in + w.k + 1 + 3
     o = alloc_outputs(w.B, w.k, w.V, pm_cap)
     pad_t = torch.as_tensor(np.asarray(pad_in, np.int32), device="cuda")
+    s_in = s_out = s_before = None
+    if tokens is not None:
+        stride = cap + 2
+        if s_rows is None:
+            s_rows = wl.make_token_rows(w, pad_in, W_in, stride, seed, PAD_ID, device="cuda")
+        s_in = s_rows
+        s_before = s_rows.cpu().numpy()
+        if tokens == "oop":
+            s_out = torch.full((w.B, W_in + 1 + 5), SENT_TOK, dtype=torch.int32, device="cuda")
+        else:
+            s_out = s_rows
     if api == "step":
         sd.specdec_step(logits, draft, pad_t, W_in, src, dst, o.tokens, o.n_acc, o.bonus, o.pad_out,
-                        o.w_new, o.pos, o.mask, o.workspace, o.dev_status)
+                        o.w_new, o.pos, o.mask, o.workspace, o.dev_status, s_in=s_in, s_out=s_out, pad_id=PAD_ID)
     else:
         sd.specdec_verify_greedy(logits, draft, pad_t, W_in, o.tokens, o.n_acc, o.bonus, o.pad_out, o.w_new,
                                  o.workspace, o.dev_status)
         sd.specdec_realign_kv(src, dst, w.k, W_in, pad_t, o.n_acc, o.w_new, o.dev_status)
         sd.specdec_build_posmask(o.pad_out, o.w_new, w.k, o.pos, o.mask, o.dev_status)
+        if tokens is not None:
+            sd.specdec_realign_tokens(s_in, s_out, o.tokens, pad_t, o.n_acc, o.w_new, W_in, PAD_ID, o.dev_status)
     torch.cuda.synchronize()
     out = dict(tokens=o.tokens.cpu().numpy(), n_acc=o.n_acc.cpu().numpy(), bonus=o.bonus.cpu().numpy(),
                pad_out=o.pad_out.cpu().numpy(), w_new=int(o.w_new.cpu()[0]), pos=o.pos.cpu().numpy(),
                mask=o.mask.cpu().numpy(), dev_status=int(o.dev_status.cpu()[0]))
-    return StepResult(w, W_in, cap, np.asarray(pad_in, np.int32), logits, draft, before, dst, out, pm_cap,
-                      variant=variant)
+    r = StepResult(w, W_in, cap, np.asarray(pad_in, np.int32), logits, draft, before, dst, out, pm_cap,
+                   variant=variant)
+    if tokens is not None:
+        r.extra.update(s_before=s_before, s_out=s_out.cpu().numpy(), s_out_dev=s_out, tokens=tokens)
+    return r
+
+
+def check_tokens_vs_oracle(r: StepResult, v):
+    """The token row against the oracle; out of place, columns beyond w_new+1
+    stay untouched."""
+    if "s_before" not in r.extra:
+        return
+    W = v["w_new"]
+    exp = oracle.realign_tokens(r.extra["s_before"], v["tokens"], r.pad_in, v["n_acc"], W, r.W_in, PAD_ID)
+    got = r.extra["s_out"]
+    assert np.array_equal(got[:, :W + 1], exp[:, :W + 1]), "token row differs from the oracle"
+    if r.extra["tokens"] == "oop":
+        assert np.all(got[:, W + 1:] == SENT_TOK), "token row written beyond w_new + 1"
 
 
 def check_verify_vs_oracle(r: StepResult):

@@ -386,11 +386,65 @@ def pin_golden_worked_example(o=None):
     for i in range(B):
         assert list(pos[i]) == g[f"pos_row{i}"]
         assert list(mask[i]) == g[f"mask_row{i}"]
+    s_in = np.asarray([g[f"s_in_row{i}"] for i in range(B)], np.int32)
+    s_out = oracle.realign_tokens(s_in, v["tokens"], pad_in, v["n_acc"], v["w_new"], W_in, g["pad_id"][0], oracle=o)
+    for i in range(B):
+        assert list(s_out[i]) == g[f"s_out_row{i}"]
+
+
+# ---- token row (Alg. 1, phase 3) -------------------------------------------------------
+
+def pin_tokens_replay(o=None):
+    """Each row alone: its own tokens (cached + pending) followed by the accepted
+    drafts D[i][:n_acc] and the bonus B[i] (Alg. 1's append); the realigned
+    row must be that list after pad_out[i] pads, with the same padding as the
+    cache (I1 shared by S and the cache)."""
+    for w in SMALL_WORKLOADS:
+        for seed in range(3):
+            n, W_in, pad_in, cap = wl.initial_geometry(w, seed=seed)
+            L = W_in - (w.k + 1)
+            logits, draft, *_ = wl.logits_and_drafts(w, seed=seed)
+            d = draft.numpy()
+            v = oracle.verify(logits, w.logit_dtype, d, pad_in, W_in, oracle=o)
+            s_in = wl.make_token_rows(w, pad_in, W_in, W_in + 2, seed=seed, pad_id=-3).numpy()
+            out = oracle.realign_tokens(s_in, v["tokens"], pad_in, v["n_acc"], v["w_new"], W_in, -3, oracle=o)
+            assert out.shape[1] == v["w_new"] + 1
+            for i in range(w.B):
+                seq = list(s_in[i, pad_in[i]:L + 1])
+                seq += list(d[i, : v["n_acc"][i]]) + [v["bonus"][i]]
+                p = v["w_new"] + 1 - len(seq)
+                assert p == v["pad_out"][i], "token row and cache disagree on the padding"
+                assert list(out[i, :p]) == [-3] * p
+                assert list(out[i, p:]) == seq, (w.name, seed, i)
+
+
+def pin_tokens_chain(o=None):
+    """16 chained steps: the token row, grown by Alg. 1's append each step,
+    stays equal to a per-row list model and keeps exactly one more token than
+    the cache (the pending token), left-aligned to the same padding."""
+    w = _small("vicuna7b", V=997, L=1, H=1, D=8, prompt=("uniform", 3, 30), extra_cap=16 * 6)
+    n, W_in, pad_in, cap = wl.initial_geometry(w)
+    L = W_in - (w.k + 1)
+    s = wl.make_token_rows(w, pad_in, W_in, cap + 2, pad_id=-1).numpy()
+    model = [list(s[i, pad_in[i]:L + 1]) for i in range(w.B)]
+    pad, W0 = pad_in.copy(), L
+    for step in range(16):
+        Wi = W0 + w.k + 1
+        logits, draft, *_ = wl.logits_and_drafts(w, seed=0, step=step)
+        d = draft.numpy()
+        v = oracle.verify(logits, w.logit_dtype, d, pad, Wi, oracle=o)
+        s = oracle.realign_tokens(s, v["tokens"], pad, v["n_acc"], v["w_new"], Wi, -1, out_stride=cap + 2, oracle=o)
+        for i in range(w.B):
+            model[i] += list(d[i, : v["n_acc"][i]]) + [v["bonus"][i]]
+            po = v["pad_out"][i]
+            assert list(s[i, po: v["w_new"] + 1]) == model[i]
+            assert len(model[i]) == (v["w_new"] - po) + 1     # cache content + the pending token
+        pad, W0 = v["pad_out"].copy(), v["w_new"]
 
 
 ALL_PINS = [
     pin_argmax_bruteforce, pin_argmax_torch, pin_argmax_specials, pin_widening_pairs,
     pin_verify_planted, pin_verify_alg3_vectorised, pin_width_exhaustive,
     pin_corollary_b3, pin_corollary_b4, pin_realign_replay, pin_realign_tagged_chain,
-    pin_posmask_closed_form, pin_golden_worked_example,
+    pin_posmask_closed_form, pin_golden_worked_example, pin_tokens_replay, pin_tokens_chain,
 ]

@@ -139,13 +139,45 @@ def test_step_rejects(sd):
     _no_gpu()
     src, dst = _kv(sd), _kv(sd, data=A + (1 << 30))
     ws = sd.workspace_bytes(2, 3, 100)
+    S_IN, S_OUT = A + (2 << 30), A + (3 << 30)
 
-    def step(B=2, pm_cap=64, src=src, dst=dst, ws_bytes=ws):
+    def step(B=2, pm_cap=64, src=src, dst=dst, ws_bytes=ws, s_in=None, s_in_stride=0, s_out=None, s_out_stride=0):
         return sd.lib.specdec_step(A, 1, A, A, B, 3, 100, 10, ctypes.byref(src), ctypes.byref(dst), A, A, A, A, A,
-                                   A, A, pm_cap, A, ws_bytes, None, None, None)
+                                   A, A, pm_cap, s_in, s_in_stride, s_out, s_out_stride, -1, A, ws_bytes, None,
+                                   None, None)
     assert step(pm_cap=13) == 1                  # pm_cap < W_in + k + 1
     assert step(src=_kv(sd, B=3), dst=_kv(sd, data=A + (1 << 30), B=3)) == 1   # cache rows differ
     assert step(ws_bytes=8) == 4
+    # token row: short strides, a missing half, overlap, in place with unequal strides
+    assert step(s_in=S_IN, s_in_stride=6, s_out=S_OUT, s_out_stride=11) == 1    # s_in_stride < W_in - k
+    assert step(s_in=S_IN, s_in_stride=7, s_out=S_OUT, s_out_stride=10) == 1    # s_out_stride < W_in + 1
+    assert step(s_in=S_IN, s_in_stride=7, s_out=None, s_out_stride=11) == 1
+    assert step(s_in=S_IN, s_in_stride=16, s_out=S_IN + 16, s_out_stride=16) == 1
+    assert step(s_in=S_IN, s_in_stride=12, s_out=S_IN, s_out_stride=16) == 1
+    assert step(s_in=S_IN + 2, s_in_stride=16, s_out=S_OUT, s_out_stride=16) == 2   # misaligned
+
+
+def test_realign_tokens_rejects(sd):
+    _no_gpu()
+    f = sd.lib.specdec_realign_tokens
+    S_IN, S_OUT = A + (2 << 30), A + (3 << 30)
+    ok_args = dict(s_in=S_IN, s_in_stride=7, s_out=S_OUT, s_out_stride=11, tokens=A, pad_in=A, n_acc=A, w_new=A,
+                   B=2, k=3, W_in=10, pad_id=-1, status=None, stream=None)
+
+    def call(**over):
+        d = dict(ok_args)
+        d.update(over)
+        return f(*d.values())
+    assert call(B=-1) == 1
+    assert call(k=65) == 1
+    assert call(W_in=3) == 1
+    assert call(s_in_stride=6) == 1
+    assert call(s_out_stride=10) == 1
+    assert call(s_out=None) == 1
+    assert call(tokens=None) == 1
+    assert call(w_new=A + 2) == 2
+    assert call(s_out=S_IN, s_out_stride=7) == 1     # in place needs s_out_stride >= W_in + 1 too
+    assert call(B=0, s_in=None, s_out=None, tokens=None) == 0
 
 
 def test_timing_query_rejects_unknown_kernel(sd):

@@ -17,9 +17,9 @@ import torch
 import oracle
 from paper_2510_22876_amd import workloads as wl
 from tests import checker
-from tests.gpu_util import (alloc_outputs, check_posmask_vs_oracle, check_relocation_on_device,
-                            check_spans_vs_oracle, check_verify_vs_oracle, host_spans, i16, run_gpu,
-                            sample_spans, say)
+from tests.gpu_util import (PAD_ID, alloc_outputs, check_posmask_vs_oracle, check_relocation_on_device,
+                            check_spans_vs_oracle, check_tokens_vs_oracle, check_verify_vs_oracle, host_spans, i16,
+                            run_gpu, sample_spans, say)
 
 pytestmark = pytest.mark.gpu
 
@@ -42,9 +42,10 @@ def test_full_size(name):
     logits, draft, *_ = wl.logits_and_drafts(w, 0, 0, device="cuda")
     src = wl.make_kv(w, pad_in, W_in, cap, device="cuda")
     src_spans = host_spans(src, spans, W_in)
-    r = run_gpu(w, variant="oop", logits=logits, draft=draft, src=src, pad_in=pad_in, W_in=W_in)
+    r = run_gpu(w, variant="oop", logits=logits, draft=draft, src=src, pad_in=pad_in, W_in=W_in, tokens="oop")
     v = check_verify_vs_oracle(r)
     check_posmask_vs_oracle(r, v)
+    check_tokens_vs_oracle(r, v)
     check_spans_vs_oracle(w, spans, src_spans, host_spans(r.dst, spans, W_in), pad_in, v, W_in)
     check_relocation_on_device(r, v["pad_out"], v["n_acc"], v["w_new"])
     say(f"{name}: out-of-place checked, w_new={v['w_new']}, n_acc={v['n_acc'].tolist()[:16]}")
@@ -70,6 +71,8 @@ def test_chained_in_place_tagged():
     pad = pad_in.copy()
     W0 = W_in - (w.k + 1)
     spans = sample_spans(w, n_extra=4)
+    s_rows = wl.make_token_rows(w, pad_in, W_in, cap + 2, 0, PAD_ID, device="cuda")
+    model = [list(s_rows[i, pad_in[i]:W_in - w.k].cpu().numpy()) for i in range(w.B)]
     for step in range(w.steps):
         if step > 0:
             wl.write_window(kv, w, W0, pad, seed=0, step=step, tagged=True)
@@ -78,9 +81,15 @@ def test_chained_in_place_tagged():
         logits, draft, *_ = wl.logits_and_drafts(w, 0, step, device="cuda")
         src_spans = host_spans(kv, spans, Wi)
         say(f"chained step {step}: W_in={Wi}")
-        r = run_gpu(w, variant="inplace", logits=logits, draft=draft, src=kv, pad_in=pad, W_in=Wi)
+        r = run_gpu(w, variant="inplace", logits=logits, draft=draft, src=kv, pad_in=pad, W_in=Wi,
+                    tokens="inplace", s_rows=s_rows)
         v = check_verify_vs_oracle(r)
         check_posmask_vs_oracle(r, v)
+        check_tokens_vs_oracle(r, v)
+        d = draft.cpu().numpy()
+        for i in range(w.B):   # Alg. 1's append, replayed per sequence
+            model[i] += list(d[i, : v["n_acc"][i]]) + [v["bonus"][i]]
+            assert list(r.extra["s_out"][i, v["pad_out"][i]: v["w_new"] + 1]) == model[i]
         check_spans_vs_oracle(w, spans, src_spans, host_spans(kv, spans, Wi), pad, v, Wi)
         check_relocation_on_device(r, v["pad_out"], v["n_acc"], v["w_new"])
         prod = checker.advance_prod_steps(prod, W0 - pad, v["n_acc"], step)

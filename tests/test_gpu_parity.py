@@ -16,7 +16,8 @@ import oracle
 from paper_2510_22876_amd import workloads as wl
 from tests import checker
 from tests.gpu_util import (SENT_KV, alloc_outputs, bits, check_kv_full_vs_oracle, check_posmask_vs_oracle,
-                            check_relocation_on_device, check_verify_vs_oracle, i16, run_gpu, say)
+                            check_relocation_on_device, check_tokens_vs_oracle, check_verify_vs_oracle, i16, run_gpu,
+                            say)
 
 pytestmark = pytest.mark.gpu
 
@@ -36,6 +37,7 @@ def _full_check(r):
     check_kv_full_vs_oracle(r, v)
     check_posmask_vs_oracle(r, v)
     check_relocation_on_device(r, r.out["pad_out"], r.out["n_acc"], r.out["w_new"])
+    check_tokens_vs_oracle(r, v)
     if r.variant == "oop":
         # out of place: columns [w_new, cap) of the destination are untouched
         tail = i16(r.dst[..., r.out["w_new"]:, :])
@@ -60,8 +62,19 @@ SMALL = {
 @pytest.mark.parametrize("api", ["step", "split"])
 @pytest.mark.parametrize("name", sorted(SMALL))
 def test_small_workloads(name, api, variant):
+    # the token row rides along: out of place with the out-of-place cache, in
+    # place with the in-place one
     for seed in (0, 1):
-        _full_check(run_gpu(SMALL[name], seed=seed, variant=variant, api=api))
+        _full_check(run_gpu(SMALL[name], seed=seed, variant=variant, api=api, tokens=variant))
+
+
+@pytest.mark.parametrize("tok", ["oop", "inplace"])
+@pytest.mark.parametrize("variant", ["oop", "inplace"])
+@pytest.mark.parametrize("name", ["tiny", "empty_old_content", "k0", "max_k", "mixed_shift_signs", "large_batch"])
+def test_token_rows(name, variant, tok):
+    w = SMALL.get(name) or EDGE[name]
+    for seed in (0, 2):
+        _full_check(run_gpu(w, seed=seed, variant=variant, tokens=tok))
 
 
 EDGE = {

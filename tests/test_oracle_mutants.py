@@ -45,6 +45,11 @@ MUTANTS = {
     "mask_off_by_one": ("uint8_t m = (j >= pad_out[i]) ? 1 : 0;", "uint8_t m = (j > pad_out[i]) ? 1 : 0;"),
     "positions_from_one": ("pos[(int64_t)i * pm_cap + j] = count - 1 > 0 ? count - 1 : 0;",
                            "pos[(int64_t)i * pm_cap + j] = count;"),
+    "token_row_drops_pending": ("for (int32_t j = pad_in[i]; j <= L; ++j) row[n++]",
+                                "for (int32_t j = pad_in[i]; j < L; ++j) row[n++]"),
+    "token_row_without_bonus": ("for (int32_t r = 0; r < a; ++r) row[n++]", "for (int32_t r = 0; r + 1 < a; ++r) row[n++]"),
+    "token_row_pads_zero": ("s_out[(int64_t)i * s_out_stride + j] = pad_id;", "s_out[(int64_t)i * s_out_stride + j] = 0;"),
+    "token_row_appends_row0": ("row[n++] = tokens[(int64_t)i * (k + 1) + r];", "row[n++] = tokens[r];"),
     "positions_raw_column": ("pos[(int64_t)i * pm_cap + j] = count - 1 > 0 ? count - 1 : 0;",
                              "pos[(int64_t)i * pm_cap + j] = j;"),
 }
