@@ -280,10 +280,10 @@ __global__ __launch_bounds__(kFinalizeThreads) void verify_finalize_kernel(Verif
 #define SPECDEC_OOP_NT 3
 #endif
 #ifndef SPECDEC_INPLACE_VEC
-#define SPECDEC_INPLACE_VEC 8
+#define SPECDEC_INPLACE_VEC 32
 #endif
 #ifndef SPECDEC_INPLACE_TPB
-#define SPECDEC_INPLACE_TPB 512
+#define SPECDEC_INPLACE_TPB 256
 #endif
 #ifndef SPECDEC_INPLACE_NT
 #define SPECDEC_INPLACE_NT 3
@@ -542,40 +542,43 @@ __device__ __forceinline__ void hold(const u32x4& v) {
   asm volatile("" ::"v"(v.x), "v"(v.y), "v"(v.z), "v"(v.w));
 }
 
-// Moves vectors [lo, lo + kTpb*kVec) (clipped to [0, n)) of one row's kept
-// entries from `from + u` to `to + u` within the same span.  All reads of the
-// chunk complete before any write to it.
+// Loads chunk [lo, lo + kTpb*kVec) (clipped to [0, n); indices outside are
+// clamped, their values unused) of one row's kept vectors, which start at
+// `from` within the span.
 template <int kVec, int kTpb, int kNt>
-__device__ __forceinline__ void move_chunk(u32x4* base, int64_t from, int64_t to, int64_t lo, int64_t n) {
-  constexpr int64_t kChunk = static_cast<int64_t>(kTpb) * kVec;
+__device__ __forceinline__ void load_chunk(const u32x4* base, int64_t from, int64_t lo, int64_t n, u32x4 (&v)[kVec]) {
   const int64_t t0 = static_cast<int64_t>(threadIdx.x >> 6) * (64 * kVec) + (threadIdx.x & 63);
-  u32x4 v[kVec];
-  if (lo >= 0 && lo + kChunk <= n) {
 #pragma unroll
-    for (int j = 0; j < kVec; ++j) v[j] = ld16<(kNt & 1) != 0>(base + (from + lo + t0 + j * 64));
-#pragma unroll
-    for (int j = 0; j < kVec; ++j) hold(v[j]);
-    __syncthreads();
-#pragma unroll
-    for (int j = 0; j < kVec; ++j) st16<(kNt & 2) != 0>(base + (to + lo + t0 + j * 64), v[j]);
-  } else {
-#pragma unroll
-    for (int j = 0; j < kVec; ++j) {
-      int64_t u = lo + t0 + j * 64;
-      u = u < 0 ? 0 : (u >= n ? n - 1 : u);
-      v[j] = ld16<(kNt & 1) != 0>(base + (from + u));
-    }
-#pragma unroll
-    for (int j = 0; j < kVec; ++j) hold(v[j]);
-    __syncthreads();
-#pragma unroll
-    for (int j = 0; j < kVec; ++j) {
-      const int64_t u = lo + t0 + j * 64;
-      if (u >= 0 && u < n) st16<(kNt & 2) != 0>(base + (to + u), v[j]);
-    }
+  for (int j = 0; j < kVec; ++j) {
+    int64_t u = lo + t0 + j * 64;
+    u = u < 0 ? 0 : (u >= n ? n - 1 : u);
+    v[j] = ld16<(kNt & 1) != 0>(base + (from + u));
   }
 }
 
+template <int kVec, int kTpb, int kNt>
+__device__ __forceinline__ void store_chunk(u32x4* base, int64_t to, int64_t lo, int64_t n, const u32x4 (&v)[kVec]) {
+  const int64_t t0 = static_cast<int64_t>(threadIdx.x >> 6) * (64 * kVec) + (threadIdx.x & 63);
+#pragma unroll
+  for (int j = 0; j < kVec; ++j) {
+    const int64_t u = lo + t0 + j * 64;
+    if (u >= 0 && u < n) st16<(kNt & 2) != 0>(base + (to + u), v[j]);
+  }
+}
+
+// Workgroup barrier that orders nothing but execution: the values this
+// thread loaded are already in its registers (hold), so no other thread's
+// later store can change them; loads issued after the barrier's program point
+// stay in flight across it.
+__device__ __forceinline__ void exec_barrier() { asm volatile("s_barrier" ::: "memory"); }
+
+// In place: one workgroup per span moves the row's kept vectors [from, from+n)
+// to [to, to+n) in chunks of kTpb*kVec, walking from the top for a shift to
+// higher addresses and from the bottom for a shift to lower ones.  The next
+// chunk's source never meets the current chunk's destination, so its loads
+// are issued before the current chunk is stored; a barrier after the current
+// chunk's loads have landed keeps every read of a chunk ahead of every write
+// to it.
 template <int kVec, int kTpb, int kNt>
 __global__ __launch_bounds__(kTpb) void realign_inplace_kernel(RealignArgs a) {
   if (blockIdx.x < a.extra_blocks) {
@@ -598,19 +601,30 @@ __global__ __launch_bounds__(kTpb) void realign_inplace_kernel(RealignArgs a) {
   const int64_t from = static_cast<int64_t>(g.pad_in) * vpc;
   const int64_t to = static_cast<int64_t>(g.pad_out) * vpc;
   constexpr int64_t kChunk = static_cast<int64_t>(kTpb) * kVec;
+  const int64_t nchunks = (n + kChunk - 1) / kChunk;
+  // chunk c starts at lo(c): from the top for s > 0, from the bottom for s < 0
+  auto lo_of = [&](int64_t c) { return s > 0 ? n - (c + 1) * kChunk : c * kChunk; };
+  u32x4 cur[kVec], nxt[kVec];
+  load_chunk<kVec, kTpb, kNt>(base, from, lo_of(0), n, cur);
+  for (int64_t c = 0; c < nchunks; ++c) {
+    const bool more = c + 1 < nchunks;
+    if (more) load_chunk<kVec, kTpb, kNt>(base, from, lo_of(c + 1), n, nxt);
+#pragma unroll
+    for (int j = 0; j < kVec; ++j) hold(cur[j]);
+    exec_barrier();  // every thread's loads of chunk c have landed
+    store_chunk<kVec, kTpb, kNt>(base, to, lo_of(c), n, cur);
+    if (more) {
+#pragma unroll
+      for (int j = 0; j < kVec; ++j) cur[j] = nxt[j];
+    }
+  }
   if (s > 0) {
-    // moving towards higher addresses: walk from the top, so a chunk's
-    // destination never covers source vectors that are still to be read
-    for (int64_t hi = n; hi > 0; hi -= kChunk) move_chunk<kVec, kTpb, kNt>(base, from, to, hi - kChunk, n);
     // the vacated columns [pad_in, pad_out) become padding; every read of
-    // them completed before the last barrier
+    // them landed before the last barrier
     const u32x4 zero = {0u, 0u, 0u, 0u};
     for (int64_t u = threadIdx.x; u < to - from; u += kTpb) st16<(kNt & 2) != 0>(base + (from + u), zero);
-  } else {
-    // moving towards lower addresses: walk from the bottom; columns
-    // [0, pad_out) already hold padding (+0.0)
-    for (int64_t lo = 0; lo < n; lo += kChunk) move_chunk<kVec, kTpb, kNt>(base, from, to, lo, n);
   }
+  // columns [0, pad_out) already hold padding (+0.0) for a shift to lower addresses
 }
 
 __global__ __launch_bounds__(kThreads) void posmask_kernel(int64_t* pos, uint8_t* mask,
