@@ -34,7 +34,7 @@ sys.path.insert(0, str(ROOT))
 
 PEAK_HBM_GBS = 8000.0
 METRIC = "verify+realign steps/s and achieved HBM GB/s (% peak), B=8 7B-shaped KV"
-KERNEL_SRC = ROOT / "paper_2510_22876_amd" / "csrc" / "specdec_kernels.hip"
+KERNEL_SRCS = [ROOT / "paper_2510_22876_amd" / "csrc" / f for f in ("specdec_kernels.hip", "span_copy.h", "posmask.h")]
 
 
 def log(*a):
@@ -42,7 +42,11 @@ def log(*a):
 
 
 def kernel_source_hash() -> str:
-    return hashlib.sha256(KERNEL_SRC.read_bytes()).hexdigest()[:16]
+    """Hash of the sources the realign kernel is built from."""
+    h = hashlib.sha256()
+    for f in KERNEL_SRCS:
+        h.update(f.read_bytes())
+    return h.hexdigest()[:16]
 
 
 def describe(w, variant):

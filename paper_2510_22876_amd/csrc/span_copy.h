@@ -1,0 +1,91 @@
+// Device helpers shared by the kernels that move bf16 cache columns: 16-byte
+// vector loads/stores with optional nontemporal hints, scalar loads of
+// per-launch invariants, and the split-piece column move used for every
+// out-of-place rewrite of a span (realignment and batch gathering).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace specdec {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+template <bool kNt>
+__device__ __forceinline__ u32x4 ld16(const u32x4* p) {
+  if constexpr (kNt) return __builtin_nontemporal_load(p);
+  else return *p;
+}
+
+template <bool kNt>
+__device__ __forceinline__ void st16(u32x4* p, u32x4 v) {
+  if constexpr (kNt) __builtin_nontemporal_store(v, p);
+  else *p = v;
+}
+
+// Loads a value that no kernel of this launch writes, through the constant
+// address space: a wave-uniform address then becomes a scalar load on the
+// scalar cache path instead of a vector load queued behind the data traffic.
+__device__ __forceinline__ int32_t load_invariant(const int32_t* p) {
+  return *(const __attribute__((address_space(4))) int32_t*)p;
+}
+
+// One workgroup's share of an out-of-place span rewrite.  The output span has
+// `total` 16-byte vectors: [0, zero_end) become +0.0, vector u in
+// [zero_end, total) receives source vector u - shift.  The workgroup moves
+// kPieces pieces of kTpb vectors (one per lane) starting at `base`, the
+// pieces kSplit vectors apart.  Each piece is padding (stores only), content
+// (one load and one store per lane), or the boundary / ragged end, where the
+// source index is clamped into the kept range so every load is in bounds.
+template <int kPieces, int kTpb, int kSplit, int kNt>
+__device__ __forceinline__ void split_pieces(const u32x4* s, u32x4* d, int64_t base, int64_t total,
+                                             int64_t zero_end, int64_t shift) {
+  const int t = threadIdx.x;
+  const u32x4 zero = {0u, 0u, 0u, 0u};
+  const int64_t lo = zero_end - shift, hi = total - 1 - shift;   // kept source range
+  u32x4 v[kPieces];
+#pragma unroll
+  for (int j = 0; j < kPieces; ++j) {
+    const int64_t p0 = base + static_cast<int64_t>(j) * kSplit;  // first vector of the piece
+    if (p0 >= zero_end && p0 + kTpb <= total) {
+      v[j] = ld16<(kNt & 1) != 0>(s + (p0 + t - shift));
+    } else if (p0 + kTpb > zero_end && p0 < total) {
+      int64_t si = p0 + t - shift;
+      si = si < lo ? lo : (si > hi ? hi : si);
+      v[j] = ld16<(kNt & 1) != 0>(s + si);
+    } else {
+      v[j] = zero;
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < kPieces; ++j) {
+    const int64_t p0 = base + static_cast<int64_t>(j) * kSplit;
+    if (p0 >= total) break;
+    const int64_t u = p0 + t;
+    if (p0 + kTpb <= zero_end) {
+      st16<(kNt & 2) != 0>(d + u, zero);
+    } else if (p0 >= zero_end && p0 + kTpb <= total) {
+      st16<(kNt & 2) != 0>(d + u, v[j]);
+    } else if (u < total) {
+      st16<(kNt & 2) != 0>(d + u, u >= zero_end ? v[j] : zero);
+    }
+  }
+}
+
+// First vector of workgroup `sub` of a span in the split-piece layout.
+template <int kPieces, int kTpb, int kSplit>
+__device__ __forceinline__ int64_t split_base(uint32_t sub) {
+  static_assert(kSplit % kTpb == 0, "a group is a whole number of workgroups");
+  constexpr uint32_t kPerGroup = kSplit / kTpb;
+  const uint32_t grp = sub / kPerGroup;
+  return static_cast<int64_t>(grp) * (kPieces * kSplit) + static_cast<int64_t>(sub - grp * kPerGroup) * kTpb;
+}
+
+// Workgroups per span in the split-piece layout for spans of `vecs` vectors.
+template <int kPieces, int kTpb, int kSplit>
+constexpr int64_t split_blocks(int64_t vecs) {
+  return ((vecs + static_cast<int64_t>(kPieces) * kSplit - 1) / (static_cast<int64_t>(kPieces) * kSplit)) *
+         (kSplit / kTpb);
+}
+
+}  // namespace specdec

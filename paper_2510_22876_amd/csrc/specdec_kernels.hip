@@ -22,6 +22,8 @@
 // matrix cores.
 #include <cstdlib>
 
+#include "posmask.h"
+#include "span_copy.h"
 #include "specdec_internal.h"
 
 namespace specdec {
@@ -289,20 +291,6 @@ __global__ __launch_bounds__(kFinalizeThreads) void verify_finalize_kernel(Verif
 #define SPECDEC_INPLACE_NT 3
 #endif
 
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-
-template <bool kNt>
-__device__ __forceinline__ u32x4 ld16(const u32x4* p) {
-  if constexpr (kNt) return __builtin_nontemporal_load(p);
-  else return *p;
-}
-
-template <bool kNt>
-__device__ __forceinline__ void st16(u32x4* p, u32x4 v) {
-  if constexpr (kNt) __builtin_nontemporal_store(v, p);
-  else *p = v;
-}
-
 struct RealignArgs {
   const u32x4* src;
   u32x4* dst;
@@ -336,13 +324,6 @@ struct RowGeom {
   int32_t pad_in, pad_out, len, w;
 };
 
-// Loads a value that no kernel of this launch writes, through the constant
-// address space: a wave-uniform address then becomes a scalar load on the
-// scalar cache path instead of a vector load queued behind the data traffic.
-__device__ __forceinline__ int32_t load_invariant(const int32_t* p) {
-  return *(const __attribute__((address_space(4))) int32_t*)p;
-}
-
 __device__ __forceinline__ uint32_t row_geometry(const RealignArgs& a, int row, RowGeom& g) {
   const int32_t L = a.W_in - (a.k + 1);
   const int32_t w = load_invariant(a.w_new);
@@ -375,17 +356,8 @@ __device__ void posmask_block(uint32_t blk, int64_t* pos, uint8_t* mask, const i
     if (cb == 0 && threadIdx.x == 0 && dev_status) atomicOr(dev_status, kBadPadOut);
     return;
   }
-  int64_t* prow = pos + static_cast<int64_t>(row) * pm_cap;
-  uint8_t* mrow = mask + static_cast<int64_t>(row) * pm_cap;
-#pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const int64_t j = static_cast<int64_t>(cb) * (4 * kTpb) + q * kTpb + threadIdx.x;
-    if (j < width) {
-      const bool content = j >= po;
-      prow[j] = content ? j - po : 0;
-      mrow[j] = content ? 1 : 0;
-    }
-  }
+  posmask_cols<kTpb>(cb, pos + static_cast<int64_t>(row) * pm_cap, mask + static_cast<int64_t>(row) * pm_cap, po,
+                     width);
 }
 
 // Token row S of one sequence (Alg. 1, phase 3): the c_i + 1 tokens of the
@@ -469,15 +441,11 @@ __device__ __forceinline__ void extra_block(const RealignArgs& a, uint32_t b) {
     token_block<kTpb>(a, b - a.pm_blocks);
 }
 
-// Out of place: every workgroup moves kPieces pieces of kTpb 16-byte vectors
-// (one per lane) of one span's output, the pieces kSplit vectors apart.  The
-// output of a span is cut into groups of kPieces*kSplit vectors; group g is
-// covered by kSplit/kTpb workgroups.  Each piece is new padding (stores only),
-// kept content (a load from the shifted source position and a store), or the
-// boundary between them / the ragged end of the span.
+// Out of place: the output of a span is cut into groups of kPieces*kSplit
+// vectors, each covered by kSplit/kTpb workgroups; every workgroup moves
+// kPieces pieces of one wave-width (see split_pieces).
 template <int kPieces, int kTpb, int kSplit, int kNt>
 __global__ __launch_bounds__(kTpb) void realign_oop_kernel(RealignArgs a) {
-  static_assert(kSplit % kTpb == 0, "a group is a whole number of workgroups");
   if (blockIdx.x < a.extra_blocks) {
     extra_block<kTpb>(a, blockIdx.x);
     return;
@@ -494,46 +462,15 @@ __global__ __launch_bounds__(kTpb) void realign_oop_kernel(RealignArgs a) {
       atomicOr(a.dev_status, err);
     return;
   }
-  constexpr uint32_t kPerGroup = kSplit / kTpb;
-  const uint32_t grp = sub / kPerGroup;
-  const int64_t base = static_cast<int64_t>(grp) * (kPieces * kSplit) + static_cast<int64_t>(sub - grp * kPerGroup) * kTpb;
+  const int64_t base = split_base<kPieces, kTpb, kSplit>(sub);
   const int64_t vpc = a.vpc;
   const int64_t total = static_cast<int64_t>(g.w) * vpc;        // output vectors of the span
   if (base >= total) return;
   const int64_t zero_end = static_cast<int64_t>(g.pad_out) * vpc;
   const int64_t shift = static_cast<int64_t>(g.pad_out - g.pad_in) * vpc;
-  const u32x4* s = a.src + static_cast<int64_t>(span) * a.src_span_vecs;
-  u32x4* d = a.dst + static_cast<int64_t>(span) * a.dst_span_vecs;
-  const int t = threadIdx.x;
-  const u32x4 zero = {0u, 0u, 0u, 0u};
-  const int64_t lo = zero_end - shift, hi = total - 1 - shift;   // kept source range
-  u32x4 v[kPieces];
-#pragma unroll
-  for (int j = 0; j < kPieces; ++j) {
-    const int64_t p0 = base + static_cast<int64_t>(j) * kSplit;  // first vector of the piece
-    if (p0 >= zero_end && p0 + kTpb <= total) {
-      v[j] = ld16<(kNt & 1) != 0>(s + (p0 + t - shift));
-    } else if (p0 + kTpb > zero_end && p0 < total) {
-      int64_t si = p0 + t - shift;
-      si = si < lo ? lo : (si > hi ? hi : si);
-      v[j] = ld16<(kNt & 1) != 0>(s + si);
-    } else {
-      v[j] = zero;
-    }
-  }
-#pragma unroll
-  for (int j = 0; j < kPieces; ++j) {
-    const int64_t p0 = base + static_cast<int64_t>(j) * kSplit;
-    if (p0 >= total) break;
-    const int64_t u = p0 + t;
-    if (p0 + kTpb <= zero_end) {
-      st16<(kNt & 2) != 0>(d + u, zero);
-    } else if (p0 >= zero_end && p0 + kTpb <= total) {
-      st16<(kNt & 2) != 0>(d + u, v[j]);
-    } else if (u < total) {
-      st16<(kNt & 2) != 0>(d + u, u >= zero_end ? v[j] : zero);
-    }
-  }
+  split_pieces<kPieces, kTpb, kSplit, kNt>(a.src + static_cast<int64_t>(span) * a.src_span_vecs,
+                                           a.dst + static_cast<int64_t>(span) * a.dst_span_vecs, base, total,
+                                           zero_end, shift);
 }
 
 // Register values of the current thread are live; forces the compiler to
@@ -800,9 +737,7 @@ hipError_t launch_tokens(const RealignLaunch& p, hipStream_t stream) {
 
 int64_t realign_grid_blocks(int64_t nspans, int64_t W_in, int32_t D, bool in_place) {
   if (in_place) return nspans;
-  const int64_t per_group = static_cast<int64_t>(kOopSplit) * kOopVec;
-  const int64_t groups = (W_in * (D / 8) + per_group - 1) / per_group;
-  return nspans * groups * (kOopSplit / kOopTpb);
+  return nspans * split_blocks<kOopVec, kOopTpb, kOopSplit>(W_in * (D / 8));
 }
 
 hipError_t launch_posmask(const PosmaskLaunch& p, hipStream_t stream) {
