@@ -59,6 +59,12 @@ class Oracle:
         lib.oracle_posmask.restype = ctypes.c_int
         lib.oracle_realign_tokens.argtypes = [P, i64, P, i64, P, P, P, i32, i32, i32, i32, i32]
         lib.oracle_realign_tokens.restype = ctypes.c_int
+        lib.oracle_gather_batch.argtypes = [P, i64, i32, P, i64, P, P, i32, i32, i32, i32, i32, P, i64, P, i64,
+                                            i32, P]
+        lib.oracle_gather_batch.restype = ctypes.c_int
+        lib.oracle_scatter_accepted.argtypes = [P, i64, i32, P, P, i32, P, P, i32, i32, i32, i32, P, i64, i32, P,
+                                                i64, P, P, i64]
+        lib.oracle_scatter_accepted.restype = ctypes.c_int
         self.lib = lib
 
 
@@ -205,6 +211,63 @@ def realign_tokens(s_in, tokens, pad_in, n_acc, w_new: int, W_in: int, pad_id: i
     if rc:
         raise OracleError(f"oracle_realign_tokens rejected its arguments (code {rc})")
     return out
+
+
+def gather_batch(pool, pool_tok, lens, slots, Lb: int, batch_cap: int, btok_stride: int, pad_id: int, out=None,
+                 oracle: Oracle | None = None):
+    """EXSpec's GetBatch (Alg. 2): rows gathered from pool slots and left-padded
+    to width Lb.  pool uint16 [L][2][N][H][cap][D]; pool_tok int32 [N][*];
+    returns (batch uint16 [L][2][B][H][batch_cap][D], batch_tok int32
+    [B][btok_stride], pads int32 [B]).  ``out`` = (batch, batch_tok) writes into
+    given arrays (cache columns >= Lb and token columns > Lb keep their
+    contents); fresh arrays are zero there."""
+    pl = _kv_bits(pool)
+    nl, two, N, H, cap, D = pl.shape
+    pt = _c(np.asarray(pool_tok), np.int32)
+    ln = _c(np.asarray(lens).reshape(N), np.int32)
+    sl = _c(np.asarray(slots).reshape(-1), np.int32)
+    B = sl.size
+    if out is None:
+        batch = np.zeros((nl, 2, B, H, batch_cap, D), np.uint16)
+        btok = np.zeros((B, btok_stride), np.int32)
+    else:
+        batch, btok = out
+        assert batch.dtype == np.uint16 and batch.flags["C_CONTIGUOUS"] and batch.shape == (nl, 2, B, H, batch_cap, D)
+        assert btok.dtype == np.int32 and btok.flags["C_CONTIGUOUS"] and btok.shape == (B, btok_stride)
+    pads = np.zeros(B, np.int32)
+    rc = _load(oracle).oracle_gather_batch(_ptr(pl), cap, N, _ptr(pt), pt.shape[1], _ptr(ln), _ptr(sl), B, int(Lb),
+                                           nl, H, D, _ptr(batch), batch_cap, _ptr(btok), btok_stride, int(pad_id),
+                                           _ptr(pads))
+    if rc:
+        raise OracleError(f"oracle_gather_batch rejected its arguments (code {rc})")
+    return batch, btok, pads
+
+
+def scatter_accepted(batch, pads, tokens, n_acc, slots, Lb: int, pool, pool_tok, lens, batch_tok=None,
+                     oracle: Oracle | None = None):
+    """EXSpec's write-back (Alg. 2, Phase 4), in place on pool (uint16), pool_tok
+    and lens (int32 numpy arrays) and, when given, the batch token row
+    batch_tok (int32 [B][stride], the step's append)."""
+    bt = _kv_bits(batch)
+    nl, two, B, H, bcap, D = bt.shape
+    assert pool.dtype == np.uint16 and pool.flags["C_CONTIGUOUS"]
+    assert pool_tok.dtype == np.int32 and pool_tok.flags["C_CONTIGUOUS"] and lens.dtype == np.int32
+    tk = _c(np.asarray(tokens), np.int32)
+    k = tk.shape[1] - 1
+    pd = _c(np.asarray(pads).reshape(B), np.int32)
+    na = _c(np.asarray(n_acc).reshape(B), np.int32)
+    sl = _c(np.asarray(slots).reshape(B), np.int32)
+    N, cap = pool.shape[2], pool.shape[4]
+    if batch_tok is not None:
+        assert batch_tok.dtype == np.int32 and batch_tok.flags["C_CONTIGUOUS"]
+        bptr, bstride = _ptr(batch_tok), batch_tok.shape[1]
+    else:
+        bptr, bstride = None, 0
+    rc = _load(oracle).oracle_scatter_accepted(_ptr(bt), bcap, B, _ptr(pd), _ptr(tk), k, _ptr(na), _ptr(sl), int(Lb),
+                                               nl, H, D, _ptr(pool), cap, N, _ptr(pool_tok), pool_tok.shape[1],
+                                               _ptr(lens), bptr, bstride)
+    if rc:
+        raise OracleError(f"oracle_scatter_accepted rejected its arguments (code {rc})")
 
 
 def step(logits, dtype: str, draft, pad_in, kv, W_in: int, dst_cap=None,

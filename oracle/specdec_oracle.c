@@ -280,6 +280,100 @@ int oracle_realign_tokens(const int32_t* s_in, int64_t s_in_stride, int32_t* s_o
   return OR_OK;
 }
 
+/* ---- EXSpec sequence pool: batch gather and write-back (Alg. 2) ------------- */
+
+/*
+ * The pool keeps every sequence unpadded: slot s holds len[s] cached entries
+ * in cache columns [0, len[s]) of its spans and len[s] + 1 tokens (its cached
+ * tokens and the pending token).
+ *
+ * Gather (Alg. 2, GetBatch): batch row i is slot slot[i], left-padded to the
+ * batch width Lb: cache columns [0, Lb - len) hold +0.0 and [Lb - len, Lb) the
+ * slot's entries; the token row holds Lb - len copies of pad_id, then the
+ * slot's len + 1 tokens (width Lb + 1); pads[i] = Lb - len.  When every row
+ * has the same length this is a plain concatenation (no padding).
+ *
+ * pool  bf16 [n_layers][2][N][H][pool_cap][D];  batch bf16 [n_layers][2][B][H][batch_cap][D]
+ * pool_tok int32 [N][tok_stride];  batch_tok int32 [B][btok_stride]
+ */
+int oracle_gather_batch(const uint16_t* pool, int64_t pool_cap, int32_t N, const int32_t* pool_tok,
+                        int64_t tok_stride, const int32_t* len, const int32_t* slot, int32_t B, int32_t Lb,
+                        int32_t n_layers, int32_t H, int32_t D, uint16_t* batch, int64_t batch_cap,
+                        int32_t* batch_tok, int64_t btok_stride, int32_t pad_id, int32_t* pads) {
+  if (B < 0 || N < 0 || Lb < 0 || batch_cap < Lb || btok_stride < (int64_t)Lb + 1) return OR_EINVAL;
+  for (int32_t i = 0; i < B; ++i) {
+    if (slot[i] < 0 || slot[i] >= N) return OR_EINVAL;
+    const int32_t n = len[slot[i]];
+    if (n < 0 || n > Lb || n > pool_cap || (int64_t)n + 1 > tok_stride) return OR_EINVAL;
+  }
+  for (int32_t i = 0; i < B; ++i) {
+    const int32_t n = len[slot[i]];
+    const int32_t p = Lb - n;
+    pads[i] = p;
+    for (int32_t l = 0; l < n_layers; ++l)
+      for (int32_t kv = 0; kv < 2; ++kv)
+        for (int32_t h = 0; h < H; ++h) {
+          const uint16_t* s = pool + ((((int64_t)l * 2 + kv) * N + slot[i]) * H + h) * pool_cap * D;
+          uint16_t* d = batch + ((((int64_t)l * 2 + kv) * B + i) * H + h) * batch_cap * D;
+          for (int64_t j = 0; j < p; ++j) memset(d + j * D, 0, sizeof(uint16_t) * D);
+          memcpy(d + (int64_t)p * D, s, sizeof(uint16_t) * (size_t)n * D);
+        }
+    for (int32_t j = 0; j < p; ++j) batch_tok[(int64_t)i * btok_stride + j] = pad_id;
+    for (int32_t j = 0; j <= n; ++j)
+      batch_tok[(int64_t)i * btok_stride + p + j] = pool_tok[(int64_t)slot[i] * tok_stride + j];
+  }
+  return OR_OK;
+}
+
+/*
+ * Write-back (Alg. 2, Phase 4): after verification of a batch formed by
+ * gather (rows end at column Lb, row i has pads[i] columns of padding, the
+ * verify window occupies [Lb, Lb + k + 1)), for every row i:
+ *   Pool[slot] <- Pool[slot] + A[i] + B[i]: the slot's token list gains the
+ *     accepted drafts and the bonus (tokens[i][0..n_acc[i]]);
+ *   Pool.KV[slot] <- KV[i]: the slot's cache becomes the row's cache,
+ *     unpadded and cut after the accepted entries: batch columns
+ *     [pads[i], Lb + n_acc[i] + 1) -> slot columns [0, len + n_acc[i] + 1);
+ *   len[slot] grows by n_acc[i] + 1.
+ * The row must mirror its slot (len[slot] == Lb - pads[i]); slots must be
+ * distinct.  When batch_tok is not NULL the batch's own token row (width
+ * Lb + 1) also gains the n_acc[i] + 1 tokens at columns [Lb + 1, Lb + n_acc[i]
+ * + 2): the step's append to S that a batch kept for the next step needs.
+ */
+int oracle_scatter_accepted(const uint16_t* batch, int64_t batch_cap, int32_t B, const int32_t* pads,
+                            const int32_t* tokens, int32_t k, const int32_t* n_acc, const int32_t* slot, int32_t Lb,
+                            int32_t n_layers, int32_t H, int32_t D, uint16_t* pool, int64_t pool_cap, int32_t N,
+                            int32_t* pool_tok, int64_t tok_stride, int32_t* len, int32_t* batch_tok,
+                            int64_t btok_stride) {
+  if (B < 0 || N < 0 || k < 0 || Lb < 0 || batch_cap < (int64_t)Lb + k + 1) return OR_EINVAL;
+  if (batch_tok && btok_stride < (int64_t)Lb + k + 2) return OR_EINVAL;
+  for (int32_t i = 0; i < B; ++i) {
+    if (slot[i] < 0 || slot[i] >= N || n_acc[i] < 0 || n_acc[i] > k) return OR_EINVAL;
+    if (pads[i] < 0 || pads[i] > Lb || len[slot[i]] != Lb - pads[i]) return OR_EINVAL;
+    for (int32_t q = 0; q < i; ++q)
+      if (slot[q] == slot[i]) return OR_EINVAL;
+    const int64_t grown = (int64_t)len[slot[i]] + n_acc[i] + 1;
+    if (grown > pool_cap || grown + 1 > tok_stride) return OR_EINVAL;
+  }
+  for (int32_t i = 0; i < B; ++i) {
+    const int32_t a = n_acc[i] + 1;
+    const int32_t n = Lb - pads[i];
+    for (int32_t l = 0; l < n_layers; ++l)
+      for (int32_t kv = 0; kv < 2; ++kv)
+        for (int32_t h = 0; h < H; ++h) {
+          const uint16_t* s = batch + ((((int64_t)l * 2 + kv) * B + i) * H + h) * batch_cap * D;
+          uint16_t* d = pool + ((((int64_t)l * 2 + kv) * N + slot[i]) * H + h) * pool_cap * D;
+          memcpy(d, s + (int64_t)pads[i] * D, sizeof(uint16_t) * (size_t)(n + a) * D);
+        }
+    int32_t* trow = pool_tok + (int64_t)slot[i] * tok_stride;
+    for (int32_t r = 0; r < a; ++r) trow[n + 1 + r] = tokens[(int64_t)i * (k + 1) + r];
+    if (batch_tok)
+      for (int32_t r = 0; r < a; ++r) batch_tok[(int64_t)i * btok_stride + Lb + 1 + r] = tokens[(int64_t)i * (k + 1) + r];
+    len[slot[i]] = n + a;
+  }
+  return OR_OK;
+}
+
 /* ---- position ids and attention mask (I2) ---------------------------------- */
 
 /*

@@ -442,9 +442,246 @@ def pin_tokens_chain(o=None):
         pad, W0 = v["pad_out"].copy(), v["w_new"]
 
 
+# ---- EXSpec: batch gather, write-back, scheduling (Alg. 2) --------------------------------
+
+def _pool(rng, N, L, H, D, cap, lens, tok_stride):
+    """A pool with random entries on [0, len) and garbage (0xFFFF) beyond."""
+    pool = np.full((L, 2, N, H, cap, D), 0xFFFF, np.uint16)
+    tok = np.full((N, tok_stride), -9, np.int32)
+    for s in range(N):
+        n = int(lens[s])
+        pool[:, :, s, :, :n, :] = rng.integers(1, 0x7F00, size=(L, 2, H, n, D), dtype=np.uint16)
+        tok[s, : n + 1] = rng.integers(0, 1000, size=n + 1)
+    return pool, tok
+
+
+def pin_gather_list_model(o=None):
+    """Each batch row, read as a list of columns, is the slot's own list of
+    cached entries after Lb - len zero columns; its token row is the slot's
+    tokens after Lb - len pad ids (checked per element, any width Lb >= the
+    longest row, slots in any order, repeated lengths, empty sequences)."""
+    rng = np.random.default_rng(21)
+    for trial in range(12):
+        N = int(rng.integers(1, 9))
+        L, H, D = int(rng.integers(1, 3)), int(rng.integers(1, 3)), int(rng.choice([1, 8]))
+        cap = 24
+        lens = rng.integers(0, cap + 1, size=N).astype(np.int32)
+        if trial % 3 == 0:
+            lens[:] = lens[0]
+        pool, tok = _pool(rng, N, L, H, D, cap, lens, cap + 3)
+        B = int(rng.integers(1, N + 1))
+        slots = rng.permutation(N)[:B].astype(np.int32)
+        Lb = int(lens[slots].max()) + int(rng.integers(0, 3))
+        bcap = Lb + int(rng.integers(0, 4))
+        bstride = Lb + 1 + int(rng.integers(0, 3))
+        out = (np.full((L, 2, B, H, bcap, D), 0xABCD, np.uint16), np.full((B, bstride), -77, np.int32))
+        batch, btok, pads = oracle.gather_batch(pool, tok, lens, slots, Lb, bcap, bstride, -5, out=out, oracle=o)
+        for i, s in enumerate(slots):
+            n = int(lens[s])
+            seq = [pool[:, :, s, :, j, :] for j in range(n)]
+            rows = [batch[:, :, i, :, j, :] for j in range(Lb)]
+            p = Lb - len(seq)
+            assert pads[i] == p
+            assert all(not r.any() for r in rows[:p]), "padding columns must be +0.0"
+            assert all(np.array_equal(a, b) for a, b in zip(rows[p:], seq))
+            assert np.all(batch[:, :, i, :, Lb:, :] == 0xABCD), "columns beyond the width are not written"
+            assert list(btok[i, : Lb + 1]) == [-5] * p + list(tok[s, : n + 1])
+            assert np.all(btok[i, Lb + 1:] == -77)
+
+
+def pin_gather_same_length_is_concat(o=None):
+    """Same-length rows (Section 3.2): the batch is the plain concatenation of
+    the slots' caches along the batch axis, with no padding."""
+    rng = np.random.default_rng(22)
+    N, L, H, D, cap = 7, 2, 3, 8, 19
+    lens = np.full(N, 13, np.int32)
+    pool, tok = _pool(rng, N, L, H, D, cap, lens, cap + 2)
+    slots = np.array([5, 0, 3, 6], np.int32)
+    batch, btok, pads = oracle.gather_batch(pool, tok, lens, slots, 13, 13, 14, -1, oracle=o)
+    assert not pads.any()
+    want = np.concatenate([pool[:, :, s: s + 1, :, :13, :] for s in slots], axis=2)
+    assert np.array_equal(batch, want)
+    assert np.array_equal(btok, tok[slots, :14])
+
+
+def pin_regroup_equals_realign(o=None):
+    """Write-back followed by a new gather of the same rows at the new width is
+    the EqSpec realignment of the batch (both unpad the rows, append the
+    accepted entries and repad to the longest row): two independent routes to
+    Section 3.1's unpad-append-repad must agree, also on the token rows."""
+    rng = np.random.default_rng(23)
+    for trial in range(10):
+        N, L, H, D, k = 9, 1, 2, 4, int(rng.integers(0, 5))
+        cap = 40
+        lens = rng.integers(0, 20, size=N).astype(np.int32)
+        pool, tok = _pool(rng, N, L, H, D, cap, lens, cap + 2)
+        B = int(rng.integers(1, N + 1))
+        slots = rng.permutation(N)[:B].astype(np.int32)
+        Lb = int(lens[slots].max())
+        bcap = Lb + k + 1
+        batch, btok, pads = oracle.gather_batch(pool, tok, lens, slots, Lb, bcap, bcap + 1, -4, oracle=o)
+        # the verify window: fresh entries for [pending, d_1..d_k]
+        batch[..., Lb:, :] = rng.integers(1, 0x7F00, size=batch[..., Lb:, :].shape, dtype=np.uint16)
+        accepts = rng.integers(0, k + 1, size=B)
+        v = _verify_from_accepts(pads, accepts, k, Lb + k + 1, o=o)
+        eq = oracle.realign_kv(batch, k, Lb + k + 1, pads, v["n_acc"], v["w_new"], oracle=o)
+        eq_tok = oracle.realign_tokens(btok, v["tokens"], pads, v["n_acc"], v["w_new"], Lb + k + 1, -4, oracle=o)
+        lens2 = lens.copy()
+        oracle.scatter_accepted(batch, pads, v["tokens"], v["n_acc"], slots, Lb, pool, tok, lens2, oracle=o)
+        assert np.array_equal(lens2[slots], lens[slots] + v["n_acc"] + 1)
+        others = np.setdiff1d(np.arange(N), slots)
+        assert np.array_equal(lens2[others], lens[others])
+        batch2, btok2, pads2 = oracle.gather_batch(pool, tok, lens2, slots, v["w_new"], v["w_new"], v["w_new"] + 1,
+                                                   -4, oracle=o)
+        assert np.array_equal(pads2, v["pad_out"])
+        assert np.array_equal(batch2, eq[..., : v["w_new"], :])
+        assert np.array_equal(btok2, eq_tok[:, : v["w_new"] + 1])
+
+
+def pin_scatter_appends_to_batch_row(o=None):
+    """With the batch token row given, write-back also appends the accepted
+    drafts and the bonus to it (Alg. 1's S <- S + A + B): a kept batch then
+    equals a new gather of its rows, and with uniform acceptance it equals
+    EqSpec's realigned batch at zero offsets (Corollary B.4)."""
+    rng = np.random.default_rng(24)
+    N, L, H, D, k = 6, 1, 1, 8, 3
+    cap = 32
+    lens = np.array([10, 4, 10, 7, 10, 1], np.int32)
+    pool, tok = _pool(rng, N, L, H, D, cap, lens, cap + 2)
+    slots = np.array([0, 2, 4, 1], np.int32)
+    Lb = 10
+    bcap = Lb + k + 1
+    batch, btok, pads = oracle.gather_batch(pool, tok, lens, slots, Lb, bcap, bcap + 1, -1, oracle=o)
+    batch[..., Lb:, :] = rng.integers(1, 0x7F00, size=batch[..., Lb:, :].shape, dtype=np.uint16)
+    v = _verify_from_accepts(pads, [2] * 4, k, Lb + k + 1, o=o)
+    assert np.array_equal(v["pad_out"], pads)                 # Corollary B.4
+    oracle.scatter_accepted(batch, pads, v["tokens"], v["n_acc"], slots, Lb, pool, tok, lens, batch_tok=btok,
+                            oracle=o)
+    w = v["w_new"]
+    assert w == Lb + 3
+    again, again_tok, again_pads = oracle.gather_batch(pool, tok, lens, slots, w, w, w + 1, -1, oracle=o)
+    assert np.array_equal(again_pads, pads)
+    assert np.array_equal(batch[..., :w, :], again)
+    assert np.array_equal(btok[:, : w + 1], again_tok)
+
+
+def _toy_setup(seed, N, V=61, equal_groups=3, lo=3, hi=20):
+    from tests.toy_model import ToyModel
+    from tests import exspec_loop as el
+    rng = np.random.default_rng(seed)
+    model = ToyModel(V=V, n_layers=1, H=2, D=4, accept=0.7, salt=seed)
+    prompts = el.random_prompts(rng, N, lo, hi, V, equal_groups=equal_groups)
+    return model, prompts
+
+
+def pin_exspec_output_equivalence(o=None):
+    """Corollary B.2 for Algorithm 2: an EXSpec loop over a pool (gather,
+    verify, write-back, scheduling with lazy realignment and same-length
+    grouping) generates, for every sequence, exactly what sequential greedy
+    decoding generates, and every slot ends caching its own tokens' entries.
+    The toy model turns any cache, mask or position-id error into a changed
+    token."""
+    from oracle.exspec import SequencePool
+    from tests import exspec_loop as el
+    for seed, (N, W, B, k, groups) in enumerate([(12, 8, 4, 3, 3), (9, 5, 3, 2, 0), (10, 10, 4, 4, 1)]):
+        model, prompts = _toy_setup(seed, N, equal_groups=groups)
+        max_new = 12
+        sched = SequencePool([len(p) - 1 for p in prompts], window=W, batch=B, max_new=max_new)
+        res = el.run_exspec(el.OracleBackend(), model, prompts, sched, k=k, max_new=max_new)
+        el.check_equivalence(model, prompts, res, max_new)
+        el.check_pool_cache(model, prompts, res)
+        assert any(t[2] for t in res.trace) or groups == 0
+        assert any(not t[3] for t in res.trace) or groups == 1
+
+
+def pin_eqspec_output_equivalence(o=None):
+    """Corollary B.2 for Algorithm 1: fixed batches realigned after every
+    round (cache, token row, positions and mask) generate what sequential
+    greedy decoding generates."""
+    from tests import exspec_loop as el
+    for seed, (N, B, k) in enumerate([(8, 4, 3), (5, 5, 5), (3, 2, 1)]):
+        model, prompts = _toy_setup(100 + seed, N, equal_groups=0, lo=2, hi=25)
+        res = el.run_eqspec(el.OracleBackend(), model, prompts, B, k, 10)
+        el.check_equivalence(model, prompts, res, 10)
+
+
+def pin_scheduler_properties(o=None):
+    """Alg. 2's structure on scheduling traces driven by random acceptance: the
+    window holds the first W active sequences, a batch draws min(B, |window|)
+    distinct members of it, same-length batches need no padding, a batch is
+    kept only after a round whose offsets were all zero (uniform acceptance,
+    Corollary B.4), a same-length group is taken whenever the window holds
+    B sequences of one length, and every sequence completes."""
+    from oracle.exspec import SequencePool
+    rng = np.random.default_rng(25)
+    for trial in range(30):
+        N = int(rng.integers(1, 25))
+        W = int(rng.integers(1, 12))
+        B = int(rng.integers(1, W + 1))
+        k = int(rng.integers(0, 5))
+        max_new = int(rng.integers(1, 20))
+        lens0 = rng.integers(0, 6 if trial % 2 else 30, size=N)
+        sp = SequencePool(list(lens0), window=W, batch=B, max_new=max_new)
+        order = sorted(range(N), key=lambda s: (lens0[s], s))
+        assert sp.order == order
+        prev_uniform = None
+        for _ in range(4 * N * (max_new + 1) + 1):
+            active = [s for s in order if sp.active[s]]
+            b = sp.next_batch()
+            if b is None:
+                assert not active
+                break
+            win = active[:W]
+            assert len(b.slots) == min(B, len(win)) and len(set(b.slots)) == len(b.slots)
+            assert set(b.slots) <= set(win)
+            assert b.lens == [sp.len[s] for s in b.slots] and b.width == max(b.lens)
+            assert b.same_length == (len(set(b.lens)) == 1)
+            if b.reuse:
+                assert prev_uniform is not None and prev_uniform == b.slots
+            else:
+                counts = {}
+                for s in win:
+                    counts[sp.len[s]] = counts.get(sp.len[s], 0) + 1
+                if max(counts.values()) >= len(b.slots):
+                    assert b.same_length
+                else:
+                    assert b.slots == win[: len(b.slots)]
+            n_acc = rng.integers(0, k + 1, size=len(b.slots)) if rng.random() < 0.6 else \
+                np.full(len(b.slots), int(rng.integers(0, k + 1)))
+            before = [sp.len[s] for s in b.slots]
+            sp.commit(b, n_acc, [[1] * (int(a) + 1) for a in n_acc])
+            assert [sp.len[s] for s in b.slots] == [x + int(a) + 1 for x, a in zip(before, n_acc)]
+            prev_uniform = list(b.slots) if len(set(int(a) for a in n_acc)) == 1 and \
+                all(sp.active[s] for s in b.slots) else None
+        assert b is None and not sp.has_active(), "the schedule did not finish"
+        assert all(max_new <= g <= max_new + k for g in sp.generated)
+
+
+def pin_scheduler_grouping_rate(o=None):
+    """Section 3.2: with prompt-length sorting and similar lengths, grouping
+    approaches unity.  Equal prompt lengths with uniform acceptance: every
+    round runs on a same-length batch, and every round after a batch's first
+    keeps it (no gather)."""
+    from oracle.exspec import SequencePool
+    sp = SequencePool([17] * 12, window=8, batch=4, max_new=10)
+    rounds = []
+    for _ in range(100):
+        b = sp.next_batch()
+        if b is None:
+            break
+        rounds.append((b.same_length, b.reuse))
+        sp.commit(b, [2] * len(b.slots), [[1, 1, 1]] * len(b.slots))
+    assert b is None and len(rounds) == 12                  # 3 batches of 4, 4 rounds each
+    assert all(s for s, _ in rounds)
+    assert sum(1 for _, r in rounds if not r) == 3          # one gather per batch of 4
+
+
 ALL_PINS = [
     pin_argmax_bruteforce, pin_argmax_torch, pin_argmax_specials, pin_widening_pairs,
     pin_verify_planted, pin_verify_alg3_vectorised, pin_width_exhaustive,
     pin_corollary_b3, pin_corollary_b4, pin_realign_replay, pin_realign_tagged_chain,
     pin_posmask_closed_form, pin_golden_worked_example, pin_tokens_replay, pin_tokens_chain,
+    pin_gather_list_model, pin_gather_same_length_is_concat, pin_regroup_equals_realign,
+    pin_scatter_appends_to_batch_row, pin_exspec_output_equivalence, pin_eqspec_output_equivalence,
+    pin_scheduler_properties, pin_scheduler_grouping_rate,
 ]

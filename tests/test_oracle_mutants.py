@@ -41,7 +41,8 @@ MUTANTS = {
                                "for (int32_t j = L + (k + 1 - a); j < L + k + 1; ++j, ++n)"),
     "unpad_skips_first_entry": ("for (int32_t j = pad_in[i]; j < L; ++j, ++n)", "for (int32_t j = pad_in[i] + (pad_in[i] < L); j < L; ++j, ++n)"),
     "no_shift": ("memcpy(d + (int64_t)p_new * D, row,", "memcpy(d + (int64_t)(p_new > pad_in[i] ? pad_in[i] : p_new) * D, row,"),
-    "pads_not_cleared": ("memset(d + j * D, 0, sizeof(uint16_t) * D);", "(void)j;"),
+    "pads_not_cleared": ("for (int64_t j = 0; j < p_new; ++j)\n            memset(d + j * D, 0, sizeof(uint16_t) * D);",
+                         "for (int64_t j = 0; j < p_new; ++j)\n            (void)j;"),
     "mask_off_by_one": ("uint8_t m = (j >= pad_out[i]) ? 1 : 0;", "uint8_t m = (j > pad_out[i]) ? 1 : 0;"),
     "positions_from_one": ("pos[(int64_t)i * pm_cap + j] = count - 1 > 0 ? count - 1 : 0;",
                            "pos[(int64_t)i * pm_cap + j] = count;"),
@@ -50,9 +51,47 @@ MUTANTS = {
     "token_row_without_bonus": ("for (int32_t r = 0; r < a; ++r) row[n++]", "for (int32_t r = 0; r + 1 < a; ++r) row[n++]"),
     "token_row_pads_zero": ("s_out[(int64_t)i * s_out_stride + j] = pad_id;", "s_out[(int64_t)i * s_out_stride + j] = 0;"),
     "token_row_appends_row0": ("row[n++] = tokens[(int64_t)i * (k + 1) + r];", "row[n++] = tokens[r];"),
+    "gather_pads_not_cleared": ("for (int64_t j = 0; j < p; ++j) memset(d + j * D, 0, sizeof(uint16_t) * D);", ""),
+    "gather_right_aligned_to_cap": ("const int32_t p = Lb - n;", "const int32_t p = (int32_t)batch_cap - n;"),
+    "gather_drops_pending_token": ("for (int32_t j = 0; j <= n; ++j)\n      batch_tok", "for (int32_t j = 0; j < n; ++j)\n      batch_tok"),
+    "scatter_drops_last_entry": ("sizeof(uint16_t) * (size_t)(n + a) * D);", "sizeof(uint16_t) * (size_t)(n + a - 1) * D);"),
+    "scatter_ignores_padding": ("memcpy(d, s + (int64_t)pads[i] * D,", "memcpy(d, s,"),
+    "scatter_overwrites_pending": ("trow[n + 1 + r] = tokens", "trow[n + r] = tokens"),
+    "scatter_len_without_bonus": ("len[slot[i]] = n + a;", "len[slot[i]] = n + a - 1;"),
+    "scatter_batch_row_at_width": ("batch_tok[(int64_t)i * btok_stride + Lb + 1 + r]", "batch_tok[(int64_t)i * btok_stride + Lb + r]"),
     "positions_raw_column": ("pos[(int64_t)i * pm_cap + j] = count - 1 > 0 ? count - 1 : 0;",
                              "pos[(int64_t)i * pm_cap + j] = j;"),
 }
+
+# Plausible slips in the scheduler (oracle/exspec.py), caught by the
+# scheduling properties or by the output-equivalence loops.
+EXSPEC_SRC = ROOT / "oracle" / "exspec.py"
+PY_MUTANTS = {
+    "reuse_after_ragged_round": ("uniform = len({int(x) for x in n_acc}) == 1", "uniform = True"),
+    "window_unbounded": ("if self.active[s]][: self.W]", "if self.active[s]]"),
+    "fallback_takes_last": ("chosen = win[:B]", "chosen = win[-B:]"),
+    "grouping_skipped": ("if chosen is not None:\n            lens", "if False:\n            lens"),
+    "no_length_sort": ("sort_by_length: bool = True", "sort_by_length: bool = False"),
+    "reuse_ignores_finished": ("if self.prev is not None and all(self.active[s] for s in self.prev)",
+                               "if self.prev is not None"),
+    "length_without_bonus": ("a = int(n_acc[i]) + 1", "a = int(n_acc[i])"),
+}
+
+PY_RUNNER = r"""
+import sys
+sys.path.insert(0, {root!r})
+import oracle, oracle.exspec as ex
+exec(compile(open({src!r}).read(), "exspec_mutant", "exec"), ex.__dict__)
+from tests import pins
+failed = []
+for pin in pins.ALL_PINS:
+    try:
+        pin(None)
+    except Exception as e:
+        failed.append(pin.__name__)
+print("FAILED_PINS", failed)
+sys.exit(1 if failed else 0)
+"""
 
 RUNNER = r"""
 import sys
@@ -82,5 +121,17 @@ def test_mutant_is_caught(name, tmp_path):
     subprocess.run(["gcc", "-O2", "-std=c11", "-fPIC", "-shared", str(mutated), "-o", str(lib), "-lm"],
                    check=True, capture_output=True)
     r = subprocess.run([sys.executable, "-c", RUNNER.format(root=str(ROOT), lib=str(lib))],
+                       capture_output=True, text=True, timeout=600, cwd=str(ROOT))
+    assert r.returncode != 0, f"mutant {name} survived every pin:\n{r.stdout[-2000:]}\n{r.stderr[-2000:]}"
+
+
+@pytest.mark.parametrize("name", sorted(PY_MUTANTS))
+def test_scheduler_mutant_is_caught(name, tmp_path):
+    old, new = PY_MUTANTS[name]
+    src = EXSPEC_SRC.read_text()
+    assert src.count(old) == 1, f"mutation anchor for {name} not unique/present"
+    mutated = tmp_path / "exspec_mutant.py"
+    mutated.write_text(src.replace(old, new))
+    r = subprocess.run([sys.executable, "-c", PY_RUNNER.format(root=str(ROOT), src=str(mutated))],
                        capture_output=True, text=True, timeout=600, cwd=str(ROOT))
     assert r.returncode != 0, f"mutant {name} survived every pin:\n{r.stdout[-2000:]}\n{r.stderr[-2000:]}"
