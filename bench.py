@@ -14,7 +14,13 @@ counters when the committed summary matches the current kernel source, and
 the CPU oracle timed on a bounded sample of the same step.
 
   python bench.py [--steps K] [--warmup W] [--workload NAME] [--variant oop|inplace]
+  python bench.py --path exspec [--exspec-batch ragged|same]
   python bench.py --copy-calibration GIB   # plain device copy, for counter scaling
+
+``--path exspec`` measures EXSpec's step instead (Algorithm 2 without the
+model forwards): the batch gather from a sequence pool (with the fused token
+rows, paddings and position ids / mask), greedy verification, and the
+append-only write-back, on the same shapes.
 """
 from __future__ import annotations
 
@@ -34,17 +40,20 @@ sys.path.insert(0, str(ROOT))
 
 PEAK_HBM_GBS = 8000.0
 METRIC = "verify+realign steps/s and achieved HBM GB/s (% peak), B=8 7B-shaped KV"
-KERNEL_SRCS = [ROOT / "paper_2510_22876_amd" / "csrc" / f for f in ("specdec_kernels.hip", "span_copy.h", "posmask.h")]
+METRIC_EXSPEC = "EXSpec gather+verify+write-back steps/s and achieved HBM GB/s (% peak), B=8 7B-shaped KV"
+CSRC = ROOT / "paper_2510_22876_amd" / "csrc"
+KERNEL_SRCS = [CSRC / f for f in ("specdec_kernels.hip", "span_copy.h", "posmask.h")]
+GATHER_SRCS = [CSRC / f for f in ("exspec_kernels.hip", "span_copy.h", "posmask.h")]
 
 
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def kernel_source_hash() -> str:
-    """Hash of the sources the realign kernel is built from."""
+def kernel_source_hash(srcs=None) -> str:
+    """Hash of the sources the measured kernel is built from."""
     h = hashlib.sha256()
-    for f in KERNEL_SRCS:
+    for f in srcs or KERNEL_SRCS:
         h.update(f.read_bytes())
     return h.hexdigest()[:16]
 
@@ -77,10 +86,10 @@ def step_bytes(w, pad_in, W_in, n_acc, w_new, variant, token_row=True):
     return dict(realign=realign, posmask=posmask, verify=verify)
 
 
-def read_traffic_summary(workload: str, variant: str):
-    """HBM bytes per realign launch from the committed rocprofv3 counter summary,
-    if it was taken on the current kernel source."""
-    path = ROOT / "profiles" / f"realign_{variant}_{workload}_hbm_counters.md"
+def read_traffic_summary(workload: str, variant: str, kernel: str = "realign", srcs=None):
+    """HBM bytes per launch of the measured kernel from the committed rocprofv3
+    counter summary, if it was taken on the current kernel source."""
+    path = ROOT / "profiles" / f"{kernel}_{variant}_{workload}_hbm_counters.md"
     if not path.exists():
         return None, "no counter summary"
     text = path.read_text()
@@ -88,7 +97,7 @@ def read_traffic_summary(workload: str, variant: str):
     m_bytes = re.search(r"hbm_bytes_per_launch:\s*([0-9.eE+]+)", text)
     if not m_hash or not m_bytes:
         return None, "summary unreadable"
-    if m_hash.group(1) != kernel_source_hash():
+    if m_hash.group(1) != kernel_source_hash(srcs):
         return None, "kernel changed since the counters were taken"
     return float(m_bytes.group(1)), path.name
 
@@ -131,6 +140,169 @@ def cpu_baseline(w, logits, draft, pad_in, W_in, src, budget_s: float, s_rows=No
                         f"single-threaded, scaled to one whole step ({est:.2f} s)"))
 
 
+def exspec_bytes(w, lens_b, Lb, n_acc):
+    """Algorithmic bytes of EXSpec's step: the gather reads each row's cached
+    entries and writes the padded batch (plus token rows and position ids /
+    mask), the append write-back moves each row's n_acc + 1 new entries, and
+    verification reads the logits."""
+    C = w.column_bytes
+    B, k = w.B, w.k
+    lens_b = lens_b.astype(np.int64)
+    a = n_acc.astype(np.int64) + 1
+    gather = int(lens_b.sum()) * C + B * Lb * C
+    gather_small = 4 * int((lens_b + 1).sum()) + 4 * B * (Lb + 1) + 9 * B * (Lb + k + 1) + 4 * 2 * B + 4 * B
+    writeback = 2 * int(a.sum()) * C + 4 * int(a.sum()) * 2 + 4 * B * (k + 1) + 4 * 4 * B
+    verify = B * (k + 1) * w.V * w.logit_bytes + 4 * B * k + 4 * B + 4 * B * (k + 1) + 3 * 4 * B + 4
+    return dict(gather=gather + gather_small, writeback=writeback, verify=verify)
+
+
+def cpu_baseline_exspec(w, pool, pool_tok, lens, slots, Lb, logits, draft, budget_s):
+    """The oracle, single-threaded, on a bounded sample of EXSpec's step:
+    verification over every logit row, and the gather and (whole-row)
+    write-back of one-layer slabs of the pool cycling over up to two layers
+    until ``budget_s`` seconds of work; scaled to one whole step."""
+    import oracle
+    import torch
+    k = w.k
+    bcap = Lb + k + 1
+    host_pool = [pool[l:l + 1].contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+                 for l in range(min(w.L, 2))]
+    tok = pool_tok.cpu().numpy()
+    t0 = time.perf_counter()
+    v = oracle.verify(logits.cpu(), w.logit_dtype, draft.cpu().numpy(), np.asarray(Lb - lens[slots], np.int32),
+                      Lb + k + 1)
+    t_verify = time.perf_counter() - t0
+    runs, t_layers = 0, 0.0
+    while t_layers < budget_s or runs == 0:
+        hp = host_pool[runs % len(host_pool)].copy()
+        ln = lens.copy()
+        tk = tok.copy()
+        t0 = time.perf_counter()
+        batch, btok, pads = oracle.gather_batch(hp, tk, ln, slots, Lb, bcap, bcap + 1, -1)
+        oracle.scatter_accepted(batch, pads, v["tokens"], v["n_acc"], slots, Lb, hp, tk, ln)
+        t_layers += time.perf_counter() - t0
+        runs += 1
+    per_layer = t_layers / runs
+    est = t_verify + per_layer * w.L
+    return dict(value=1.0 / est, unit="steps/s", cores=1, kind="oracle",
+                sample=(f"oracle verify over all {w.B * (k + 1)} logit rows ({t_verify * 1e3:.1f} ms), gather + "
+                        f"whole-row write-back of {runs} one-layer pool slabs ({per_layer * 1e3:.1f} ms per layer, "
+                        f"x{w.L} layers); single-threaded, scaled to one whole step ({est:.2f} s)"))
+
+
+def bench_exspec(args, w):
+    """EXSpec's step on one GPU: gather a batch of B rows from a pool of 4B
+    sequences, verify it, write the accepted entries back (append mode)."""
+    import torch
+    from paper_2510_22876_amd import specdec as sd
+    from paper_2510_22876_amd import workloads as wl
+
+    B, k = w.B, w.k
+    N = 4 * B
+    lens = wl.pool_lengths(w, N, args.seed)
+    if args.exspec_batch == "same":
+        lens[:B] = lens[0]                      # a same-length group: the batch is a plain concatenation
+    slots = np.arange(B, dtype=np.int32)        # the batch: the pool's first B sequences
+    Lb = int(lens[:B].max())
+    cap = int(lens.max()) + 2 * (k + 1)
+    pool, pool_tok = wl.make_pool(w, lens, cap, cap + 2, args.seed, device="cuda")
+    bcap = Lb + k + 1
+    batch = torch.empty((w.L, 2, B, w.H, bcap, w.D), dtype=torch.bfloat16, device="cuda")
+    btok = torch.empty((B, bcap + 1), dtype=torch.int32, device="cuda")
+    pads = torch.empty(B, dtype=torch.int32, device="cuda")
+    pos = torch.empty((B, bcap), dtype=torch.int64, device="cuda")
+    mask = torch.empty((B, bcap), dtype=torch.uint8, device="cuda")
+    logits, draft, *_ = wl.logits_and_drafts(w, args.seed, 0, device="cuda")
+    bufs = sd.StepBuffers(B, k, w.V, bcap, "cuda")
+    lens_d = torch.as_tensor(lens, device="cuda")
+    lens0 = lens_d.clone()
+    slots_d = torch.as_tensor(slots, device="cuda")
+    status = bufs.dev_status
+    W_in = Lb + k + 1
+    desc = (f"{w.name} pool: N={N} sequences, lengths {w.prompt}; batch: slots 0..{B - 1} "
+            f"({'same length' if args.exspec_batch == 'same' else 'ragged, unpad-repad'}), Lb={Lb}; B={B} k={k} "
+            f"V={w.V} {w.logit_dtype} logits; KV L={w.L} H={w.H} D={w.D} bf16; append write-back")
+    log(f"[bench] exspec: {desc}")
+
+    def step():
+        sd.specdec_gather_batch(pool, pool_tok, lens_d, slots_d, Lb, batch, pads, batch_tok=btok, pos=pos, mask=mask,
+                                k=k, pad_id=-1, dev_status=status)
+        sd.specdec_verify_greedy(logits, draft, pads, W_in, bufs.tokens, bufs.n_acc, bufs.bonus, bufs.pad_out,
+                                 bufs.w_new, bufs.workspace, status)
+        sd.specdec_scatter_accepted(batch, pads, bufs.tokens, bufs.n_acc, slots_d, Lb, pool, pool_tok, lens_d,
+                                    batch_tok=btok, mode=sd.WRITEBACK_APPEND, dev_status=status)
+
+    def timed_pass(K, mask_bits):
+        # the write-back grows each slot's length: restore it before every
+        # step, outside the events that bracket the step
+        sd.timing_reset()
+        sd.timing_enable(mask_bits)
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        total = 0.0
+        for _ in range(K):
+            lens_d.copy_(lens0)
+            s.record()
+            step()
+            e.record()
+            torch.cuda.synchronize()
+            total += s.elapsed_time(e) / 1e3
+        sd.timing_enable(False)
+        return total
+
+    timed_pass(args.warmup, 0)
+    if int(status.cpu()[0]) != 0:
+        raise RuntimeError("device flagged invalid values")
+    n_acc = bufs.n_acc.cpu().numpy()
+    K = args.steps
+    elapsed = timed_pass(K, 1 << sd.KERNEL_GATHER)
+    gather_ms, gather_n = sd.timing_query(sd.KERNEL_GATHER)
+    timed_pass(K, (1 << sd.KERNEL_VERIFY) | (1 << sd.KERNEL_WRITEBACK))
+    verify_ms, verify_n = sd.timing_query(sd.KERNEL_VERIFY)
+    wb_ms, wb_n = sd.timing_query(sd.KERNEL_WRITEBACK)
+    assert gather_n == K and verify_n == K and wb_n == K
+    by = exspec_bytes(w, lens[:B], Lb, n_acc)
+    g_ms = gather_ms / K
+    achieved = by["gather"] / (g_ms * 1e-3) / 1e9
+    ms_per_step = elapsed / K * 1e3
+    total_bytes = by["gather"] + by["writeback"] + by["verify"]
+    variant = "same" if args.exspec_batch == "same" else "ragged"
+    traffic, traffic_src = read_traffic_summary(w.name, variant, kernel="gather", srcs=GATHER_SRCS)
+    log(f"[bench] exspec n_acc={n_acc.tolist()} gather {g_ms:.4f} ms ({by['gather'] / 1e9:.3f} GB, {achieved:.0f} GB/s), "
+        f"verify {verify_ms / K:.4f} ms, write-back {wb_ms / K:.4f} ms ({by['writeback'] / 1e6:.2f} MB), "
+        f"step {ms_per_step:.4f} ms; traffic: {traffic_src}")
+    cpu = None
+    if args.cpu_baseline_seconds > 0:
+        cpu = cpu_baseline_exspec(w, pool, pool_tok, lens, slots, Lb, logits, draft, args.cpu_baseline_seconds)
+        log(f"[bench] cpu baseline: {cpu['value']:.4f} steps/s ({cpu['sample']})")
+    line = {
+        "metric": METRIC_EXSPEC,
+        "value": K / elapsed,
+        "unit": "steps/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": desc, "B": B, "k": k, "V": w.V, "L": w.L, "H": w.H, "D": w.D, "N": N, "Lb": Lb,
+            "batch": variant, "seed": args.seed, "step_bytes": total_bytes,
+            "step_GBps": round(total_bytes / (ms_per_step * 1e-3) / 1e9, 1),
+            "gather_ms": round(g_ms, 5), "verify_ms": round(verify_ms / K, 5), "writeback_ms": round(wb_ms / K, 5),
+        },
+        "roofline": {
+            "bound": "hbm", "kernel": "gather (+ fused token rows, pos/mask)", "achieved": round(achieved, 1),
+            "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic,
+            "algorithmic_bytes": by["gather"],
+        },
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
 def copy_calibration(gib: float):
     import torch
     n = int(gib * (1 << 30))
@@ -166,6 +338,10 @@ def main():
     ap.add_argument("--kernel-timers", choices=["on", "off"], default="on",
                     help="record the library's HIP events around the realign kernel inside the timed region "
                          "(off: a second pass measures it)")
+    ap.add_argument("--path", choices=["eqspec", "exspec"], default="eqspec",
+                    help="eqspec: the verify + realign step (default); exspec: gather + verify + write-back")
+    ap.add_argument("--exspec-batch", choices=["ragged", "same"], default="ragged",
+                    help="exspec: a batch of prompt-distributed lengths (unpad-repad) or one length (concatenation)")
     ap.add_argument("--copy-calibration", type=float, default=0.0,
                     help="run a plain device copy of this many GiB each way and exit")
     args = ap.parse_args()
@@ -188,6 +364,9 @@ def main():
     from paper_2510_22876_amd import workloads as wl
 
     w = wl.WORKLOADS[args.workload]
+    if args.path == "exspec":
+        bench_exspec(args, w)
+        return
     variant = args.variant
     n, W_in, pad_in, cap = wl.initial_geometry(w, args.seed)
     log(f"[bench] workload {describe(w, variant)}; W_in={W_in} cap={cap}")

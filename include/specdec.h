@@ -46,7 +46,7 @@
 extern "C" {
 #endif
 
-#define SPECDEC_ABI_VERSION 2
+#define SPECDEC_ABI_VERSION 3
 
 typedef enum {
   SPECDEC_OK = 0,
@@ -63,6 +63,9 @@ typedef enum { SPECDEC_F32 = 0, SPECDEC_BF16 = 1, SPECDEC_F16 = 2 } specdec_dtyp
 #define SPECDEC_DEV_BAD_ACCEPT 0x2u  /* n_acc[i] outside [0, k]                         */
 #define SPECDEC_DEV_BAD_WIDTH 0x4u   /* w_new outside [1, W_in] or shorter than a row   */
 #define SPECDEC_DEV_BAD_PAD_OUT 0x8u /* pad_out[i] outside [0, w_new] or pos/mask short */
+#define SPECDEC_DEV_BAD_SLOT 0x10u   /* pool slot outside [0, N), or its length does not
+                                        fit the batch width, the pool or its token row */
+#define SPECDEC_DEV_SLOT_LEN 0x20u   /* write-back: lens[slot] != Lb - pads[i] on entry */
 
 /* Limits checked by the host. */
 #define SPECDEC_MAX_B 65536
@@ -213,6 +216,149 @@ specdec_status_t specdec_step(const void* logits, int32_t dtype, const int32_t* 
                               void* workspace, size_t workspace_bytes, uint32_t* dev_status,
                               int32_t* w_new_host, void* stream);
 
+/* ---- EXSpec (Algorithm 2): sequence pool, batch gather and write-back ---------
+ *
+ * EXSpec keeps every sequence unpadded in its own slot of a pool and forms each
+ * step's batch from a window of active sequences (Section 3.2, "Cross-Batch
+ * Scheduling"; Appendix: EXSpec, Algorithm 2).  The pool cache has the KV
+ * layout with one row per slot: [L][2][N][H][pool_cap][D] (pool->B = N);
+ * slot s holds its lens[s] cached entries in columns [0, lens[s]).  The pool
+ * token rows are int32 [N][pool_tok_stride]; slot s holds its lens[s] cached
+ * tokens and then its pending token in columns [0, lens[s]].
+ */
+
+/*
+ * GetBatch (Algorithm 2, phase 1): gather the rows `slots` of the pool into a
+ * batch left-padded to width Lb.  Same-length rows concatenate with no padding
+ * (the case the scheduler looks for); otherwise this is the unpad-repad
+ * fallback.  For row i with slot s = slots[i] and n = lens[s]:
+ *   pads[i] = Lb - n;
+ *   batch columns [0, pads[i]) of every (layer, K/V, head) span become +0.0 and
+ *   column j in [pads[i], Lb) receives pool column j - pads[i] of slot s;
+ *   batch_tok[i][0, pads[i]) = pad_id, batch_tok[i][pads[i] + j] =
+ *   pool_tok[s][j] for j in [0, n]  (Lb + 1 columns);
+ *   pos / mask over columns [0, Lb + k + 1) as in specdec_build_posmask with
+ *   pad_out = pads and w_new = Lb (the mask of the draft and verify forwards).
+ * Batch columns [Lb, cap) and token columns beyond Lb are left as they are.
+ *
+ *   pool      the pool cache (pool->B = N slots); pool_tok int32 [N][pool_tok_stride].
+ *   lens      int32 [N] (device): cached entries per slot.
+ *   slots     int32 [B] (device): the batch's slots, row order.  Slots must be
+ *             distinct (not checked: repeated slots are gathered twice).
+ *   Lb        batch width (host), >= lens[slots[i]] for every row.
+ *   batch     cache [L][2][B][H][cap][D] with equal L, H, D, cap >= Lb; must
+ *             not overlap the pool.
+ *   batch_tok int32 [B][btok_stride], btok_stride >= Lb + 1; may be NULL.
+ *   pads      int32 [B] out; -1 for a row that was skipped.
+ *   pos, mask int64 / uint8 [B][pm_cap], pm_cap >= Lb + k + 1; may be NULL
+ *             (both, then k is not used).
+ * A row whose slot is outside [0, N) or whose length is outside [0, Lb], above
+ * pool_cap or above pool_tok_stride - 1 is skipped (no byte of it written) and
+ * flagged SPECDEC_DEV_BAD_SLOT.
+ */
+specdec_status_t specdec_gather_batch(const specdec_kv_t* pool, const int32_t* pool_tok,
+                                      int64_t pool_tok_stride, const int32_t* lens,
+                                      const int32_t* slots, int32_t B, int32_t Lb, int32_t k,
+                                      const specdec_kv_t* batch, int32_t* batch_tok,
+                                      int64_t btok_stride, int32_t pad_id, int32_t* pads,
+                                      int64_t* pos, uint8_t* mask, int64_t pm_cap,
+                                      uint32_t* dev_status, void* stream);
+
+#define SPECDEC_WRITEBACK_FULL 0   /* copy the row's whole unpadded cache            */
+#define SPECDEC_WRITEBACK_APPEND 1 /* copy only the row's n_acc[i] + 1 new entries     */
+
+/*
+ * Write-back (Algorithm 2, phase 4) after verification of a gathered batch
+ * (rows end at column Lb, row i has pads[i] columns of padding, the verify
+ * window is in columns [Lb, Lb + k + 1)).  For row i with slot s = slots[i],
+ * n = Lb - pads[i] and a = n_acc[i] + 1:
+ *   Pool[s] <- Pool[s] + A[i] + B[i]: pool_tok[s][n + 1 + r] = tokens[i][r]
+ *     for r in [0, a) (the accepted drafts and the bonus token);
+ *   Pool.KV[s] <- KV[i]: pool columns [0, n + a) of slot s receive batch
+ *     columns [pads[i], Lb + a) of row i (SPECDEC_WRITEBACK_FULL), or only
+ *     columns [n, n + a) receive batch columns [Lb, Lb + a)
+ *     (SPECDEC_WRITEBACK_APPEND: the same result whenever the slot still holds
+ *     the n entries the row was gathered from, which Algorithm 2 guarantees:
+ *     the forwards only append to the batch);
+ *   lens[s] = n + a;
+ *   when batch_tok is not NULL: batch_tok[i][Lb + 1 + r] = tokens[i][r] for
+ *     r in [0, a), so a batch kept for the next step (lazy realignment, all
+ *     rows accepting alike) has its token rows extended as a new gather would.
+ *
+ *   batch     cache [L][2][B][H][cap][D], cap >= Lb + k + 1; must not overlap
+ *             the pool.  pads int32 [B], tokens int32 [B][k+1], n_acc int32 [B]:
+ *             from specdec_gather_batch and specdec_verify_greedy.
+ *   slots     int32 [B], distinct (not checked: repeated slots leave those
+ *             slots' contents unspecified; every access stays in bounds).
+ *   pool, pool_tok, lens  as for specdec_gather_batch; written.
+ *   batch_tok int32 [B][btok_stride], btok_stride >= Lb + k + 2; may be NULL.
+ *   mode      SPECDEC_WRITEBACK_FULL or SPECDEC_WRITEBACK_APPEND.
+ * A row with a slot outside [0, N), n_acc outside [0, k], pads outside
+ * [0, Lb], or n + a above pool_cap or above pool_tok_stride - 1 is skipped and
+ * flagged (SPECDEC_DEV_BAD_SLOT / _BAD_ACCEPT / _BAD_PAD_IN).  lens[s] !=
+ * Lb - pads[i] on entry is flagged SPECDEC_DEV_SLOT_LEN (the row is still
+ * written back).
+ */
+specdec_status_t specdec_scatter_accepted(const specdec_kv_t* batch, const int32_t* pads,
+                                          const int32_t* tokens, const int32_t* n_acc,
+                                          const int32_t* slots, int32_t B, int32_t k, int32_t Lb,
+                                          const specdec_kv_t* pool, int32_t* pool_tok,
+                                          int64_t pool_tok_stride, int32_t* lens,
+                                          int32_t* batch_tok, int64_t btok_stride, int32_t mode,
+                                          uint32_t* dev_status, void* stream);
+
+/*
+ * The SequencePool scheduler of Algorithm 2 (host only; no GPU call).
+ *
+ * Holds N sequences with their lengths (cached entries), generated counts and
+ * active flags.  The window is the first `window` active sequences in pool
+ * order (sorted by initial length, ties by index, when sort_by_length; else
+ * input order).  specdec_sched_next_batch picks, in this order:
+ *   1. lazy realignment: the previous batch unchanged when its last step
+ *      accepted the same number of drafts in every row (every offset of
+ *      Eq. (2) is zero, Corollary B.4) and all its rows are still active;
+ *   2. same-length grouping: window members bucketed by length; the bucket of
+ *      the oldest window member if it has >= b members (b = min(batch, window
+ *      members)), else the largest bucket with >= b members (ties: the
+ *      shorter length); its first b members in pool order;
+ *   3. fallback (unpad-repad): the first b window members.
+ * The batch width is the longest row's length.  specdec_sched_commit records a
+ * step's outcome: every row grows by n_acc[i] + 1; a sequence is deactivated
+ * once it has generated >= max_new tokens or appended eos_id (eos_id >= 0).
+ */
+typedef struct specdec_sched specdec_sched_t; /* opaque */
+
+typedef struct specdec_batch_info {
+  int32_t B;           /* rows (0: no active sequence is left)               */
+  int32_t width;       /* Lb: the longest row's length                       */
+  int32_t same_length; /* 1: every row has the same length (no padding)      */
+  int32_t reuse;       /* 1: the previous batch, unchanged (no gather needed) */
+} specdec_batch_info_t;
+
+/* lens: host int32 [N] initial cached entries per sequence (>= 0).  window,
+ * batch >= 1, max_new >= 1.  *out receives the scheduler (free it with
+ * specdec_sched_destroy). */
+specdec_status_t specdec_sched_create(const int32_t* lens, int32_t N, int32_t window, int32_t batch,
+                                      int32_t max_new, int32_t sort_by_length, int32_t eos_id,
+                                      specdec_sched_t** out);
+void specdec_sched_destroy(specdec_sched_t* s);
+
+/* slots, lens: host int32 [batch] out (lens may be NULL): the batch's slots in
+ * row order and their lengths.  Calling it again before a commit returns the
+ * same batch. */
+specdec_status_t specdec_sched_next_batch(specdec_sched_t* s, int32_t* slots, int32_t* lens,
+                                          specdec_batch_info_t* info);
+
+/* Outcome of the step run on the last batch: n_acc host int32 [B]; tokens host
+ * int32 [B][k+1] (the predictions; row i appended tokens[i][0 .. n_acc[i]]),
+ * may be NULL when eos_id < 0. */
+specdec_status_t specdec_sched_commit(specdec_sched_t* s, const int32_t* n_acc,
+                                      const int32_t* tokens, int32_t k);
+
+/* Current lengths (host int32 [N] out), and the number of active sequences. */
+specdec_status_t specdec_sched_lengths(const specdec_sched_t* s, int32_t* lens);
+int32_t specdec_sched_active(const specdec_sched_t* s);
+
 /*
  * Kernel timers (for measurement; off by default).  specdec_timing_enable
  * takes a mask of kernels (bit 1 << SPECDEC_KERNEL_*; 0 turns the timers
@@ -220,13 +366,15 @@ specdec_status_t specdec_step(const void* logits, int32_t dtype, const int32_t* 
  * the launch stream around its launch (verify: around its two launches).
  * specdec_timing_query waits for the recorded events, adds their durations to
  * the totals of `kernel` (0 = verify, 1 = realign, with the fused position ids
- * / mask in specdec_step, 2 = position ids / mask alone) and returns the
- * totals since the last reset.
+ * / mask in specdec_step, 2 = position ids / mask alone, 3 = batch gather,
+ * 4 = write-back) and returns the totals since the last reset.
  */
 #define SPECDEC_KERNEL_VERIFY 0
 #define SPECDEC_KERNEL_REALIGN 1
 #define SPECDEC_KERNEL_POSMASK 2
-#define SPECDEC_TIMING_ALL 7
+#define SPECDEC_KERNEL_GATHER 3
+#define SPECDEC_KERNEL_WRITEBACK 4
+#define SPECDEC_TIMING_ALL 31
 specdec_status_t specdec_timing_enable(int32_t kernel_mask);
 specdec_status_t specdec_timing_reset(void);
 specdec_status_t specdec_timing_query(int32_t kernel, double* total_ms, int64_t* launches);

@@ -36,7 +36,9 @@ __device__ __forceinline__ int32_t load_invariant(const int32_t* p) {
 // kPieces pieces of kTpb vectors (one per lane) starting at `base`, the
 // pieces kSplit vectors apart.  Each piece is padding (stores only), content
 // (one load and one store per lane), or the boundary / ragged end, where the
-// source index is clamped into the kept range so every load is in bounds.
+// source index is clamped into the kept range so every load is in bounds.  A
+// span with no kept vector (zero_end >= total) is padding throughout and
+// loads nothing.
 template <int kPieces, int kTpb, int kSplit, int kNt>
 __device__ __forceinline__ void split_pieces(const u32x4* s, u32x4* d, int64_t base, int64_t total,
                                              int64_t zero_end, int64_t shift) {
@@ -49,7 +51,7 @@ __device__ __forceinline__ void split_pieces(const u32x4* s, u32x4* d, int64_t b
     const int64_t p0 = base + static_cast<int64_t>(j) * kSplit;  // first vector of the piece
     if (p0 >= zero_end && p0 + kTpb <= total) {
       v[j] = ld16<(kNt & 1) != 0>(s + (p0 + t - shift));
-    } else if (p0 + kTpb > zero_end && p0 < total) {
+    } else if (p0 + kTpb > zero_end && p0 < total && zero_end < total) {
       int64_t si = p0 + t - shift;
       si = si < lo ? lo : (si > hi ? hi : si);
       v[j] = ld16<(kNt & 1) != 0>(s + si);

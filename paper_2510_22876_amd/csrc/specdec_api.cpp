@@ -32,6 +32,15 @@ specdec_status_t ok() {
   return SPECDEC_OK;
 }
 
+}  // namespace
+
+namespace specdec {
+void set_last_error(const char* msg) { g_last_error = msg; }
+void clear_last_error() { g_last_error.clear(); }
+}  // namespace specdec
+
+namespace {
+
 specdec_status_t hip_fail(hipError_t e, const char* what) {
   return fail(SPECDEC_ERR_HIP, "%s: %s (%d)", what, hipGetErrorString(e), static_cast<int>(e));
 }
@@ -49,6 +58,8 @@ int logit_bytes(int32_t dtype) {
 
 // ---- kernel timers -------------------------------------------------------------
 
+constexpr int kTimedKernels = 5;
+
 struct TimedLaunch {
   int kernel;
   hipEvent_t begin, end;
@@ -59,8 +70,8 @@ struct Timers {
   int32_t mask = 0;
   std::vector<TimedLaunch> pending;
   std::vector<hipEvent_t> pool;
-  double total_ms[3] = {0, 0, 0};
-  int64_t launches[3] = {0, 0, 0};
+  double total_ms[kTimedKernels] = {};
+  int64_t launches[kTimedKernels] = {};
 };
 
 Timers& timers() {
@@ -220,6 +231,47 @@ specdec_status_t check_posmask_args(const int32_t* pad_out, const int32_t* w_new
   if (!pad_out || !w_new || !pos || !mask) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "NULL pad_out / w_new / pos / mask");
   if (!aligned(pos, 8)) return fail(SPECDEC_ERR_UNSUPPORTED, "pos not 8-byte aligned");
   if (!aligned(pad_out, 4) || !aligned(w_new, 4)) return fail(SPECDEC_ERR_UNSUPPORTED, "int32 tensor not 4-byte aligned");
+  return SPECDEC_OK;
+}
+
+
+bool ranges_overlap(const void* a, int64_t abytes, const void* b, int64_t bbytes) {
+  const uintptr_t a0 = reinterpret_cast<uintptr_t>(a), b0 = reinterpret_cast<uintptr_t>(b);
+  return a0 < b0 + static_cast<uintptr_t>(bbytes) && b0 < a0 + static_cast<uintptr_t>(abytes);
+}
+
+// Common checks of the pool / batch pair of a gather or write-back.
+specdec_status_t check_pool_pair(const specdec_kv_t* pool, const specdec_kv_t* batch, int32_t B, int32_t Lb,
+                                 int32_t k, int64_t batch_cap_min, const int32_t* lens, const int32_t* slots) {
+  specdec_status_t s = check_kv(pool, "pool");
+  if (s) return s;
+  s = check_kv(batch, "batch");
+  if (s) return s;
+  if (B < 0 || B > SPECDEC_MAX_B) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "B=%d outside [0,%d]", B, SPECDEC_MAX_B);
+  if (k < 0 || k > SPECDEC_MAX_K) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "k=%d outside [0,%d]", k, SPECDEC_MAX_K);
+  if (Lb < 0 || Lb > SPECDEC_MAX_WIDTH)
+    return fail(SPECDEC_ERR_INVALID_ARGUMENT, "Lb=%d outside [0,%d]", Lb, SPECDEC_MAX_WIDTH);
+  if (batch->B != B) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "batch has %d rows, B=%d", batch->B, B);
+  if (pool->L != batch->L || pool->H != batch->H || pool->D != batch->D)
+    return fail(SPECDEC_ERR_INVALID_ARGUMENT, "pool and batch shapes differ");
+  if (B == 0) return SPECDEC_OK;
+  if (pool->B < 1) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "the pool has no slot");
+  if (!lens || !slots) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "NULL lens / slots");
+  if (!aligned(lens, 4) || !aligned(slots, 4)) return fail(SPECDEC_ERR_UNSUPPORTED, "int32 tensor not 4-byte aligned");
+  const int64_t spans = static_cast<int64_t>(batch->L) * 2 * B * batch->H;
+  if (spans > 0) {
+    if (batch->cap < batch_cap_min)
+      return fail(SPECDEC_ERR_INVALID_ARGUMENT, "batch cap=%lld < %lld", (long long)batch->cap, (long long)batch_cap_min);
+    if (pool->cap > 0 && batch->cap > 0 && ranges_overlap(pool->data, kv_bytes(pool), batch->data, kv_bytes(batch)))
+      return fail(SPECDEC_ERR_INVALID_ARGUMENT, "pool and batch caches overlap");
+  }
+  return SPECDEC_OK;
+}
+
+specdec_status_t check_stride(int64_t stride, int64_t need, const char* name) {
+  if (stride < need || stride > static_cast<int64_t>(SPECDEC_MAX_WIDTH) + SPECDEC_MAX_K + 2)
+    return fail(SPECDEC_ERR_INVALID_ARGUMENT, "%s=%lld outside [%lld, %lld]", name, (long long)stride, (long long)need,
+                (long long)SPECDEC_MAX_WIDTH + SPECDEC_MAX_K + 2);
   return SPECDEC_OK;
 }
 
@@ -408,6 +460,115 @@ specdec_status_t specdec_step(const void* logits, int32_t dtype, const int32_t* 
   return ok();
 }
 
+specdec_status_t specdec_gather_batch(const specdec_kv_t* pool, const int32_t* pool_tok, int64_t pool_tok_stride,
+                                      const int32_t* lens, const int32_t* slots, int32_t B, int32_t Lb, int32_t k,
+                                      const specdec_kv_t* batch, int32_t* batch_tok, int64_t btok_stride,
+                                      int32_t pad_id, int32_t* pads, int64_t* pos, uint8_t* mask, int64_t pm_cap,
+                                      uint32_t* dev_status, void* stream) {
+  specdec_status_t s = check_pool_pair(pool, batch, B, Lb, k, Lb, lens, slots);
+  if (s) return s;
+  if (B == 0) return ok();
+  if (!pads) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "NULL pads");
+  if (!aligned(pads, 4)) return fail(SPECDEC_ERR_UNSUPPORTED, "int32 tensor not 4-byte aligned");
+  if (batch_tok) {
+    if (!pool_tok) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "batch_tok given without pool_tok");
+    if (!aligned(batch_tok, 4) || !aligned(pool_tok, 4)) return fail(SPECDEC_ERR_UNSUPPORTED, "token rows not 4-byte aligned");
+    if ((s = check_stride(btok_stride, static_cast<int64_t>(Lb) + 1, "btok_stride"))) return s;
+    if ((s = check_stride(pool_tok_stride, 1, "pool_tok_stride"))) return s;
+    if (ranges_overlap(batch_tok, static_cast<int64_t>(B) * btok_stride * 4, pool_tok,
+                       static_cast<int64_t>(pool->B) * pool_tok_stride * 4))
+      return fail(SPECDEC_ERR_INVALID_ARGUMENT, "batch and pool token rows overlap");
+  }
+  if ((pos == nullptr) != (mask == nullptr)) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "give both pos and mask, or neither");
+  if (pos) {
+    if (!aligned(pos, 8)) return fail(SPECDEC_ERR_UNSUPPORTED, "pos not 8-byte aligned");
+    if (pm_cap < static_cast<int64_t>(Lb) + k + 1 || pm_cap > static_cast<int64_t>(SPECDEC_MAX_WIDTH) + SPECDEC_MAX_K + 1)
+      return fail(SPECDEC_ERR_INVALID_ARGUMENT, "pm_cap=%lld < Lb+k+1=%lld", (long long)pm_cap,
+                  (long long)Lb + k + 1);
+  }
+  if (dev_status && !aligned(dev_status, 4)) return fail(SPECDEC_ERR_UNSUPPORTED, "dev_status not 4-byte aligned");
+  specdec::GatherLaunch p{};
+  p.pool = pool->data;
+  p.pool_cap = pool->cap;
+  p.N = pool->B;
+  p.pool_tok = pool_tok;
+  p.pool_tok_stride = pool_tok_stride;
+  p.lens = lens;
+  p.slots = slots;
+  p.L = batch->L;
+  p.B = B;
+  p.H = batch->H;
+  p.D = batch->D;
+  p.Lb = Lb;
+  p.k = k;
+  p.batch = batch->data;
+  p.batch_cap = batch->cap;
+  p.batch_tok = batch_tok;
+  p.btok_stride = btok_stride;
+  p.pad_id = pad_id;
+  p.pads = pads;
+  p.pos = pos;
+  p.mask = mask;
+  p.pm_cap = pm_cap;
+  p.dev_status = dev_status;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  hipError_t e = timed(SPECDEC_KERNEL_GATHER, st, [&] { return specdec::launch_gather(p, st); });
+  if (e != hipSuccess) return hip_fail(e, "gather launch");
+  return ok();
+}
+
+specdec_status_t specdec_scatter_accepted(const specdec_kv_t* batch, const int32_t* pads, const int32_t* tokens,
+                                          const int32_t* n_acc, const int32_t* slots, int32_t B, int32_t k,
+                                          int32_t Lb, const specdec_kv_t* pool, int32_t* pool_tok,
+                                          int64_t pool_tok_stride, int32_t* lens, int32_t* batch_tok,
+                                          int64_t btok_stride, int32_t mode, uint32_t* dev_status, void* stream) {
+  if (mode != SPECDEC_WRITEBACK_FULL && mode != SPECDEC_WRITEBACK_APPEND)
+    return fail(SPECDEC_ERR_INVALID_ARGUMENT, "write-back mode %d unknown", mode);
+  specdec_status_t s = check_pool_pair(pool, batch, B, Lb, k, static_cast<int64_t>(Lb) + k + 1, lens, slots);
+  if (s) return s;
+  if (B == 0) return ok();
+  if (!pads || !tokens || !n_acc || !pool_tok)
+    return fail(SPECDEC_ERR_INVALID_ARGUMENT, "NULL pads / tokens / n_acc / pool_tok");
+  if (!aligned(pads, 4) || !aligned(tokens, 4) || !aligned(n_acc, 4) || !aligned(pool_tok, 4))
+    return fail(SPECDEC_ERR_UNSUPPORTED, "int32 tensor not 4-byte aligned");
+  if ((s = check_stride(pool_tok_stride, 1, "pool_tok_stride"))) return s;
+  if (batch_tok) {
+    if (!aligned(batch_tok, 4)) return fail(SPECDEC_ERR_UNSUPPORTED, "batch_tok not 4-byte aligned");
+    if ((s = check_stride(btok_stride, static_cast<int64_t>(Lb) + k + 2, "btok_stride"))) return s;
+    if (ranges_overlap(batch_tok, static_cast<int64_t>(B) * btok_stride * 4, pool_tok,
+                       static_cast<int64_t>(pool->B) * pool_tok_stride * 4))
+      return fail(SPECDEC_ERR_INVALID_ARGUMENT, "batch and pool token rows overlap");
+  }
+  if (dev_status && !aligned(dev_status, 4)) return fail(SPECDEC_ERR_UNSUPPORTED, "dev_status not 4-byte aligned");
+  specdec::WritebackLaunch p{};
+  p.batch = batch->data;
+  p.batch_cap = batch->cap;
+  p.pads = pads;
+  p.tokens = tokens;
+  p.n_acc = n_acc;
+  p.slots = slots;
+  p.L = batch->L;
+  p.B = B;
+  p.H = batch->H;
+  p.D = batch->D;
+  p.k = k;
+  p.Lb = Lb;
+  p.pool = pool->data;
+  p.pool_cap = pool->cap;
+  p.N = pool->B;
+  p.pool_tok = pool_tok;
+  p.pool_tok_stride = pool_tok_stride;
+  p.lens = lens;
+  p.batch_tok = batch_tok;
+  p.btok_stride = btok_stride;
+  p.append_only = mode == SPECDEC_WRITEBACK_APPEND;
+  p.dev_status = dev_status;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  hipError_t e = timed(SPECDEC_KERNEL_WRITEBACK, st, [&] { return specdec::launch_writeback(p, st); });
+  if (e != hipSuccess) return hip_fail(e, "write-back launch");
+  return ok();
+}
+
 specdec_status_t specdec_timing_enable(int32_t kernel_mask) {
   if (kernel_mask < 0 || kernel_mask > SPECDEC_TIMING_ALL)
     return fail(SPECDEC_ERR_INVALID_ARGUMENT, "timing mask %d outside [0,%d]", kernel_mask, SPECDEC_TIMING_ALL);
@@ -426,7 +587,7 @@ specdec_status_t specdec_timing_reset(void) {
     t.pool.push_back(p.end);
   }
   t.pending.clear();
-  for (int i = 0; i < 3; ++i) {
+  for (int i = 0; i < kTimedKernels; ++i) {
     t.total_ms[i] = 0;
     t.launches[i] = 0;
   }
@@ -434,7 +595,7 @@ specdec_status_t specdec_timing_reset(void) {
 }
 
 specdec_status_t specdec_timing_query(int32_t kernel, double* total_ms, int64_t* launches) {
-  if (kernel < 0 || kernel > 2) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "unknown kernel id %d", kernel);
+  if (kernel < 0 || kernel >= kTimedKernels) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "unknown kernel id %d", kernel);
   Timers& t = timers();
   std::lock_guard<std::mutex> lk(t.mu);
   for (const TimedLaunch& p : t.pending) {

@@ -69,6 +69,65 @@ int64_t verify_chunks(int64_t rows, int64_t V);
 // Workgroups of the realign grid (without the fused position-id blocks).
 int64_t realign_grid_blocks(int64_t nspans, int64_t W_in, int32_t D, bool in_place);
 
+// EXSpec batch gather (pool slots -> left-padded batch, token rows, paddings,
+// position ids / mask).
+struct GatherLaunch {
+  const void* pool;
+  int64_t pool_cap;
+  int32_t N;
+  const int32_t* pool_tok;     // may be null when batch_tok is
+  int64_t pool_tok_stride;
+  const int32_t* lens;
+  const int32_t* slots;
+  int32_t L, B, H, D;
+  int32_t Lb, k;
+  void* batch;
+  int64_t batch_cap;
+  int32_t* batch_tok;          // may be null
+  int64_t btok_stride;
+  int32_t pad_id;
+  int32_t* pads;
+  int64_t* pos;                // may be null (then mask is too)
+  uint8_t* mask;
+  int64_t pm_cap;
+  uint32_t* dev_status;
+};
+
+// EXSpec write-back (batch rows -> pool slots).
+struct WritebackLaunch {
+  const void* batch;
+  int64_t batch_cap;
+  const int32_t* pads;
+  const int32_t* tokens;
+  const int32_t* n_acc;
+  const int32_t* slots;
+  int32_t L, B, H, D;
+  int32_t k, Lb;
+  void* pool;
+  int64_t pool_cap;
+  int32_t N;
+  int32_t* pool_tok;
+  int64_t pool_tok_stride;
+  int32_t* lens;
+  int32_t* batch_tok;          // may be null
+  int64_t btok_stride;
+  bool append_only;
+  uint32_t* dev_status;
+};
+
+hipError_t launch_gather(const GatherLaunch& p, hipStream_t stream);
+hipError_t launch_writeback(const WritebackLaunch& p, hipStream_t stream);
+
+// Message of the calling thread's last failure (specdec_last_error), for
+// entry points defined outside the main API source.
+void set_last_error(const char* msg);
+void clear_last_error();
+
+// Largest number of work-items one dispatch may hold (2^32 - 1, or lower when
+// the environment variable SPECDEC_MAX_LAUNCH_ITEMS asks for it, to exercise
+// the split of a grid over several launches).
+int64_t max_launch_items();
+
 hipError_t launch_verify(const VerifyLaunch& p, hipStream_t stream);
 hipError_t launch_realign(const RealignLaunch& p, hipStream_t stream);
 hipError_t launch_posmask(const PosmaskLaunch& p, hipStream_t stream);

@@ -588,6 +588,15 @@ static_assert(kOopTpb % 64 == 0 && kInTpb % 64 == 0, "workgroups are whole wavef
 
 }  // namespace
 
+int64_t max_launch_items() {
+  int64_t max_items = 0xFFFFFFFFLL;
+  if (const char* env = std::getenv("SPECDEC_MAX_LAUNCH_ITEMS")) {
+    const long long v = std::atoll(env);
+    if (v > 0 && v < max_items) max_items = v;
+  }
+  return max_items;
+}
+
 int64_t verify_chunk_elems(int64_t rows, int64_t V) {
   // about 2048 workgroups in total, each scanning 2048..16384 elements, and
   // at most kMaxVerifyChunks workgroups per row
@@ -687,14 +696,8 @@ hipError_t launch_realign(const RealignLaunch& p, hipStream_t stream) {
   const int64_t chunks = p.in_place ? 1 : realign_grid_blocks(1, p.W_in, p.D, false);
   a.chunks = static_cast<uint32_t>(chunks);
   // one dispatch holds fewer than 2^32 work-items: split the spans over
-  // several launches when the cache is larger than that (the environment
-  // variable SPECDEC_MAX_LAUNCH_ITEMS lowers the cap, to exercise the split)
-  int64_t max_items = 0xFFFFFFFFLL;
-  if (const char* env = std::getenv("SPECDEC_MAX_LAUNCH_ITEMS")) {
-    const long long v = std::atoll(env);
-    if (v > 0 && v < max_items) max_items = v;
-  }
-  const int64_t max_blocks = (max_items / tpb) - extra;
+  // several launches when the cache is larger than that
+  const int64_t max_blocks = (max_launch_items() / tpb) - extra;
   const int64_t spans_per_launch = max_blocks / chunks;
   if (spans_per_launch < 1) return hipErrorInvalidConfiguration;
   const dim3 block(tpb);

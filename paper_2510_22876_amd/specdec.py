@@ -17,14 +17,18 @@ _LIB_PATH = Path(__file__).resolve().parent / "libspecdec.so"
 OK, ERR_INVALID_ARGUMENT, ERR_UNSUPPORTED, ERR_HIP, ERR_WORKSPACE = 0, 1, 2, 3, 4
 F32, BF16, F16 = 0, 1, 2
 DTYPE_OF = {torch.float32: F32, torch.bfloat16: BF16, torch.float16: F16}
-KERNEL_VERIFY, KERNEL_REALIGN, KERNEL_POSMASK = 0, 1, 2
-TIMING_ALL = 7
+KERNEL_VERIFY, KERNEL_REALIGN, KERNEL_POSMASK, KERNEL_GATHER, KERNEL_WRITEBACK = 0, 1, 2, 3, 4
+TIMING_ALL = 31
 DEV_BAD_PAD_IN, DEV_BAD_ACCEPT, DEV_BAD_WIDTH, DEV_BAD_PAD_OUT = 1, 2, 4, 8
+DEV_BAD_SLOT, DEV_SLOT_LEN = 0x10, 0x20
+WRITEBACK_FULL, WRITEBACK_APPEND = 0, 1
 
 EXPORTED = (
     "specdec_abi_version", "specdec_last_error", "specdec_workspace_bytes", "specdec_workspace_init",
     "specdec_verify_greedy", "specdec_realign_kv", "specdec_build_posmask", "specdec_realign_tokens",
-    "specdec_step",
+    "specdec_step", "specdec_gather_batch", "specdec_scatter_accepted",
+    "specdec_sched_create", "specdec_sched_destroy", "specdec_sched_next_batch", "specdec_sched_commit",
+    "specdec_sched_lengths", "specdec_sched_active",
     "specdec_timing_enable", "specdec_timing_reset", "specdec_timing_query",
 )
 
@@ -39,6 +43,12 @@ class KV(ctypes.Structure):
     """specdec_kv_t: bf16 cache [L][2][B][H][cap][D]."""
     _fields_ = [("data", ctypes.c_void_p), ("L", ctypes.c_int32), ("B", ctypes.c_int32),
                 ("H", ctypes.c_int32), ("D", ctypes.c_int32), ("cap", ctypes.c_int64)]
+
+
+class BatchInfo(ctypes.Structure):
+    """specdec_batch_info_t."""
+    _fields_ = [("B", ctypes.c_int32), ("width", ctypes.c_int32), ("same_length", ctypes.c_int32),
+                ("reuse", ctypes.c_int32)]
 
 
 def _load(path: Path = _LIB_PATH) -> ctypes.CDLL:
@@ -58,11 +68,23 @@ def _load(path: Path = _LIB_PATH) -> ctypes.CDLL:
     lib.specdec_realign_tokens.argtypes = [P, i64, P, i64, P, P, P, P, i32, i32, i32, i32, P, P]
     lib.specdec_step.argtypes = [P, i32, P, P, i32, i32, i32, i32, pKV, pKV, P, P, P, P, P, P, P, i64,
                                  P, i64, P, i64, i32, P, sz, P, P, P]
+    lib.specdec_gather_batch.argtypes = [pKV, P, i64, P, P, i32, i32, i32, pKV, P, i64, i32, P, P, P, i64, P, P]
+    lib.specdec_scatter_accepted.argtypes = [pKV, P, P, P, P, i32, i32, i32, pKV, P, i64, P, P, i64, i32, P, P]
+    lib.specdec_sched_create.argtypes = [P, i32, i32, i32, i32, i32, i32, ctypes.POINTER(P)]
+    lib.specdec_sched_destroy.argtypes = [P]
+    lib.specdec_sched_destroy.restype = None
+    lib.specdec_sched_next_batch.argtypes = [P, P, P, ctypes.POINTER(BatchInfo)]
+    lib.specdec_sched_commit.argtypes = [P, P, P, i32]
+    lib.specdec_sched_lengths.argtypes = [P, P]
+    lib.specdec_sched_active.argtypes = [P]
+    lib.specdec_sched_active.restype = i32
     lib.specdec_timing_enable.argtypes = [i32]
     lib.specdec_timing_query.argtypes = [i32, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)]
     for name in ("specdec_workspace_init", "specdec_verify_greedy", "specdec_realign_kv",
                  "specdec_build_posmask", "specdec_realign_tokens", "specdec_step", "specdec_timing_enable",
-                 "specdec_timing_reset", "specdec_timing_query"):
+                 "specdec_timing_reset", "specdec_timing_query", "specdec_gather_batch",
+                 "specdec_scatter_accepted", "specdec_sched_create", "specdec_sched_next_batch",
+                 "specdec_sched_commit", "specdec_sched_lengths"):
         getattr(lib, name).restype = ctypes.c_int
     return lib
 
@@ -231,6 +253,116 @@ def specdec_step(logits, draft, pad_in, W_in: int, src, dst, tokens, n_acc, bonu
         _p(workspace), workspace.numel() * workspace.element_size(),
         _p(dev_status), ctypes.byref(host) if sync_w_new else None, _stream(stream)))
     return host.value if sync_w_new else None
+
+
+def specdec_gather_batch(pool, pool_tok, lens, slots, Lb: int, batch, pads, batch_tok=None, pos=None, mask=None,
+                         k: int = 0, pad_id: int = 0, dev_status=None, stream=None) -> None:
+    """EXSpec's GetBatch: rows ``slots`` of the pool gathered into ``batch``,
+    left-padded to width ``Lb`` (with token rows, paddings and, when given,
+    position ids / mask over [0, Lb + k + 1))."""
+    pl = kv_desc(pool)
+    bt = kv_desc(batch)
+    B = bt.B
+    _req("lens", lens, (pl.B,), torch.int32)
+    _req("slots", slots, (B,), torch.int32)
+    _req("pads", pads, (B,), torch.int32)
+    _req("dev_status", dev_status, (1,), torch.int32, optional=True)
+    tok_stride = btok_stride = 0
+    if batch_tok is not None:
+        _req("pool_tok", pool_tok, (pl.B, pool_tok.shape[1]), torch.int32)
+        _req("batch_tok", batch_tok, (B, batch_tok.shape[1]), torch.int32)
+        tok_stride, btok_stride = pool_tok.shape[1], batch_tok.shape[1]
+    pm_cap = 0
+    if pos is not None or mask is not None:
+        _req("pos", pos, (B, pos.shape[1]), torch.int64)
+        _req("mask", mask, (B, pos.shape[1]), torch.uint8)
+        pm_cap = pos.shape[1]
+    _check(lib.specdec_gather_batch(ctypes.byref(pl), _p(pool_tok) if batch_tok is not None else None, tok_stride,
+                                    _p(lens), _p(slots), B, Lb, k, ctypes.byref(bt), _p(batch_tok), btok_stride,
+                                    pad_id, _p(pads), _p(pos), _p(mask), pm_cap, _p(dev_status), _stream(stream)))
+
+
+def specdec_scatter_accepted(batch, pads, tokens, n_acc, slots, Lb: int, pool, pool_tok, lens, batch_tok=None,
+                             mode: int = WRITEBACK_FULL, dev_status=None, stream=None) -> None:
+    """EXSpec's write-back: each row's unpadded cache up to its accepted
+    entries returns to its pool slot (whole, or only the new entries with
+    ``mode=WRITEBACK_APPEND``); the slot's token list and length grow."""
+    bt = kv_desc(batch)
+    pl = kv_desc(pool)
+    B = bt.B
+    _req("tokens", tokens, (B, tokens.shape[1]), torch.int32)
+    k = tokens.shape[1] - 1
+    _req("pads", pads, (B,), torch.int32)
+    _req("n_acc", n_acc, (B,), torch.int32)
+    _req("slots", slots, (B,), torch.int32)
+    _req("lens", lens, (pl.B,), torch.int32)
+    _req("pool_tok", pool_tok, (pl.B, pool_tok.shape[1]), torch.int32)
+    _req("batch_tok", batch_tok, (B, batch_tok.shape[1] if batch_tok is not None else 0), torch.int32, optional=True)
+    _req("dev_status", dev_status, (1,), torch.int32, optional=True)
+    _check(lib.specdec_scatter_accepted(ctypes.byref(bt), _p(pads), _p(tokens), _p(n_acc), _p(slots), B, k, Lb,
+                                        ctypes.byref(pl), _p(pool_tok), pool_tok.shape[1], _p(lens), _p(batch_tok),
+                                        batch_tok.shape[1] if batch_tok is not None else 0, mode, _p(dev_status),
+                                        _stream(stream)))
+
+
+class SchedBatch:
+    """One batch chosen by the scheduler: its slots (row order), their lengths,
+    the width, and whether it is same-length / the previous batch reused."""
+
+    def __init__(self, slots, lens, width, same_length, reuse):
+        self.slots, self.lens, self.width = slots, lens, width
+        self.same_length, self.reuse = same_length, reuse
+
+
+class Scheduler:
+    """The library's SequencePool scheduler (specdec_sched_*; host only)."""
+
+    def __init__(self, lens, window: int, batch: int, max_new: int, sort_by_length: bool = True,
+                 eos_id: int = -1):
+        import numpy as np
+        ln = np.ascontiguousarray(np.asarray(lens, dtype=np.int32).reshape(-1))
+        self._lib = lib
+        self._h = ctypes.c_void_p(None)
+        self.N = ln.size
+        self.batch = batch
+        _check(lib.specdec_sched_create(ln.ctypes.data if ln.size else None, ln.size, window, batch, max_new,
+                                        1 if sort_by_length else 0, eos_id, ctypes.byref(self._h)))
+
+    def __del__(self):
+        h = getattr(self, "_h", None)
+        if h is not None and h.value:
+            self._lib.specdec_sched_destroy(h)
+            self._h = None
+
+    def next_batch(self) -> SchedBatch | None:
+        import numpy as np
+        slots = np.zeros(max(self.batch, 1), np.int32)
+        lens = np.zeros(max(self.batch, 1), np.int32)
+        info = BatchInfo()
+        _check(lib.specdec_sched_next_batch(self._h, slots.ctypes.data, lens.ctypes.data, ctypes.byref(info)))
+        if info.B == 0:
+            return None
+        return SchedBatch([int(x) for x in slots[:info.B]], [int(x) for x in lens[:info.B]], int(info.width),
+                          bool(info.same_length), bool(info.reuse))
+
+    def commit(self, batch: SchedBatch, n_acc, appended) -> None:
+        """n_acc[i] accepted drafts; appended[i] the n_acc[i] + 1 tokens row i gained."""
+        import numpy as np
+        na = np.ascontiguousarray(np.asarray(n_acc, np.int32).reshape(-1))
+        k = int(max(len(a) for a in appended)) - 1 if len(appended) else 0
+        tok = np.full((max(na.size, 1), k + 1), -1, np.int32)
+        for i, a in enumerate(appended):
+            tok[i, : len(a)] = a
+        _check(lib.specdec_sched_commit(self._h, na.ctypes.data, tok.ctypes.data, k))
+
+    def lengths(self) -> list:
+        import numpy as np
+        out = np.zeros(max(self.N, 1), np.int32)
+        _check(lib.specdec_sched_lengths(self._h, out.ctypes.data))
+        return [int(x) for x in out[: self.N]]
+
+    def has_active(self) -> bool:
+        return lib.specdec_sched_active(self._h) > 0
 
 
 def timing_enable(on=True) -> None:

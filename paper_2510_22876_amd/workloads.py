@@ -325,3 +325,41 @@ def make_token_rows(w: Workload, pad_in: np.ndarray, W_in: int, stride: int, see
         p = int(pad_in[i])
         rows[i, p:L + 1] = r.integers(0, max(w.V, 1), size=L + 1 - p)
     return torch.as_tensor(rows, device=device)
+
+
+# ---- EXSpec sequence pool ------------------------------------------------------
+
+_T_POOL_LEN, _T_POOL_KV, _T_POOL_TOK, _T_POOL_SLOTS = 20, 21, 22, 23
+
+
+def pool_lengths(w: Workload, N: int, seed: int = 0) -> np.ndarray:
+    """Cached entries of N pooled sequences, drawn from the workload's prompt
+    distribution (int32 [N])."""
+    return prompt_lengths(w.scaled(B=N), seed + 7919 * _T_POOL_LEN).astype(np.int32)
+
+
+def make_pool(w: Workload, lens: np.ndarray, cap: int, tok_stride: int, seed: int = 0, device="cpu",
+              fill: float = 0.0):
+    """Sequence pool of EXSpec: cache bf16 [L][2][N][H][cap][D] whose slot s
+    holds lens[s] entries (N(0,1) rounded to bf16) in columns [0, lens[s]) and
+    ``fill`` beyond; token rows int32 [N][tok_stride] holding lens[s] + 1
+    tokens (uniform in [0, V): the cached tokens and the pending one) and -1
+    beyond."""
+    lens = np.asarray(lens, np.int64)
+    N = lens.size
+    L, H, D = w.L, w.H, w.D
+    pool = torch.empty((L, 2, N, H, cap, D), dtype=torch.bfloat16, device=device)
+    col = torch.arange(cap, device=device)
+    live = (col.view(1, cap) < torch.as_tensor(lens, device=device).view(N, 1)).view(N, 1, cap, 1)
+    fill_t = torch.full((), fill, dtype=torch.bfloat16, device=device)
+    for l in range(L):
+        for kvi in range(2):
+            g = torch.Generator(device=device)
+            g.manual_seed(_torch_seed(seed, _T_POOL_KV, 0, l * 2 + kvi))
+            vals = torch.randn((N, H, cap, D), generator=g, device=device, dtype=torch.float32).to(torch.bfloat16)
+            pool[l, kvi].copy_(torch.where(live, vals, fill_t))
+    r = _rng(seed, _T_POOL_TOK)
+    tok = np.full((N, tok_stride), -1, dtype=np.int32)
+    for s in range(N):
+        tok[s, : lens[s] + 1] = r.integers(0, max(w.V, 1), size=int(lens[s]) + 1)
+    return pool, torch.as_tensor(tok, device=device)

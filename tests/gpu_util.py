@@ -218,3 +218,81 @@ def check_spans_vs_oracle(w, spans, src_spans, dst_spans, pad_in, v, W_in):
         W = v["w_new"]
         e = exp.reshape(2, W_in, w.D)[:, :W]
         assert np.array_equal(got[:, :W], e), f"span {s}: " + _first_diff(got[:, :W], e)
+
+
+class HipBackend:
+    """Every step of the method through the library's C ABI, on device
+    tensors: the GPU counterpart of ``tests.exspec_loop.OracleBackend``.
+    Pool and batch caches are bf16 tensors; token rows, lengths and slots are
+    int32 tensors.  ``writeback`` picks the write-back mode."""
+
+    def __init__(self, writeback: int | None = None, device="cuda"):
+        from paper_2510_22876_amd import specdec as sd
+        self.sd = sd
+        self.dev = device
+        self.writeback = sd.WRITEBACK_FULL if writeback is None else writeback
+        self.status = torch.zeros(1, dtype=torch.int32, device=device)
+
+    def to_host(self, x):
+        if isinstance(x, torch.Tensor):
+            if x.dtype == torch.bfloat16:
+                return bits(x)
+            return x.cpu().numpy()
+        return x
+
+    def from_host(self, x):
+        if isinstance(x, torch.Tensor):
+            return x.to(self.dev)
+        x = np.asarray(x)
+        if x.dtype == np.uint16:
+            return torch.from_numpy(np.ascontiguousarray(x).view(np.int16)).to(self.dev).view(torch.bfloat16)
+        return torch.from_numpy(np.ascontiguousarray(x)).to(self.dev)
+
+    def check_status(self):
+        st = int(self.status.cpu()[0])
+        assert st == 0, f"device flagged {st:#x}"
+
+    def gather(self, pool, pool_tok, lens, slots, Lb, batch_cap, btok_stride, pad_id):
+        L, _, N, H, cap, D = pool.shape
+        B = int(slots.numel())
+        batch = torch.full((L, 2, B, H, batch_cap, D), SENT_KV, dtype=torch.int16, device=self.dev).view(torch.bfloat16)
+        btok = torch.zeros((B, btok_stride), dtype=torch.int32, device=self.dev)
+        pads = torch.full((B,), -99, dtype=torch.int32, device=self.dev)
+        self.sd.specdec_gather_batch(pool, pool_tok, lens, slots, Lb, batch, pads, batch_tok=btok, pad_id=pad_id,
+                                     dev_status=self.status)
+        self.check_status()
+        return batch, btok, pads
+
+    def posmask(self, pads, width, k, pm_cap):
+        B = int(pads.numel())
+        pos = torch.full((B, pm_cap), SENT_POS, dtype=torch.int64, device=self.dev)
+        mask = torch.full((B, pm_cap), SENT_MASK, dtype=torch.uint8, device=self.dev)
+        w = torch.tensor([width], dtype=torch.int32, device=self.dev)
+        self.sd.specdec_build_posmask(pads, w, k, pos, mask, self.status)
+        self.check_status()
+        return pos, mask
+
+    def write_window(self, batch, row, col, entries):
+        e = torch.from_numpy(np.ascontiguousarray(entries).view(np.int16)).to(self.dev)
+        batch.view(torch.int16)[:, :, row, :, col: col + entries.shape[3], :] = e
+
+    def verify(self, logits, draft, pads, W_in):
+        B, kp1, V = logits.shape
+        o = self.sd.StepBuffers(B, kp1 - 1, V, W_in + kp1, self.dev)
+        self.sd.specdec_verify_greedy(logits, draft, pads, W_in, o.tokens, o.n_acc, o.bonus, o.pad_out, o.w_new,
+                                      o.workspace, self.status)
+        self.check_status()
+        return dict(tokens=o.tokens, n_acc=o.n_acc, bonus=o.bonus, pad_out=o.pad_out, w_new=o.w_new)
+
+    def scatter(self, batch, pads, tokens, n_acc, slots, Lb, pool, pool_tok, lens, batch_tok):
+        self.sd.specdec_scatter_accepted(batch, pads, tokens, n_acc, slots, Lb, pool, pool_tok, lens,
+                                         batch_tok=batch_tok, mode=self.writeback, dev_status=self.status)
+        self.check_status()
+
+    def realign(self, kv, k, W_in, pads, n_acc, w_new, tokens, s, pad_id):
+        out = torch.zeros_like(kv)
+        self.sd.specdec_realign_kv(kv, out, k, W_in, pads, n_acc, w_new, self.status)
+        s_out = torch.full_like(s, SENT_TOK)
+        self.sd.specdec_realign_tokens(s, s_out, tokens, pads, n_acc, w_new, W_in, pad_id, self.status)
+        self.check_status()
+        return out, s_out

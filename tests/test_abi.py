@@ -183,7 +183,9 @@ def test_realign_tokens_rejects(sd):
 def test_timing_query_rejects_unknown_kernel(sd):
     assert sd.lib.specdec_timing_query(7, None, None) == 1
     assert sd.lib.specdec_timing_enable(0) == 0
-    assert sd.lib.specdec_timing_enable(8) == 1
+    assert sd.lib.specdec_timing_enable(31) == 0
+    assert sd.lib.specdec_timing_enable(32) == 1
+    assert sd.lib.specdec_timing_enable(0) == 0
     assert sd.lib.specdec_timing_enable(-1) == 1
 
 
@@ -191,3 +193,79 @@ def test_workspace_init_argument_checks(sd):
     _no_gpu()
     assert sd.lib.specdec_workspace_init(None, 0, None) == 0
     assert sd.lib.specdec_workspace_init(None, 16, None) == 4
+
+
+POOL = A + (4 << 30)
+BTOK, PTOK = A + (5 << 30), A + (6 << 30)
+
+
+def _gather(sd, pool=None, batch=None, **over):
+    pool = pool if pool is not None else _kv(sd, data=POOL, B=5, cap=64)
+    batch = batch if batch is not None else _kv(sd, B=2, cap=32)
+    args = dict(pool_tok=PTOK, pool_tok_stride=65, lens=A, slots=A, B=2, Lb=20, k=3, batch_tok=BTOK,
+                btok_stride=21, pad_id=-1, pads=A, pos=A, mask=A, pm_cap=24, status=None, stream=None)
+    args.update(over)
+    a = list(args.values())
+    return sd.lib.specdec_gather_batch(ctypes.byref(pool), *a[:7], ctypes.byref(batch), *a[7:])
+
+
+def test_gather_rejects(sd):
+    _no_gpu()
+    K = lambda **kw: _kv(sd, **kw)
+    assert _gather(sd, Lb=-1) == 1
+    assert _gather(sd, Lb=33) == 1                                   # batch cap < Lb
+    assert _gather(sd, B=3) == 1                                     # batch rows differ
+    assert _gather(sd, batch=K(B=2, cap=32, H=3)) == 1               # shapes differ
+    assert _gather(sd, pool=K(data=A + 4096, B=5, cap=64)) == 1      # pool overlaps the batch
+    assert _gather(sd, pool=K(data=POOL, B=0, cap=64)) == 1          # no slot
+    assert _gather(sd, lens=None) == 1
+    assert _gather(sd, slots=A + 2) == 2
+    assert _gather(sd, pads=None) == 1
+    assert _gather(sd, btok_stride=20) == 1                          # < Lb + 1
+    assert _gather(sd, pool_tok=None) == 1                           # batch_tok without pool_tok
+    assert _gather(sd, pool_tok_stride=0) == 1
+    assert _gather(sd, batch_tok=PTOK + 64) == 1                     # token rows overlap
+    assert _gather(sd, pm_cap=23) == 1                               # < Lb + k + 1
+    assert _gather(sd, mask=None) == 1                               # pos without mask
+    assert _gather(sd, pos=A + 4) == 2
+    assert _gather(sd, k=65) == 1
+    assert _gather(sd, batch=K(B=2, cap=32, D=12)) == 2
+    assert _gather(sd, B=0, batch=K(B=0, cap=32), lens=None, slots=None, pads=None) == 0   # empty batch
+
+
+def test_gather_valid_arguments_pass_validation(sd):
+    """The same call with valid arguments would be enqueued (only checked with
+    an empty batch here, so no kernel is launched)."""
+    _no_gpu()
+    assert _gather(sd, B=0, batch=_kv(sd, B=0, cap=32)) == 0
+
+
+def _scatter(sd, pool=None, batch=None, **over):
+    pool = pool if pool is not None else _kv(sd, data=POOL, B=5, cap=64)
+    batch = batch if batch is not None else _kv(sd, B=2, cap=32)
+    args = dict(pads=A, tokens=A, n_acc=A, slots=A, B=2, k=3, Lb=20)
+    rest = dict(pool_tok=PTOK, pool_tok_stride=65, lens=A, batch_tok=BTOK, btok_stride=25, mode=0, status=None,
+                stream=None)
+    args.update({k: v for k, v in over.items() if k in args})
+    rest.update({k: v for k, v in over.items() if k in rest})
+    return sd.lib.specdec_scatter_accepted(ctypes.byref(batch), *args.values(), ctypes.byref(pool), *rest.values())
+
+
+def test_scatter_rejects(sd):
+    _no_gpu()
+    K = lambda **kw: _kv(sd, **kw)
+    assert _scatter(sd, mode=2) == 1
+    assert _scatter(sd, Lb=29) == 1                                  # batch cap < Lb + k + 1
+    assert _scatter(sd, k=-1) == 1
+    assert _scatter(sd, B=3) == 1
+    assert _scatter(sd, pool=K(data=A + 4096, B=5, cap=64)) == 1
+    assert _scatter(sd, pads=None) == 1
+    assert _scatter(sd, tokens=None) == 1
+    assert _scatter(sd, n_acc=A + 2) == 2
+    assert _scatter(sd, pool_tok=None) == 1
+    assert _scatter(sd, pool_tok_stride=0) == 1
+    assert _scatter(sd, btok_stride=24) == 1                         # < Lb + k + 2
+    assert _scatter(sd, batch_tok=PTOK) == 1                         # token rows overlap
+    assert _scatter(sd, lens=None) == 1
+    assert _scatter(sd, B=0, batch=K(B=0, cap=32), pads=None, tokens=None, n_acc=None, slots=None,
+                    lens=None) == 0

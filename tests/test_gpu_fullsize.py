@@ -98,3 +98,88 @@ def test_chained_in_place_tagged():
             say(f"chained step {step}: tags checked")
         del r
         pad, W0 = v["pad_out"].copy(), v["w_new"]
+
+
+@pytest.mark.parametrize("batch_kind", ["ragged", "same"])
+def test_exspec_full_size(batch_kind):
+    """EXSpec's step at the vicuna7b shape in the benchmark's configuration
+    (pool of 32 sequences, the first 8 gathered, verified, written back in
+    append mode): paddings, token rows and pos/mask against the oracle in
+    full; sampled (layer, row, head) spans of the batch and of the pool after
+    write-back against the oracle; every row of the batch and every slot with
+    torch on the device against the gather / write-back definitions."""
+    from paper_2510_22876_amd import specdec as sd
+    w = wl.WORKLOADS["vicuna7b"]
+    B, k = w.B, w.k
+    N = 4 * B
+    lens = wl.pool_lengths(w, N, 0)
+    if batch_kind == "same":
+        lens[:B] = lens[0]
+    slots = np.arange(B, dtype=np.int32)
+    Lb = int(lens[:B].max())
+    cap = int(lens.max()) + 2 * (k + 1)
+    say(f"exspec full size {batch_kind}: N={N} Lb={Lb} cap={cap}")
+    pool, pool_tok = wl.make_pool(w, lens, cap, cap + 2, 0, device="cuda")
+    spans = sample_spans(w)
+    pool_before = {s: i16(pool[s[0], :, s[1], s[2], :cap, :]).cpu().numpy().view(np.uint16) for s in spans}
+    tok_before = pool_tok.cpu().numpy()
+    bcap = Lb + k + 1
+    batch = torch.empty((w.L, 2, B, w.H, bcap, w.D), dtype=torch.bfloat16, device="cuda")
+    btok = torch.empty((B, bcap + 1), dtype=torch.int32, device="cuda")
+    pads = torch.empty(B, dtype=torch.int32, device="cuda")
+    pos = torch.empty((B, bcap), dtype=torch.int64, device="cuda")
+    mask = torch.empty((B, bcap), dtype=torch.uint8, device="cuda")
+    lens_d = torch.as_tensor(lens, device="cuda")
+    slots_d = torch.as_tensor(slots, device="cuda")
+    logits, draft, *_ = wl.logits_and_drafts(w, 0, 0, device="cuda")
+    o = alloc_outputs(B, k, w.V, bcap)
+    sd.specdec_gather_batch(pool, pool_tok, lens_d, slots_d, Lb, batch, pads, batch_tok=btok, pos=pos, mask=mask,
+                            k=k, pad_id=PAD_ID, dev_status=o.dev_status)
+    wl.write_window(batch, w, Lb, Lb - lens[:B], seed=0, step=1)
+    sd.specdec_verify_greedy(logits, draft, pads, Lb + k + 1, o.tokens, o.n_acc, o.bonus, o.pad_out, o.w_new,
+                             o.workspace, o.dev_status)
+    batch_spans = host_spans(batch, spans, bcap)
+    sd.specdec_scatter_accepted(batch, pads, o.tokens, o.n_acc, slots_d, Lb, pool, pool_tok, lens_d,
+                                batch_tok=btok, mode=sd.WRITEBACK_APPEND, dev_status=o.dev_status)
+    torch.cuda.synchronize()
+    assert int(o.dev_status.cpu()[0]) == 0
+    pads_h = pads.cpu().numpy()
+    assert np.array_equal(pads_h, Lb - lens[:B])
+    if batch_kind == "same":
+        assert not pads_h.any()
+    n_acc = o.n_acc.cpu().numpy()
+    v = oracle.verify(logits.cpu(), w.logit_dtype, draft.cpu().numpy(), pads_h, Lb + k + 1)
+    assert np.array_equal(n_acc, v["n_acc"]) and np.array_equal(o.tokens.cpu().numpy(), v["tokens"])
+    # pos / mask and token rows in full
+    epos, emask = oracle.posmask(pads_h, Lb, k, bcap)
+    assert np.array_equal(pos.cpu().numpy(), epos) and np.array_equal(mask.cpu().numpy(), emask)
+    exp_tok = tok_before.copy()
+    exp_lens = lens.copy()
+    # sampled spans: the gather against the oracle on the span, then the write-back
+    for s in spans:
+        l, i, h = s
+        one = pool_before[(l, slots[i], h)] if (l, slots[i], h) in pool_before else \
+            i16(pool[l, :, slots[i], h, :cap, :]).cpu().numpy().view(np.uint16)
+        got = batch_spans[s]
+        eb, _, _ = oracle.gather_batch(one.reshape(1, 2, 1, 1, cap, w.D), tok_before[slots[i]:slots[i] + 1],
+                                       lens[slots[i]:slots[i] + 1], np.zeros(1, np.int32), Lb, bcap, bcap + 1, PAD_ID)
+        assert np.array_equal(got[:, :Lb], eb.reshape(2, bcap, w.D)[:, :Lb]), f"gathered span {s} differs"
+    # the whole batch and pool on the device: pads +0.0, content = the slot's entries, appended entries
+    for i in range(B):
+        p, n, a = int(pads_h[i]), int(lens[i]), int(n_acc[i]) + 1
+        if p:
+            assert bool((i16(batch[:, :, i, :, :p, :]) == 0).all()), f"row {i}: pads not +0.0"
+        assert torch.equal(i16(batch[:, :, i, :, p:Lb, :]), i16(pool[:, :, slots[i], :, :n, :])), f"row {i} content"
+        assert torch.equal(i16(pool[:, :, slots[i], :, n:n + a, :]), i16(batch[:, :, i, :, Lb:Lb + a, :])), \
+            f"slot {slots[i]}: appended entries"
+    eb_all, et_all, ep_all = oracle.gather_batch(np.zeros((1, 2, N, 1, cap, 8), np.uint16), tok_before, lens, slots,
+                                                 Lb, bcap, bcap + 1, PAD_ID)
+    oracle.scatter_accepted(eb_all, ep_all, v["tokens"], v["n_acc"], slots, Lb,
+                            np.zeros((1, 2, N, 1, cap, 8), np.uint16), exp_tok, exp_lens, batch_tok=et_all)
+    assert np.array_equal(lens_d.cpu().numpy(), exp_lens)
+    assert np.array_equal(pool_tok.cpu().numpy(), exp_tok)
+    got_btok = btok.cpu().numpy()
+    for i in range(B):   # columns [0, Lb + 1 + a): the gathered row and the appended tokens
+        end = Lb + 2 + int(n_acc[i])
+        assert np.array_equal(got_btok[i, :end], et_all[i, :end]), f"batch token row {i}"
+    say(f"exspec full size {batch_kind}: checked, n_acc={n_acc.tolist()}")
