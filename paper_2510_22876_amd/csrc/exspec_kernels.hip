@@ -51,6 +51,7 @@ struct GatherArgs {
   int64_t pm_cap;
   uint32_t* dev_status;
   uint32_t chunks;        // workgroups per span
+  uint32_t misaligned;    // batch spans tiled from the group boundary below them
   uint32_t span_base;     // first span of this launch
   uint32_t pm_blocks;     // position-id / mask workgroups (first launch only)
   uint32_t pm_col_blocks;
@@ -117,15 +118,15 @@ __global__ __launch_bounds__(kTpb) void gather_kernel(GatherArgs a) {
   int32_t slot;
   const int32_t n = gather_row_len(a, row, &slot);
   if (n < 0) return;                                        // flagged by the row's token workgroup
-  const int64_t base = split_base<kPieces, kTpb, kSplit>(sub);
+  u32x4* dspan = a.batch + static_cast<int64_t>(span) * a.batch_span_vecs;
+  const int64_t mis = a.misaligned ? split_misalign<kPieces, kSplit>(dspan) : 0;
+  const int64_t base = split_base<kPieces, kTpb, kSplit>(sub) - mis;
   const int64_t vpc = a.vpc;
   const int64_t total = static_cast<int64_t>(a.Lb) * vpc;
   if (base >= total) return;
   const int64_t pad = (static_cast<int64_t>(a.Lb) - n) * vpc;
   const int64_t pool_span = (static_cast<int64_t>(lk) * a.N + slot) * a.H + h;
-  split_pieces<kPieces, kTpb, kSplit, kNt>(a.pool + pool_span * a.pool_span_vecs,
-                                           a.batch + static_cast<int64_t>(span) * a.batch_span_vecs, base, total,
-                                           pad, pad);
+  split_pieces<kPieces, kTpb, kSplit, kNt>(a.pool + pool_span * a.pool_span_vecs, dspan, base, total, pad, pad);
 }
 
 struct WritebackArgs {
@@ -146,6 +147,7 @@ struct WritebackArgs {
   int64_t btok_stride;
   uint32_t* dev_status;
   uint32_t chunks;        // workgroups per span
+  uint32_t misaligned;    // whole-row mode: pool spans tiled from the group boundary below them
   uint32_t span_base;
   uint32_t meta_blocks;   // one per row (first launch only)
 };
@@ -223,13 +225,13 @@ __global__ __launch_bounds__(kTpb) void writeback_full_kernel(WritebackArgs a) {
   RowBack g;
   if (writeback_row(a, row, g)) return;   // flagged by the row's meta workgroup
   const int64_t vpc = a.vpc;
-  const int64_t base = split_base<kPieces, kTpb, kSplit>(sub);
+  u32x4* dspan = a.pool + ((lkN + g.slot) * a.H + h) * a.pool_span_vecs;
+  const int64_t mis = a.misaligned ? split_misalign<kPieces, kSplit>(dspan) : 0;
+  const int64_t base = split_base<kPieces, kTpb, kSplit>(sub) - mis;
   const int64_t total = static_cast<int64_t>(g.n + g.a) * vpc;
   if (base >= total) return;
-  const int64_t pool_span = (lkN + g.slot) * a.H + h;
-  split_pieces<kPieces, kTpb, kSplit, kNt>(a.batch + static_cast<int64_t>(span) * a.batch_span_vecs,
-                                           a.pool + pool_span * a.pool_span_vecs, base, total, 0,
-                                           -static_cast<int64_t>(g.pad) * vpc);
+  split_pieces<kPieces, kTpb, kSplit, kNt>(a.batch + static_cast<int64_t>(span) * a.batch_span_vecs, dspan, base,
+                                           total, 0, -static_cast<int64_t>(g.pad) * vpc);
 }
 
 // New entries only: pool columns [n, n + a) of the slot receive batch columns
@@ -293,7 +295,8 @@ hipError_t launch_gather(const GatherLaunch& p, hipStream_t stream) {
   const int64_t tok_blocks = static_cast<int64_t>(a.tok_col_blocks) * p.B;
   const int64_t extra = pm_blocks + tok_blocks;
   const int64_t nspans = p.Lb > 0 ? static_cast<int64_t>(p.L) * 2 * p.B * p.H : 0;
-  const int64_t chunks = split_blocks<kPieces, kTpb, kSplit>(static_cast<int64_t>(p.Lb) * a.vpc);
+  a.misaligned = !split_spans_aligned<kPieces, kSplit>(p.batch, a.batch_span_vecs);
+  const int64_t chunks = split_blocks<kPieces, kTpb, kSplit>(static_cast<int64_t>(p.Lb) * a.vpc, a.misaligned != 0);
   a.chunks = static_cast<uint32_t>(chunks > 0 ? chunks : 1);
   const int64_t max_blocks = max_launch_items() / kTpb - extra;
   const int64_t per_launch = max_blocks / a.chunks;
@@ -341,7 +344,9 @@ hipError_t launch_writeback(const WritebackLaunch& p, hipStream_t stream) {
   const int64_t nspans = static_cast<int64_t>(p.L) * 2 * p.B * p.H;
   const int64_t extra = p.B;
   int64_t chunks = 1;
-  if (!p.append_only) chunks = split_blocks<kPieces, kTpb, kSplit>((static_cast<int64_t>(p.Lb) + p.k + 1) * a.vpc);
+  a.misaligned = !p.append_only && !split_spans_aligned<kPieces, kSplit>(p.pool, a.pool_span_vecs);
+  if (!p.append_only)
+    chunks = split_blocks<kPieces, kTpb, kSplit>((static_cast<int64_t>(p.Lb) + p.k + 1) * a.vpc, a.misaligned != 0);
   a.chunks = static_cast<uint32_t>(chunks);
   const int64_t max_blocks = max_launch_items() / kTpb - extra;
   const int64_t per_launch = max_blocks / chunks;

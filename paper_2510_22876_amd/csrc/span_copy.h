@@ -38,7 +38,9 @@ __device__ __forceinline__ int32_t load_invariant(const int32_t* p) {
 // (one load and one store per lane), or the boundary / ragged end, where the
 // source index is clamped into the kept range so every load is in bounds.  A
 // span with no kept vector (zero_end >= total) is padding throughout and
-// loads nothing.
+// loads nothing.  `base` may be negative (a span tiled from the group
+// boundary below its start, see split_misalign): vectors before the span are
+// neither loaded nor stored.
 template <int kPieces, int kTpb, int kSplit, int kNt>
 __device__ __forceinline__ void split_pieces(const u32x4* s, u32x4* d, int64_t base, int64_t total,
                                              int64_t zero_end, int64_t shift) {
@@ -64,11 +66,11 @@ __device__ __forceinline__ void split_pieces(const u32x4* s, u32x4* d, int64_t b
     const int64_t p0 = base + static_cast<int64_t>(j) * kSplit;
     if (p0 >= total) break;
     const int64_t u = p0 + t;
-    if (p0 + kTpb <= zero_end) {
+    if (p0 >= 0 && p0 + kTpb <= zero_end) {
       st16<(kNt & 2) != 0>(d + u, zero);
     } else if (p0 >= zero_end && p0 + kTpb <= total) {
       st16<(kNt & 2) != 0>(d + u, v[j]);
-    } else if (u < total) {
+    } else if (u >= 0 && u < total) {
       st16<(kNt & 2) != 0>(d + u, u >= zero_end ? v[j] : zero);
     }
   }
@@ -83,11 +85,37 @@ __device__ __forceinline__ int64_t split_base(uint32_t sub) {
   return static_cast<int64_t>(grp) * (kPieces * kSplit) + static_cast<int64_t>(sub - grp * kPerGroup) * kTpb;
 }
 
-// Workgroups per span in the split-piece layout for spans of `vecs` vectors.
+// Workgroups per span in the split-piece layout for spans of `vecs` vectors;
+// with `misaligned`, room for one more group (a span tiled from the group
+// boundary below its start).
 template <int kPieces, int kTpb, int kSplit>
-constexpr int64_t split_blocks(int64_t vecs) {
-  return ((vecs + static_cast<int64_t>(kPieces) * kSplit - 1) / (static_cast<int64_t>(kPieces) * kSplit)) *
-         (kSplit / kTpb);
+constexpr int64_t split_blocks(int64_t vecs, bool misaligned = false) {
+  constexpr int64_t kGroup = static_cast<int64_t>(kPieces) * kSplit;
+  return ((vecs + (misaligned ? kGroup - 1 : 0) + kGroup - 1) / kGroup) * (kSplit / kTpb);
+}
+
+// Output spans are tiled in groups of kPieces*kSplit vectors.  When a span
+// does not start on a group boundary of the address space (a capacity that is
+// not a multiple of the group), the tiling starts at the boundary below the
+// span instead: every piece then covers the same aligned 1 KB slots of memory
+// whatever the capacity, which keeps the stores of a group on whole aligned
+// 16 KB blocks (measured on MI355X: about 8% more bandwidth than tiling from
+// a 256-byte-aligned span start).  Returns the span start's offset, in
+// vectors, from that boundary.
+template <int kPieces, int kSplit>
+__device__ __forceinline__ int64_t split_misalign(const u32x4* d) {
+  constexpr uint64_t kGroup = static_cast<uint64_t>(kPieces) * kSplit;
+  static_assert((kGroup & (kGroup - 1)) == 0, "the group is a power of two vectors");
+  return static_cast<int64_t>((reinterpret_cast<uintptr_t>(d) / 16u) & (kGroup - 1));
+}
+
+// True when every span of a buffer (base pointer, span stride in vectors)
+// starts on a group boundary, so no span needs the extra group.
+template <int kPieces, int kSplit>
+inline bool split_spans_aligned(const void* base, int64_t span_vecs) {
+  constexpr uint64_t kGroup = static_cast<uint64_t>(kPieces) * kSplit;
+  return (reinterpret_cast<uintptr_t>(base) % (kGroup * 16u)) == 0 &&
+         (static_cast<uint64_t>(span_vecs) % kGroup) == 0;
 }
 
 }  // namespace specdec

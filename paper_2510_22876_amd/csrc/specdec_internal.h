@@ -66,8 +66,6 @@ struct PosmaskLaunch {
 int64_t verify_chunk_elems(int64_t rows, int64_t V);
 int64_t verify_chunks(int64_t rows, int64_t V);
 
-// Workgroups of the realign grid (without the fused position-id blocks).
-int64_t realign_grid_blocks(int64_t nspans, int64_t W_in, int32_t D, bool in_place);
 
 // EXSpec batch gather (pool slots -> left-padded batch, token rows, paddings,
 // position ids / mask).

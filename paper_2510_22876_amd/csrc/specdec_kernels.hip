@@ -302,6 +302,7 @@ struct RealignArgs {
   const int32_t* w_new;
   uint32_t* dev_status;
   uint32_t chunks;                       // workgroups per span (out of place)
+  uint32_t misaligned;                   // out of place: spans tiled from the group boundary below them
   uint32_t realign_blocks;               // realign workgroups in this launch
   uint32_t span_base;                    // first span of this launch
   // workgroups before the realign ones: position ids / mask, then the token row
@@ -462,14 +463,15 @@ __global__ __launch_bounds__(kTpb) void realign_oop_kernel(RealignArgs a) {
       atomicOr(a.dev_status, err);
     return;
   }
-  const int64_t base = split_base<kPieces, kTpb, kSplit>(sub);
+  u32x4* dspan = a.dst + static_cast<int64_t>(span) * a.dst_span_vecs;
+  const int64_t mis = a.misaligned ? split_misalign<kPieces, kSplit>(dspan) : 0;
+  const int64_t base = split_base<kPieces, kTpb, kSplit>(sub) - mis;
   const int64_t vpc = a.vpc;
   const int64_t total = static_cast<int64_t>(g.w) * vpc;        // output vectors of the span
   if (base >= total) return;
   const int64_t zero_end = static_cast<int64_t>(g.pad_out) * vpc;
   const int64_t shift = static_cast<int64_t>(g.pad_out - g.pad_in) * vpc;
-  split_pieces<kPieces, kTpb, kSplit, kNt>(a.src + static_cast<int64_t>(span) * a.src_span_vecs,
-                                           a.dst + static_cast<int64_t>(span) * a.dst_span_vecs, base, total,
+  split_pieces<kPieces, kTpb, kSplit, kNt>(a.src + static_cast<int64_t>(span) * a.src_span_vecs, dspan, base, total,
                                            zero_end, shift);
 }
 
@@ -693,7 +695,9 @@ hipError_t launch_realign(const RealignLaunch& p, hipStream_t stream) {
   fill_token_args(a, p, tpb);
   const int64_t tok_blocks = static_cast<int64_t>(a.tok_col_blocks) * p.B;
   const int64_t extra = pm_blocks + tok_blocks;
-  const int64_t chunks = p.in_place ? 1 : realign_grid_blocks(1, p.W_in, p.D, false);
+  a.misaligned = !p.in_place && !split_spans_aligned<kOopVec, kOopSplit>(p.dst, a.dst_span_vecs);
+  const int64_t chunks = p.in_place ? 1 : split_blocks<kOopVec, kOopTpb, kOopSplit>(
+                                                static_cast<int64_t>(p.W_in) * a.vpc, a.misaligned != 0);
   a.chunks = static_cast<uint32_t>(chunks);
   // one dispatch holds fewer than 2^32 work-items: split the spans over
   // several launches when the cache is larger than that
@@ -738,10 +742,6 @@ hipError_t launch_tokens(const RealignLaunch& p, hipStream_t stream) {
   return hipGetLastError();
 }
 
-int64_t realign_grid_blocks(int64_t nspans, int64_t W_in, int32_t D, bool in_place) {
-  if (in_place) return nspans;
-  return nspans * split_blocks<kOopVec, kOopTpb, kOopSplit>(W_in * (D / 8));
-}
 
 hipError_t launch_posmask(const PosmaskLaunch& p, hipStream_t stream) {
   const int64_t col_blocks = (p.col_bound + kPmColsPerBlock - 1) / kPmColsPerBlock;

@@ -310,3 +310,70 @@ def test_eqspec_loop_on_gpu(sd):
     model, prompts = _loop_setup(77, 7, 0)
     res = el.run_eqspec(HipBackend(), model, prompts, B=4, k=4, max_new=12)
     el.check_equivalence(model, prompts, res, 12)
+
+
+def _view_at(nbytes_offset, shape, fill=SENT_KV):
+    """A contiguous bf16 tensor of ``shape`` whose data starts ``nbytes_offset``
+    bytes past a 16 KB boundary (a view into a larger buffer)."""
+    n = int(np.prod(shape))
+    buf = torch.full((n + 3 * 8192,), fill, dtype=torch.int16, device="cuda")
+    base = buf.data_ptr()
+    skip = ((-base) % 16384 + nbytes_offset) // 2
+    return buf[skip: skip + n].view(shape).view(torch.bfloat16)
+
+
+OFFSETS = [0, 256, 1024, 4096 + 256, 16384 - 256]
+
+
+@pytest.mark.parametrize("offset", OFFSETS)
+@pytest.mark.parametrize("cap_kind", ["aligned", "ragged"])
+def test_alignment_of_destination(sd, offset, cap_kind):
+    """Gather, whole-row write-back and out-of-place realignment with the
+    destination at various offsets from a 16 KB boundary and capacities that
+    are (or are not) a multiple of 16 KB per span: the spans are tiled from the
+    group boundary below them when they are not aligned; results equal the
+    oracle's, and nothing outside the written columns changes."""
+    say(f"alignment offset={offset} cap={cap_kind}")
+    rng = np.random.default_rng(offset + (0 if cap_kind == "aligned" else 1))
+    L, H, D, N, B, k = 1, 2, 128, 6, 4, 3             # 16 vectors per column: 64 columns = 16 KB
+    lens = rng.integers(40, 140, size=N).astype(np.int32)
+    pcap = 192 if cap_kind == "aligned" else 171
+    pool, tok = _host_pool(rng, N, L, H, D, pcap, lens, pcap + 2)
+    slots = rng.permutation(N)[:B].astype(np.int32)
+    Lb = int(lens[slots].max())
+    bcap = 192 if cap_kind == "aligned" else Lb + k + 1
+    batch = _view_at(offset, (L, 2, B, H, bcap, D))
+    pads = torch.zeros(B, dtype=torch.int32, device="cuda")
+    btok = torch.full((B, bcap + 1), SENT_TOK, dtype=torch.int32, device="cuda")
+    sd.specdec_gather_batch(_dev16(pool), _dev(tok), _dev(lens), _dev(slots), Lb, batch, pads, batch_tok=btok,
+                            pad_id=PAD)
+    torch.cuda.synchronize()
+    eb, et, ep = oracle.gather_batch(pool, tok, lens, slots, Lb, bcap, bcap + 1, PAD,
+                                     out=(np.full((L, 2, B, H, bcap, D), SENT_KV, np.uint16),
+                                          np.full((B, bcap + 1), SENT_TOK, np.int32)))
+    assert np.array_equal(bits(batch), eb), "gather differs from the oracle"
+    # write-back (whole rows) into a pool placed at the same offset
+    dpool = _view_at(offset, pool.shape)
+    dpool.view(torch.int16).copy_(torch.from_numpy(pool.view(np.int16)).cuda())
+    hb = bits(batch)
+    hb[..., Lb:, :] = rng.integers(0, 0x10000, size=hb[..., Lb:, :].shape, dtype=np.uint16)
+    batch.view(torch.int16).copy_(torch.from_numpy(hb.view(np.int16)).cuda())
+    tokens = rng.integers(0, 999, size=(B, k + 1)).astype(np.int32)
+    n_acc = rng.integers(0, k + 1, size=B).astype(np.int32)
+    d_tok, d_lens = _dev(tok), _dev(lens)
+    sd.specdec_scatter_accepted(batch, pads, _dev(tokens), _dev(n_acc), _dev(slots), Lb, dpool, d_tok, d_lens,
+                                mode=sd.WRITEBACK_FULL)
+    torch.cuda.synchronize()
+    exp_pool, exp_tok, exp_lens = pool.copy(), tok.copy(), lens.copy()
+    oracle.scatter_accepted(hb, ep, tokens, n_acc, slots, Lb, exp_pool, exp_tok, exp_lens)
+    assert np.array_equal(bits(dpool), exp_pool), "write-back differs from the oracle"
+    assert np.array_equal(d_lens.cpu().numpy(), exp_lens)
+    # out-of-place realignment of the batch into a destination at the offset
+    W_in = Lb + k + 1
+    dst = _view_at(offset, (L, 2, B, H, bcap, D))
+    w_new = int((Lb - ep + n_acc + 1).max())
+    sd.specdec_realign_kv(batch, dst, k, W_in, pads, _dev(n_acc),
+                          torch.tensor([w_new], dtype=torch.int32, device="cuda"))
+    torch.cuda.synchronize()
+    exp = oracle.realign_kv(hb, k, W_in, ep, n_acc, w_new, dst=np.full(hb.shape, SENT_KV, np.uint16))
+    assert np.array_equal(bits(dst), exp), "realignment differs from the oracle"
