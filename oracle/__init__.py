@@ -65,6 +65,9 @@ class Oracle:
         lib.oracle_scatter_accepted.argtypes = [P, i64, i32, P, P, i32, P, P, i32, i32, i32, i32, P, i64, i32, P,
                                                 i64, P, P, i64]
         lib.oracle_scatter_accepted.restype = ctypes.c_int
+        lib.oracle_verify_sample.argtypes = [P, P, ctypes.c_int, P, P, P, P, ctypes.c_double, i32, i32, i64, i32,
+                                             P, P, P, P, P]
+        lib.oracle_verify_sample.restype = ctypes.c_int
         self.lib = lib
 
 
@@ -138,6 +141,37 @@ def verify(logits, dtype: str, draft, pad_in, W_in: int, oracle: Oracle | None =
                                _ptr(tokens), _ptr(n_acc), _ptr(bonus), _ptr(pad_out), _ptr(w_new))
     if rc:
         raise OracleError(f"oracle_verify rejected its arguments (code {rc})")
+    return dict(tokens=tokens, n_acc=n_acc, bonus=bonus, pad_out=pad_out, w_new=int(w_new[0]))
+
+
+def verify_sample(logits, draft_logits, dtype: str, draft, pad_in, u_accept, u_sample, temperature: float,
+                  W_in: int, oracle: Oracle | None = None):
+    """Stochastic (T > 0) verification by speculative sampling: accept draft
+    x_r iff u_accept[i][r] * q_r(x_r) < p_r(x_r); at the first rejection the
+    correction is drawn from max(0, p_r - q_r) by inversion with u_sample[i];
+    after k acceptances the bonus is drawn from p_k.  p = softmax(logits / T),
+    q = softmax(draft_logits / T), in double.  Returns the same dict as
+    ``verify`` (tokens[i][0..n_acc] are the accepted drafts and the sampled
+    token, -1 beyond)."""
+    lg = _raw_logits(logits, dtype)
+    dl = _raw_logits(draft_logits, dtype)
+    B, kp1, V = lg.shape
+    k = kp1 - 1
+    assert dl.shape == (B, k, V)
+    dr = _c(np.asarray(draft).reshape(B, k), np.int32)
+    pad = _c(np.asarray(pad_in).reshape(B), np.int32)
+    ua = _c(np.asarray(u_accept).reshape(B, k), np.float32)
+    us = _c(np.asarray(u_sample).reshape(B), np.float32)
+    tokens = np.zeros((B, kp1), np.int32)
+    n_acc = np.zeros(B, np.int32)
+    bonus = np.zeros(B, np.int32)
+    pad_out = np.zeros(B, np.int32)
+    w_new = np.zeros(1, np.int32)
+    rc = _load(oracle).oracle_verify_sample(_ptr(lg), _ptr(dl), DTYPE_CODE[dtype], _ptr(dr), _ptr(pad), _ptr(ua),
+                                            _ptr(us), float(temperature), B, k, V, W_in, _ptr(tokens), _ptr(n_acc),
+                                            _ptr(bonus), _ptr(pad_out), _ptr(w_new))
+    if rc:
+        raise OracleError(f"oracle_verify_sample rejected its arguments (code {rc})")
     return dict(tokens=tokens, n_acc=n_acc, bonus=bonus, pad_out=pad_out, w_new=int(w_new[0]))
 
 

@@ -397,3 +397,117 @@ int oracle_posmask(const int32_t* pad_out, int32_t w_new, int32_t B, int32_t k,
   }
   return OR_OK;
 }
+
+/* ---- stochastic verification (temperature T > 0) --------------------------- */
+
+/*
+ * At T > 0, output equivalence means the emitted tokens follow the target
+ * model's distribution (Section 2, the equivalence requirement), which the
+ * speculative-sampling rule the paper builds on guarantees (Chen et al.,
+ * 2023, "Accelerating large language model decoding with speculative
+ * sampling"; Leviathan et al., 2023).  With target distributions
+ * p_r = softmax(logits[i][r] / T) and draft distributions
+ * q_r = softmax(draft_logits[i][r] / T):
+ *   - draft x_r = draft[i][r] is accepted iff u_accept[i][r] * q_r(x_r) <
+ *     p_r(x_r), i.e. with probability min(1, p_r(x_r) / q_r(x_r));
+ *   - at the first rejected slot r, the correction token is sampled from the
+ *     residual distribution proportional to max(0, p_r - q_r);
+ *   - when all k drafts are accepted, the bonus token is sampled from p_k.
+ * Sampling uses one uniform per row, u_sample[i], by inversion: the smallest
+ * index j whose cumulative weight exceeds u_sample[i] times the total.
+ * Readings: one temperature for target and draft; a residual with zero mass
+ * (only possible when p_r(x_r) = q_r(x_r) = 0) falls back to p_r; a draft id
+ * outside [0, V) has probability 0 under both and is rejected; the accepted
+ * drafts and then the sampled token form tokens[i][0 .. n_acc] (later entries
+ * are -1); the width and paddings follow Eq. (1) and Eq. (2) as in greedy
+ * verification.  Everything is computed in double.  Logits must be finite or
+ * -inf, with a finite maximum per row.
+ */
+
+/* p = softmax(row / T), in double, with the row's maximum subtracted */
+static void softmax_row(const void* row, int dtype, int64_t V, double T, double* p) {
+  double m = -INFINITY;
+  for (int64_t v = 0; v < V; ++v) {
+    double x = logit_at(row, dtype, v);
+    if (x > m) m = x;
+  }
+  double z = 0.0;
+  for (int64_t v = 0; v < V; ++v) {
+    p[v] = exp((logit_at(row, dtype, v) - m) / T);
+    z += p[v];
+  }
+  for (int64_t v = 0; v < V; ++v) p[v] /= z;
+}
+
+/* inversion: the smallest j with w_0 + .. + w_j > u * (w_0 + .. + w_{V-1});
+ * the last index of positive weight when rounding leaves none; -1 if all are 0 */
+static int64_t sample_by_inversion(const double* w, int64_t V, double u) {
+  double total = 0.0;
+  for (int64_t v = 0; v < V; ++v) total += w[v];
+  const double target = u * total;
+  double c = 0.0;
+  int64_t last = -1;
+  for (int64_t v = 0; v < V; ++v) {
+    if (w[v] > 0.0) last = v;
+    c += w[v];
+    if (c > target) return v;
+  }
+  return last;
+}
+
+int oracle_verify_sample(const void* logits, const void* draft_logits, int dtype, const int32_t* draft,
+                         const int32_t* pad_in, const float* u_accept, const float* u_sample,
+                         double temperature, int32_t B, int32_t k, int64_t V, int32_t W_in,
+                         int32_t* tokens, int32_t* n_acc, int32_t* bonus, int32_t* pad_out,
+                         int32_t* w_new) {
+  int eb = oracle_logit_bytes(dtype);
+  if (B < 0 || k < 0 || V <= 0 || eb == 0 || W_in < k + 1) return OR_EINVAL;
+  if (!(temperature > 0.0) || !isfinite(temperature)) return OR_EINVAL;
+  const int32_t L = W_in - (k + 1);
+  for (int32_t i = 0; i < B; ++i) {
+    if (pad_in[i] < 0 || pad_in[i] > L) return OR_EINVAL;
+    if (!(u_sample[i] >= 0.0f && u_sample[i] < 1.0f)) return OR_EINVAL;
+    for (int32_t r = 0; r < k; ++r)
+      if (!(u_accept[(int64_t)i * k + r] >= 0.0f && u_accept[(int64_t)i * k + r] < 1.0f)) return OR_EINVAL;
+  }
+  double* p = (double*)malloc(sizeof(double) * (size_t)V);
+  double* q = (double*)malloc(sizeof(double) * (size_t)V);
+  double* w = (double*)malloc(sizeof(double) * (size_t)V);
+  if (!p || !q || !w) {
+    free(p); free(q); free(w);
+    return OR_ENOMEM;
+  }
+  for (int32_t i = 0; i < B; ++i) {
+    int32_t j = k;
+    int64_t x_out = -1;
+    for (int32_t r = 0; r < k; ++r) {
+      softmax_row((const char*)logits + ((int64_t)i * (k + 1) + r) * V * eb, dtype, V, temperature, p);
+      softmax_row((const char*)draft_logits + ((int64_t)i * k + r) * V * eb, dtype, V, temperature, q);
+      const int32_t x = draft[(int64_t)i * k + r];
+      const double px = (x >= 0 && x < V) ? p[x] : 0.0;
+      const double qx = (x >= 0 && x < V) ? q[x] : 0.0;
+      if ((double)u_accept[(int64_t)i * k + r] * qx < px) continue;   /* accepted */
+      j = r;                                                             /* rejected: residual */
+      for (int64_t v = 0; v < V; ++v) w[v] = p[v] > q[v] ? p[v] - q[v] : 0.0;
+      x_out = sample_by_inversion(w, V, (double)u_sample[i]);
+      if (x_out < 0) x_out = sample_by_inversion(p, V, (double)u_sample[i]);
+      break;
+    }
+    if (j == k) {                                                        /* all accepted: bonus from p_k */
+      softmax_row((const char*)logits + ((int64_t)i * (k + 1) + k) * V * eb, dtype, V, temperature, p);
+      x_out = sample_by_inversion(p, V, (double)u_sample[i]);
+    }
+    n_acc[i] = j;
+    for (int32_t r = 0; r <= k; ++r)
+      tokens[(int64_t)i * (k + 1) + r] = r < j ? draft[(int64_t)i * k + r] : (r == j ? (int32_t)x_out : -1);
+    if (bonus) bonus[i] = (int32_t)x_out;
+  }
+  free(p); free(q); free(w);
+  /* Eq. (1) and Eq. (2) */
+  int32_t Lp = 0;
+  for (int32_t i = 0; i < B; ++i)
+    if ((L - pad_in[i]) + n_acc[i] + 1 > Lp) Lp = (L - pad_in[i]) + n_acc[i] + 1;
+  for (int32_t i = 0; i < B; ++i) pad_out[i] = pad_in[i] + ((Lp - L) - (n_acc[i] + 1));
+  *w_new = Lp;
+  return OR_OK;
+}

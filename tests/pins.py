@@ -676,6 +676,113 @@ def pin_scheduler_grouping_rate(o=None):
     assert sum(1 for _, r in rounds if not r) == 3          # one gather per batch of 4
 
 
+# ---- stochastic verification (T > 0): speculative sampling ---------------------------------------
+
+def _softmax64(x, T):
+    z = (np.asarray(x, np.float64) - np.max(x, axis=-1, keepdims=True)) / T
+    e = np.exp(z)
+    return e / e.sum(axis=-1, keepdims=True)
+
+
+def pin_sample_preserves_target_distribution(o=None):
+    """The guarantee that makes T > 0 decoding output-equivalent: with the draft
+    x ~ q_0, the first emitted token is distributed as p_0, and after an
+    acceptance the next token as p_1.  Measured exactly by integrating the
+    oracle's decisions over a midpoint grid of the two uniforms (error at most
+    1/Na + 2/Ns per outcome), for every draft token of a small vocabulary."""
+    rng = np.random.default_rng(31)
+    V, Na, Ns = 5, 300, 300
+    for trial, T in enumerate((0.7, 1.6)):
+        tl = rng.normal(0, 1.5, size=(2, V)).astype(np.float32)      # target rows 0 and 1
+        dl = rng.normal(0, 1.5, size=(1, V)).astype(np.float32)      # draft row 0
+        p0, p1 = _softmax64(tl[0], T), _softmax64(tl[1], T)
+        q0 = _softmax64(dl[0], T)
+        ua = (np.arange(Na) + 0.5) / Na
+        us = (np.arange(Ns) + 0.5) / Ns
+        B = V * Na * Ns
+        x0 = np.repeat(np.arange(V), Na * Ns).astype(np.int32)
+        UA = np.tile(np.repeat(ua, Ns), V).astype(np.float32)
+        US = np.tile(us, V * Na).astype(np.float32)
+        logits = np.broadcast_to(tl, (B, 2, V))
+        dlog = np.broadcast_to(dl, (B, 1, V))
+        v = oracle.verify_sample(logits, dlog, "f32", x0.reshape(B, 1), np.zeros(B, np.int32), UA.reshape(B, 1), US,
+                                 T, 2, oracle=o)
+        first = v["tokens"][:, 0]
+        got = np.zeros(V)
+        for x in range(V):
+            sel = x0 == x
+            got += q0[x] * np.bincount(first[sel], minlength=V)[:V] / sel.sum()
+        tol = 1.0 / Na + 2.0 / Ns + 1e-9
+        assert np.max(np.abs(got - p0)) <= tol, (trial, got, p0)
+        acc = v["n_acc"] == 1
+        assert np.array_equal(first[acc], x0[acc]) and np.all(first[~acc] != -1)
+        # the bonus after an acceptance follows p_1 (over the sampling uniform alone)
+        sel = acc & (x0 == int(np.argmax(np.minimum(1.0, p0 / q0))))
+        bon = np.bincount(v["bonus"][sel], minlength=V)[:V] / sel.sum()
+        assert np.max(np.abs(bon - p1)) <= 2.0 / Ns + 1e-9, (bon, p1)
+        # the acceptance rate of each draft token is min(1, p_0(x) / q_0(x))
+        for x in range(V):
+            sel = x0 == x
+            assert abs(acc[sel].mean() - min(1.0, p0[x] / q0[x])) <= 1.0 / Na + 1e-9
+
+
+def pin_sample_special_cases(o=None):
+    """q = p accepts every draft and samples the bonus from p_k by inversion;
+    T -> 0 with a clear maximum reduces to greedy verification (Algorithm 3);
+    scaling logits and T together changes nothing; a correction token always
+    has p_r > q_r; I1 and Eq. (1)-(2) hold."""
+    rng = np.random.default_rng(32)
+    B, k, V = 6, 3, 40
+    tl = rng.normal(0, 2, size=(B, k + 1, V)).astype(np.float32)
+    pad = rng.integers(0, 5, size=B).astype(np.int32)
+    W_in = 12 + k + 1
+    ua = rng.random((B, k)).astype(np.float32)
+    us = rng.random(B).astype(np.float32)
+    draft = rng.integers(0, V, size=(B, k)).astype(np.int32)
+    T = 0.9
+    v = oracle.verify_sample(tl, tl[:, :k], "f32", draft, pad, ua, us, T, W_in, oracle=o)
+    assert np.all(v["n_acc"] == k)                              # q = p: u * q(x) < q(x) for every u < 1
+    for i in range(B):
+        cdf = np.cumsum(_softmax64(tl[i, k], T))
+        assert v["bonus"][i] == int(np.searchsorted(cdf, float(us[i]) * cdf[-1], side="right"))
+        assert list(v["tokens"][i, :k]) == list(draft[i])
+    # T -> 0: one-hot distributions; the result is greedy verification's
+    for trial in range(4):
+        tl = rng.normal(0, 2, size=(B, k + 1, V)).astype(np.float32)
+        gl = tl.copy()
+        greedy_tok = gl.argmax(-1)
+        np.put_along_axis(gl, greedy_tok[..., None], gl.max(-1, keepdims=True) + 8.0, axis=-1)   # 8 above the rest
+        acc = rng.integers(0, k + 1, size=B)
+        draft = greedy_tok[:, :k].copy()
+        for i in range(B):
+            if acc[i] < k:
+                draft[i, acc[i]] = (draft[i, acc[i]] + 1 + rng.integers(V - 1)) % V
+        dl = np.zeros((B, k, V), np.float32)
+        dl[np.arange(B)[:, None], np.arange(k)[None, :], draft] = 8.0        # the draft model's own maximum
+        vs = oracle.verify_sample(gl.astype(np.float32), dl, "f32", draft.astype(np.int32), pad, ua, us, 0.05, W_in,
+                                  oracle=o)
+        vg = oracle.verify(gl.astype(np.float32), "f32", draft.astype(np.int32), pad, W_in, oracle=o)
+        assert np.array_equal(vs["n_acc"], vg["n_acc"]) and np.array_equal(vs["bonus"], vg["bonus"])
+        assert np.array_equal(vs["pad_out"], vg["pad_out"]) and vs["w_new"] == vg["w_new"]
+        for i in range(B):
+            assert list(vs["tokens"][i, : vs["n_acc"][i] + 1]) == list(vg["tokens"][i, : vg["n_acc"][i] + 1])
+    # scale invariance, correction support, geometry
+    tl = rng.normal(0, 2, size=(B, k + 1, V)).astype(np.float32)
+    dl = rng.normal(0, 2, size=(B, k, V)).astype(np.float32)
+    draft = rng.integers(0, V, size=(B, k)).astype(np.int32)
+    a = oracle.verify_sample(tl, dl, "f32", draft, pad, ua, us, 1.3, W_in, oracle=o)
+    b = oracle.verify_sample(tl * 2, dl * 2, "f32", draft, pad, ua, us, 2.6, W_in, oracle=o)
+    assert all(np.array_equal(a[x], b[x]) for x in ("tokens", "n_acc", "bonus", "pad_out")) and a["w_new"] == b["w_new"]
+    for i in range(B):
+        r = int(a["n_acc"][i])
+        if r < k:
+            t = int(a["bonus"][i])
+            assert _softmax64(tl[i, r], 1.3)[t] > _softmax64(dl[i, r], 1.3)[t], "correction outside the residual"
+        assert list(a["tokens"][i, :r]) == list(draft[i, :r]) and np.all(a["tokens"][i, r + 1:] == -1)
+    from tests import checker
+    checker.check_geometry(pad, a["n_acc"], a["pad_out"], a["w_new"], W_in, k)
+
+
 ALL_PINS = [
     pin_argmax_bruteforce, pin_argmax_torch, pin_argmax_specials, pin_widening_pairs,
     pin_verify_planted, pin_verify_alg3_vectorised, pin_width_exhaustive,
@@ -684,4 +791,5 @@ ALL_PINS = [
     pin_gather_list_model, pin_gather_same_length_is_concat, pin_regroup_equals_realign,
     pin_scatter_appends_to_batch_row, pin_exspec_output_equivalence, pin_eqspec_output_equivalence,
     pin_scheduler_properties, pin_scheduler_grouping_rate,
+    pin_sample_preserves_target_distribution, pin_sample_special_cases,
 ]

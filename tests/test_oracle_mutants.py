@@ -61,6 +61,22 @@ MUTANTS = {
     "scatter_batch_row_at_width": ("batch_tok[(int64_t)i * btok_stride + Lb + 1 + r]", "batch_tok[(int64_t)i * btok_stride + Lb + r]"),
     "positions_raw_column": ("pos[(int64_t)i * pm_cap + j] = count - 1 > 0 ? count - 1 : 0;",
                              "pos[(int64_t)i * pm_cap + j] = j;"),
+    # stochastic verification (speculative sampling)
+    "sample_ratio_inverted": ("if ((double)u_accept[(int64_t)i * k + r] * qx < px) continue;",
+                              "if ((double)u_accept[(int64_t)i * k + r] * px < qx) continue;"),
+    "sample_residual_is_target": ("w[v] = p[v] > q[v] ? p[v] - q[v] : 0.0;", "w[v] = p[v];"),
+    "sample_residual_reversed": ("w[v] = p[v] > q[v] ? p[v] - q[v] : 0.0;", "w[v] = q[v] > p[v] ? q[v] - p[v] : 0.0;"),
+    "sample_temperature_ignored": ("p[v] = exp((logit_at(row, dtype, v) - m) / T);",
+                                   "p[v] = exp(logit_at(row, dtype, v) - m);"),
+    "sample_temperature_multiplies": ("p[v] = exp((logit_at(row, dtype, v) - m) / T);",
+                                      "p[v] = exp((logit_at(row, dtype, v) - m) * T);"),
+    "sample_bonus_from_previous_row": ("softmax_row((const char*)logits + ((int64_t)i * (k + 1) + k) * V * eb",
+                                       "softmax_row((const char*)logits + ((int64_t)i * (k + 1) + k - 1) * V * eb"),
+    "sample_correction_uses_accept_uniform": ("x_out = sample_by_inversion(w, V, (double)u_sample[i]);",
+                                              "x_out = sample_by_inversion(w, V, (double)u_accept[(int64_t)i * k + r]);"),
+    "sample_draft_logits_of_target": ("softmax_row((const char*)draft_logits + ((int64_t)i * k + r) * V * eb",
+                                      "softmax_row((const char*)logits + ((int64_t)i * (k + 1) + r) * V * eb"),
+    "sample_accepted_tokens_not_drafts": ("r < j ? draft[(int64_t)i * k + r] :", "r < j ? (int32_t)x_out :"),
 }
 
 # Plausible slips in the scheduler (oracle/exspec.py), caught by the
