@@ -478,7 +478,7 @@ int oracle_verify_sample(const void* logits, const void* draft_logits, int dtype
     return OR_ENOMEM;
   }
   for (int32_t i = 0; i < B; ++i) {
-    int32_t j = k;
+    int32_t acc = k;
     int64_t x_out = -1;
     for (int32_t r = 0; r < k; ++r) {
       softmax_row((const char*)logits + ((int64_t)i * (k + 1) + r) * V * eb, dtype, V, temperature, p);
@@ -487,19 +487,19 @@ int oracle_verify_sample(const void* logits, const void* draft_logits, int dtype
       const double px = (x >= 0 && x < V) ? p[x] : 0.0;
       const double qx = (x >= 0 && x < V) ? q[x] : 0.0;
       if ((double)u_accept[(int64_t)i * k + r] * qx < px) continue;   /* accepted */
-      j = r;                                                             /* rejected: residual */
+      acc = r;                                                           /* rejected: residual */
       for (int64_t v = 0; v < V; ++v) w[v] = p[v] > q[v] ? p[v] - q[v] : 0.0;
       x_out = sample_by_inversion(w, V, (double)u_sample[i]);
       if (x_out < 0) x_out = sample_by_inversion(p, V, (double)u_sample[i]);
       break;
     }
-    if (j == k) {                                                        /* all accepted: bonus from p_k */
+    if (acc == k) {                                                      /* all accepted: bonus from p_k */
       softmax_row((const char*)logits + ((int64_t)i * (k + 1) + k) * V * eb, dtype, V, temperature, p);
       x_out = sample_by_inversion(p, V, (double)u_sample[i]);
     }
-    n_acc[i] = j;
+    n_acc[i] = acc;
     for (int32_t r = 0; r <= k; ++r)
-      tokens[(int64_t)i * (k + 1) + r] = r < j ? draft[(int64_t)i * k + r] : (r == j ? (int32_t)x_out : -1);
+      tokens[(int64_t)i * (k + 1) + r] = r < acc ? draft[(int64_t)i * k + r] : (r == acc ? (int32_t)x_out : -1);
     if (bonus) bonus[i] = (int32_t)x_out;
   }
   free(p); free(q); free(w);

@@ -76,7 +76,7 @@ MUTANTS = {
                                               "x_out = sample_by_inversion(w, V, (double)u_accept[(int64_t)i * k + r]);"),
     "sample_draft_logits_of_target": ("softmax_row((const char*)draft_logits + ((int64_t)i * k + r) * V * eb",
                                       "softmax_row((const char*)logits + ((int64_t)i * (k + 1) + r) * V * eb"),
-    "sample_accepted_tokens_not_drafts": ("r < j ? draft[(int64_t)i * k + r] :", "r < j ? (int32_t)x_out :"),
+    "sample_accepted_tokens_not_drafts": ("r < acc ? draft[(int64_t)i * k + r] :", "r < acc ? (int32_t)x_out :"),
 }
 
 # Plausible slips in the scheduler (oracle/exspec.py), caught by the
