@@ -15,6 +15,7 @@ the CPU oracle timed on a bounded sample of the same step.
 
   python bench.py [--steps K] [--warmup W] [--workload NAME] [--variant oop|inplace]
   python bench.py --path exspec [--exspec-batch ragged|same]
+  python bench.py --verify sample [--temperature T]
   python bench.py --copy-calibration GIB   # plain device copy, for counter scaling
 
 ``--path exspec`` measures EXSpec's step instead (Algorithm 2 without the
@@ -41,6 +42,7 @@ sys.path.insert(0, str(ROOT))
 PEAK_HBM_GBS = 8000.0
 METRIC = "verify+realign steps/s and achieved HBM GB/s (% peak), B=8 7B-shaped KV"
 METRIC_EXSPEC = "EXSpec gather+verify+write-back steps/s and achieved HBM GB/s (% peak), B=8 7B-shaped KV"
+METRIC_SAMPLE = "stochastic verify+realign steps/s and achieved HBM GB/s (% peak), B=8 7B-shaped KV"
 CSRC = ROOT / "paper_2510_22876_amd" / "csrc"
 KERNEL_SRCS = [CSRC / f for f in ("specdec_kernels.hip", "span_copy.h", "posmask.h")]
 GATHER_SRCS = [CSRC / f for f in ("exspec_kernels.hip", "span_copy.h", "posmask.h")]
@@ -257,7 +259,7 @@ def bench_exspec(args, w):
     elapsed = timed_pass(K, 1 << sd.KERNEL_GATHER)
     gather_ms, gather_n = sd.timing_query(sd.KERNEL_GATHER)
     timed_pass(K, (1 << sd.KERNEL_VERIFY) | (1 << sd.KERNEL_WRITEBACK))
-    verify_ms, verify_n = sd.timing_query(sd.KERNEL_VERIFY)
+    verify_ms, verify_n = sd.timing_query(vkern)
     wb_ms, wb_n = sd.timing_query(sd.KERNEL_WRITEBACK)
     assert gather_n == K and verify_n == K and wb_n == K
     by = exspec_bytes(w, lens[:B], Lb, n_acc)
@@ -338,6 +340,9 @@ def main():
     ap.add_argument("--kernel-timers", choices=["on", "off"], default="on",
                     help="record the library's HIP events around the realign kernel inside the timed region "
                          "(off: a second pass measures it)")
+    ap.add_argument("--verify", choices=["greedy", "sample"], default="greedy",
+                    help="greedy verification (default) or stochastic verification by speculative sampling")
+    ap.add_argument("--temperature", type=float, default=1.0, help="--verify sample: the sampling temperature")
     ap.add_argument("--path", choices=["eqspec", "exspec"], default="eqspec",
                     help="eqspec: the verify + realign step (default); exspec: gather + verify + write-back")
     ap.add_argument("--exspec-batch", choices=["ragged", "same"], default="ragged",
@@ -370,7 +375,12 @@ def main():
     variant = args.variant
     n, W_in, pad_in, cap = wl.initial_geometry(w, args.seed)
     log(f"[bench] workload {describe(w, variant)}; W_in={W_in} cap={cap}")
-    logits, draft, *_ = wl.logits_and_drafts(w, args.seed, 0, device="cuda")
+    sample = args.verify == "sample"
+    if sample:
+        logits, draft_logits, draft, u_accept, u_sample = wl.sampled_inputs(w, args.seed, 0, device="cuda",
+                                                                            temperature=args.temperature)
+    else:
+        logits, draft, *_ = wl.logits_and_drafts(w, args.seed, 0, device="cuda")
     src = wl.make_kv(w, pad_in, W_in, cap, args.seed, device="cuda")
     pristine = None
     if variant == "oop":
@@ -388,10 +398,17 @@ def main():
         s_out = torch.empty_like(s_in) if variant == "oop" else s_in
     pristine_s = s_in.clone() if (token_row and variant != "oop") else None
 
+    sws = sd.alloc_sample_workspace(w.B, w.k, w.V) if sample else None
+
     def step():
-        sd.specdec_step(logits, draft, pad_t, W_in, src, dst, bufs.tokens, bufs.n_acc, bufs.bonus, bufs.pad_out,
-                        bufs.w_new, bufs.pos, bufs.mask, bufs.workspace, bufs.dev_status, s_in=s_in, s_out=s_out,
-                        pad_id=-1)
+        if sample:
+            sd.specdec_step_sample(logits, draft_logits, draft, pad_t, u_accept, u_sample, args.temperature, W_in,
+                                   src, dst, bufs.tokens, bufs.n_acc, bufs.bonus, bufs.pad_out, bufs.w_new, bufs.pos,
+                                   bufs.mask, sws, bufs.dev_status, s_in=s_in, s_out=s_out, pad_id=-1)
+        else:
+            sd.specdec_step(logits, draft, pad_t, W_in, src, dst, bufs.tokens, bufs.n_acc, bufs.bonus, bufs.pad_out,
+                            bufs.w_new, bufs.pos, bufs.mask, bufs.workspace, bufs.dev_status, s_in=s_in, s_out=s_out,
+                            pad_id=-1)
 
     def restore():
         src.copy_(pristine)
@@ -437,19 +454,23 @@ def main():
     # a second pass of K steps after the timed region: the verify kernels'
     # durations (and the realign kernel's when it was not timed above)
     sd.timing_reset()
-    sd.timing_enable((1 << sd.KERNEL_VERIFY) | (0 if timers else 1 << sd.KERNEL_REALIGN))
+    vkern = sd.KERNEL_SAMPLE if sample else sd.KERNEL_VERIFY
+    sd.timing_enable((1 << vkern) | (0 if timers else 1 << sd.KERNEL_REALIGN))
     for _ in range(K):
         if pristine is not None:
             restore()
         step()
     torch.cuda.synchronize()
     sd.timing_enable(False)
-    verify_ms, verify_n = sd.timing_query(sd.KERNEL_VERIFY)
+    verify_ms, verify_n = sd.timing_query(vkern)
     if not timers:
         realign_ms, realign_n = sd.timing_query(sd.KERNEL_REALIGN)
     assert realign_n == K and verify_n == K
 
     by = step_bytes(w, pad_in, W_in, n_acc, w_new, variant, token_row)
+    if sample:
+        # every target and draft logit is read once; inputs and outputs are a few KB
+        by["verify"] = w.B * (2 * w.k + 1) * w.V * w.logit_bytes + 4 * w.B * (2 * w.k + 1) + 4 * w.B * (w.k + 5) + 4
     realign_avg_ms = realign_ms / realign_n
     verify_avg_ms = verify_ms / verify_n
     realign_bytes = by["realign"] + by["posmask"]
@@ -462,7 +483,9 @@ def main():
         f"({by['verify'] / 1e6:.2f} MB), step {ms_per_step:.4f} ms ({step_gbs:.0f} GB/s); traffic: {traffic_src}")
 
     cpu = None
-    if args.cpu_baseline_seconds > 0:
+    if args.cpu_baseline_seconds > 0 and sample:
+        log("[bench] cpu baseline skipped for --verify sample")
+    elif args.cpu_baseline_seconds > 0:
         s_host = None
         if token_row:
             s_host = (pristine_s if pristine_s is not None else s_in).cpu().numpy()
@@ -471,7 +494,7 @@ def main():
         log(f"[bench] cpu baseline: {cpu['value']:.4f} steps/s ({cpu['sample']})")
 
     line = {
-        "metric": METRIC,
+        "metric": METRIC_SAMPLE if sample else METRIC,
         "value": K / elapsed,
         "unit": "steps/s",
         "n_gpus": 1,
@@ -484,9 +507,11 @@ def main():
         "dtype": "bf16",
         "data": "synthetic",
         "config": {
-            "workload": describe(w, variant),
+            "workload": describe(w, variant) + (f"; stochastic verification at T={args.temperature}, draft logits = "
+                                                 f"target + N(0,1), drafts drawn from q" if sample else ""),
             "B": w.B, "k": w.k, "V": w.V, "L": w.L, "H": w.H, "D": w.D, "W_in": W_in, "w_new": w_new,
-            "variant": variant, "seed": args.seed, "token_row": token_row,
+            "variant": variant, "seed": args.seed, "token_row": token_row, "verify": args.verify,
+            **({"temperature": args.temperature, "draft_noise": 1.0} if sample else {}),
             "step_GBps": round(step_gbs, 1),
             "step_bytes": realign_bytes + by["verify"],
             "verify_ms": round(verify_avg_ms, 5),

@@ -46,7 +46,7 @@
 extern "C" {
 #endif
 
-#define SPECDEC_ABI_VERSION 3
+#define SPECDEC_ABI_VERSION 4
 
 typedef enum {
   SPECDEC_OK = 0,
@@ -66,6 +66,7 @@ typedef enum { SPECDEC_F32 = 0, SPECDEC_BF16 = 1, SPECDEC_F16 = 2 } specdec_dtyp
 #define SPECDEC_DEV_BAD_SLOT 0x10u   /* pool slot outside [0, N), or its length does not
                                         fit the batch width, the pool or its token row */
 #define SPECDEC_DEV_SLOT_LEN 0x20u   /* write-back: lens[slot] != Lb - pads[i] on entry */
+#define SPECDEC_DEV_BAD_UNIFORM 0x40u /* a uniform outside [0, 1) (clamped into it)       */
 
 /* Limits checked by the host. */
 #define SPECDEC_MAX_B 65536
@@ -129,6 +130,51 @@ specdec_status_t specdec_workspace_init(void* workspace, size_t workspace_bytes,
  */
 specdec_status_t specdec_verify_greedy(const void* logits, int32_t dtype, const int32_t* draft,
                                        const int32_t* pad_in, int32_t B, int32_t k, int32_t V,
+                                       int32_t W_in, int32_t* tokens, int32_t* n_acc,
+                                       int32_t* bonus, int32_t* pad_out, int32_t* w_new,
+                                       void* workspace, size_t workspace_bytes,
+                                       uint32_t* dev_status, void* stream);
+
+/*
+ * Stochastic verification at temperature T > 0: the counterpart of
+ * specdec_verify_greedy for sampled decoding.  At T > 0, output equivalence
+ * means the emitted tokens follow the target model's distribution (the
+ * equivalence requirement of Section 2), which speculative sampling keeps
+ * (Chen et al. 2023; Leviathan et al. 2023).  With p_r = softmax(logits[i][r]
+ * / T) and q_r = softmax(draft_logits[i][r] / T):
+ *   draft r is accepted iff u_accept[i][r] * q_r(draft[i][r]) <
+ *   p_r(draft[i][r]); n_acc[i] is the first rejected slot (k if none);
+ *   at a rejection the correction token is drawn from max(0, p_r - q_r)
+ *   (normalised; p_r if that has no mass), after k acceptances the bonus
+ *   from p_k, by inversion with u_sample[i]: the smallest index whose
+ *   cumulative weight exceeds u_sample[i] times the total.
+ * tokens[i][0 .. n_acc[i]] are the accepted drafts and the drawn token (later
+ * entries -1), bonus[i] the drawn token; pad_out and w_new as in greedy
+ * verification (Eq. (1), Eq. (2)), so the realignment entry points apply
+ * unchanged.
+ *
+ *   logits        [B][k+1][V], draft_logits [B][k][V], both of `dtype`
+ *                 (SPECDEC_F32 / _BF16 / _F16), contiguous, aligned to the
+ *                 element size.  Every row needs a finite maximum; -inf
+ *                 entries have probability 0; NaN or +inf give unspecified
+ *                 tokens (never an out-of-bounds access).
+ *   u_accept      float [B][k], u_sample float [B]: uniforms in [0, 1) drawn by
+ *                 the caller (values outside are clamped into [0, 1) and
+ *                 flagged SPECDEC_DEV_BAD_UNIFORM).
+ *   temperature   T > 0, finite, with log2(e) / T finite in fp32.
+ *   workspace     specdec_sample_workspace_bytes(B, k, V) bytes, 8-byte
+ *                 aligned; no initialisation needed.
+ * Arithmetic is fp32 (exp2 of scaled differences from the row maximum, sums
+ * in a fixed parallel order): a decision whose fp64 margin is within the
+ * fp32 rounding of these sums may differ from an fp64 evaluation.
+ * Limits as specdec_verify_greedy, with B*(2k+1) <= SPECDEC_MAX_ROWS.
+ */
+size_t specdec_sample_workspace_bytes(int32_t B, int32_t k, int32_t V);
+
+specdec_status_t specdec_verify_sample(const void* logits, const void* draft_logits, int32_t dtype,
+                                       const int32_t* draft, const int32_t* pad_in,
+                                       const float* u_accept, const float* u_sample,
+                                       float temperature, int32_t B, int32_t k, int32_t V,
                                        int32_t W_in, int32_t* tokens, int32_t* n_acc,
                                        int32_t* bonus, int32_t* pad_out, int32_t* w_new,
                                        void* workspace, size_t workspace_bytes,
@@ -360,6 +406,24 @@ specdec_status_t specdec_sched_lengths(const specdec_sched_t* s, int32_t* lens);
 int32_t specdec_sched_active(const specdec_sched_t* s);
 
 /*
+ * The whole step with stochastic verification: specdec_verify_sample, then
+ * the same fused realignment launch as specdec_step (cache, position ids /
+ * mask, token row when s_in is not NULL).  Arguments as specdec_verify_sample
+ * and specdec_step; the workspace is specdec_sample_workspace_bytes(B, k, V).
+ */
+specdec_status_t specdec_step_sample(const void* logits, const void* draft_logits, int32_t dtype,
+                                     const int32_t* draft, const int32_t* pad_in,
+                                     const float* u_accept, const float* u_sample,
+                                     float temperature, int32_t B, int32_t k, int32_t V,
+                                     int32_t W_in, const specdec_kv_t* src, const specdec_kv_t* dst,
+                                     int32_t* tokens, int32_t* n_acc, int32_t* bonus,
+                                     int32_t* pad_out, int32_t* w_new, int64_t* pos, uint8_t* mask,
+                                     int64_t pm_cap, const int32_t* s_in, int64_t s_in_stride,
+                                     int32_t* s_out, int64_t s_out_stride, int32_t pad_id,
+                                     void* workspace, size_t workspace_bytes, uint32_t* dev_status,
+                                     int32_t* w_new_host, void* stream);
+
+/*
  * Kernel timers (for measurement; off by default).  specdec_timing_enable
  * takes a mask of kernels (bit 1 << SPECDEC_KERNEL_*; 0 turns the timers
  * off).  For each selected kernel the library records a pair of HIP events on
@@ -367,14 +431,16 @@ int32_t specdec_sched_active(const specdec_sched_t* s);
  * specdec_timing_query waits for the recorded events, adds their durations to
  * the totals of `kernel` (0 = verify, 1 = realign, with the fused position ids
  * / mask in specdec_step, 2 = position ids / mask alone, 3 = batch gather,
- * 4 = write-back) and returns the totals since the last reset.
+ * 4 = write-back, 5 = stochastic verification) and returns the totals since
+ * the last reset.
  */
 #define SPECDEC_KERNEL_VERIFY 0
 #define SPECDEC_KERNEL_REALIGN 1
 #define SPECDEC_KERNEL_POSMASK 2
 #define SPECDEC_KERNEL_GATHER 3
 #define SPECDEC_KERNEL_WRITEBACK 4
-#define SPECDEC_TIMING_ALL 31
+#define SPECDEC_KERNEL_SAMPLE 5
+#define SPECDEC_TIMING_ALL 63
 specdec_status_t specdec_timing_enable(int32_t kernel_mask);
 specdec_status_t specdec_timing_reset(void);
 specdec_status_t specdec_timing_query(int32_t kernel, double* total_ms, int64_t* launches);

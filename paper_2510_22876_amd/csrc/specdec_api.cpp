@@ -4,6 +4,7 @@
 // exercised without a device.
 #include <hip/hip_runtime.h>
 
+#include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <mutex>
@@ -58,7 +59,7 @@ int logit_bytes(int32_t dtype) {
 
 // ---- kernel timers -------------------------------------------------------------
 
-constexpr int kTimedKernels = 5;
+constexpr int kTimedKernels = 6;
 
 struct TimedLaunch {
   int kernel;
@@ -235,6 +236,112 @@ specdec_status_t check_posmask_args(const int32_t* pad_out, const int32_t* w_new
 }
 
 
+specdec_status_t check_sample_args(const void* logits, const void* draft_logits, int32_t dtype, const int32_t* draft,
+                                   const int32_t* pad_in, const float* u_accept, const float* u_sample,
+                                   float temperature, int32_t B, int32_t k, int32_t V, int32_t W_in,
+                                   const int32_t* tokens, const int32_t* n_acc, const int32_t* bonus,
+                                   const int32_t* pad_out, const int32_t* w_new, const void* workspace,
+                                   size_t workspace_bytes, const uint32_t* dev_status, float* c_out) {
+  if (B < 0 || B > SPECDEC_MAX_B) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "B=%d outside [0,%d]", B, SPECDEC_MAX_B);
+  if (k < 0 || k > SPECDEC_MAX_K) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "k=%d outside [0,%d]", k, SPECDEC_MAX_K);
+  if (V < 1) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "V=%d must be >= 1", V);
+  if (W_in < k + 1 || W_in > SPECDEC_MAX_WIDTH)
+    return fail(SPECDEC_ERR_INVALID_ARGUMENT, "W_in=%d outside [k+1=%d, %d]", W_in, k + 1, SPECDEC_MAX_WIDTH);
+  const int eb = logit_bytes(dtype);
+  if (eb == 0) return fail(SPECDEC_ERR_UNSUPPORTED, "logit dtype %d not supported", dtype);
+  const double c = 1.4426950408889634 / static_cast<double>(temperature);
+  if (!(temperature > 0.0f) || !std::isfinite(temperature) || !std::isfinite(static_cast<float>(c)))
+    return fail(SPECDEC_ERR_INVALID_ARGUMENT, "temperature %g must be finite and > 0 (with log2(e)/T finite)",
+                static_cast<double>(temperature));
+  *c_out = static_cast<float>(c);
+  const int64_t rows = static_cast<int64_t>(B) * (2 * k + 1);
+  if (rows > SPECDEC_MAX_ROWS)
+    return fail(SPECDEC_ERR_INVALID_ARGUMENT, "B*(2k+1)=%lld exceeds %d", (long long)rows, SPECDEC_MAX_ROWS);
+  if (B == 0) return SPECDEC_OK;
+  if (!logits || !pad_in || !u_sample || !tokens || !n_acc || !pad_out || !w_new ||
+      (k > 0 && (!draft || !draft_logits || !u_accept)))
+    return fail(SPECDEC_ERR_INVALID_ARGUMENT, "NULL tensor pointer");
+  if (!aligned(logits, eb) || (draft_logits && !aligned(draft_logits, eb)))
+    return fail(SPECDEC_ERR_UNSUPPORTED, "logits not aligned to %d bytes", eb);
+  const void* w4[] = {draft, pad_in, u_accept, u_sample, tokens, n_acc, bonus, pad_out, w_new, dev_status};
+  for (const void* q : w4)
+    if (q && !aligned(q, 4)) return fail(SPECDEC_ERR_UNSUPPORTED, "4-byte tensor not 4-byte aligned");
+  const int64_t blocks = rows * specdec::sample_chunks(rows, V);
+  if (blocks * 256 > 0xFFFFFFFFLL) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "logits too large for one launch");
+  const size_t need = specdec_sample_workspace_bytes(B, k, V);
+  if (!workspace) return fail(SPECDEC_ERR_WORKSPACE, "workspace is NULL (need %zu bytes)", need);
+  if (!aligned(workspace, 8)) return fail(SPECDEC_ERR_WORKSPACE, "workspace not 8-byte aligned");
+  if (workspace_bytes < need)
+    return fail(SPECDEC_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", workspace_bytes, need);
+  return SPECDEC_OK;
+}
+
+// Checks shared by the fused steps after their verification arguments.
+specdec_status_t check_step_rest(int32_t B, int32_t k, int32_t W_in, const specdec_kv_t* src, const specdec_kv_t* dst,
+                                 const int32_t* pad_in, const int32_t* n_acc, const int32_t* pad_out,
+                                 const int32_t* w_new, const int64_t* pos, const uint8_t* mask, int64_t pm_cap,
+                                 const int32_t* s_in, int64_t s_in_stride, const int32_t* s_out,
+                                 int64_t s_out_stride, const uint32_t* dev_status, bool* in_place) {
+  specdec_status_t s = check_realign_args(src, dst, k, W_in, pad_in, n_acc, w_new, in_place);
+  if (s) return s;
+  if (src->B != B) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "cache rows B=%d differ from logits rows B=%d", src->B, B);
+  s = check_posmask_args(pad_out, w_new, B, k, pos, mask, pm_cap);
+  if (s) return s;
+  if (B > 0 && pm_cap < static_cast<int64_t>(W_in) + k + 1)
+    return fail(SPECDEC_ERR_INVALID_ARGUMENT, "pm_cap=%lld < W_in+k+1=%d", (long long)pm_cap, W_in + k + 1);
+  if (s_in || s_out) {
+    s = check_token_args(s_in, s_in_stride, s_out, s_out_stride, B, k, W_in);
+    if (s) return s;
+  }
+  if (dev_status && !aligned(dev_status, 4)) return fail(SPECDEC_ERR_UNSUPPORTED, "dev_status not 4-byte aligned");
+  return SPECDEC_OK;
+}
+
+// The realignment launch of a fused step (cache, position ids / mask, token
+// row), then the optional host copy of the new width.
+specdec_status_t step_realign(int32_t k, int32_t W_in, const specdec_kv_t* src, const specdec_kv_t* dst,
+                              bool in_place, const int32_t* pad_in, const int32_t* tokens, const int32_t* n_acc,
+                              const int32_t* pad_out, const int32_t* w_new, int64_t* pos, uint8_t* mask,
+                              int64_t pm_cap, const int32_t* s_in, int64_t s_in_stride, int32_t* s_out,
+                              int64_t s_out_stride, int32_t pad_id, uint32_t* dev_status, int32_t* w_new_host,
+                              hipStream_t st) {
+  specdec::RealignLaunch rp{};
+  rp.src = src->data;
+  rp.dst = dst->data;
+  rp.src_cap = src->cap;
+  rp.dst_cap = dst->cap;
+  rp.L = src->L;
+  rp.B = src->B;
+  rp.H = src->H;
+  rp.D = src->D;
+  rp.k = k;
+  rp.W_in = W_in;
+  rp.pad_in = pad_in;
+  rp.n_acc = n_acc;
+  rp.w_new = w_new;
+  rp.dev_status = dev_status;
+  rp.in_place = in_place;
+  rp.pos = pos;
+  rp.mask = mask;
+  rp.pm_cap = pm_cap;
+  rp.pad_out = pad_out;
+  rp.s_in = s_in;
+  rp.s_out = s_out;
+  rp.s_in_stride = s_in_stride;
+  rp.s_out_stride = s_out_stride;
+  rp.tokens = tokens;
+  rp.pad_id = pad_id;
+  hipError_t e = timed(SPECDEC_KERNEL_REALIGN, st, [&] { return specdec::launch_realign(rp, st); });
+  if (e != hipSuccess) return hip_fail(e, "realign launch");
+  if (w_new_host) {
+    e = hipMemcpyAsync(w_new_host, w_new, sizeof(int32_t), hipMemcpyDeviceToHost, st);
+    if (e != hipSuccess) return hip_fail(e, "w_new copy");
+    e = hipStreamSynchronize(st);
+    if (e != hipSuccess) return hip_fail(e, "stream synchronize");
+  }
+  return ok();
+}
+
 bool ranges_overlap(const void* a, int64_t abytes, const void* b, int64_t bbytes) {
   const uintptr_t a0 = reinterpret_cast<uintptr_t>(a), b0 = reinterpret_cast<uintptr_t>(b);
   return a0 < b0 + static_cast<uintptr_t>(bbytes) && b0 < a0 + static_cast<uintptr_t>(abytes);
@@ -312,6 +419,31 @@ specdec_status_t specdec_verify_greedy(const void* logits, int32_t dtype, const 
   hipStream_t st = static_cast<hipStream_t>(stream);
   hipError_t e = timed(SPECDEC_KERNEL_VERIFY, st, [&] { return specdec::launch_verify(p, st); });
   if (e != hipSuccess) return hip_fail(e, "verify launch");
+  return ok();
+}
+
+size_t specdec_sample_workspace_bytes(int32_t B, int32_t k, int32_t V) {
+  if (B < 0 || B > SPECDEC_MAX_B || k < 0 || k > SPECDEC_MAX_K || V < 1) return 0;
+  const int64_t rows = static_cast<int64_t>(B) * (2 * k + 1);
+  return specdec::kWsHeaderBytes + static_cast<size_t>(rows * specdec::sample_chunks(rows, V)) * 8u;
+}
+
+specdec_status_t specdec_verify_sample(const void* logits, const void* draft_logits, int32_t dtype,
+                                       const int32_t* draft, const int32_t* pad_in, const float* u_accept,
+                                       const float* u_sample, float temperature, int32_t B, int32_t k, int32_t V,
+                                       int32_t W_in, int32_t* tokens, int32_t* n_acc, int32_t* bonus,
+                                       int32_t* pad_out, int32_t* w_new, void* workspace, size_t workspace_bytes,
+                                       uint32_t* dev_status, void* stream) {
+  float c = 0.0f;
+  specdec_status_t s = check_sample_args(logits, draft_logits, dtype, draft, pad_in, u_accept, u_sample, temperature, B,
+                                         k, V, W_in, tokens, n_acc, bonus, pad_out, w_new, workspace, workspace_bytes,
+                                         dev_status, &c);
+  if (s || B == 0) return s ? s : ok();
+  specdec::SampleLaunch p{logits, draft_logits, dtype, draft, pad_in, u_accept, u_sample, c,
+                          B, k, V, W_in, tokens, n_acc, bonus, pad_out, w_new, workspace, dev_status};
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  hipError_t e = timed(SPECDEC_KERNEL_SAMPLE, st, [&] { return specdec::launch_verify_sample(p, st); });
+  if (e != hipSuccess) return hip_fail(e, "stochastic verify launch");
   return ok();
 }
 
@@ -405,59 +537,46 @@ specdec_status_t specdec_step(const void* logits, int32_t dtype, const int32_t* 
                                          pad_out, w_new, workspace, workspace_bytes);
   if (s) return s;
   bool in_place = false;
-  s = check_realign_args(src, dst, k, W_in, pad_in, n_acc, w_new, &in_place);
+  s = check_step_rest(B, k, W_in, src, dst, pad_in, n_acc, pad_out, w_new, pos, mask, pm_cap, s_in, s_in_stride, s_out,
+                      s_out_stride, dev_status, &in_place);
   if (s) return s;
-  if (src->B != B) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "cache rows B=%d differ from logits rows B=%d", src->B, B);
-  s = check_posmask_args(pad_out, w_new, B, k, pos, mask, pm_cap);
-  if (s) return s;
-  if (B > 0 && pm_cap < static_cast<int64_t>(W_in) + k + 1)
-    return fail(SPECDEC_ERR_INVALID_ARGUMENT, "pm_cap=%lld < W_in+k+1=%d", (long long)pm_cap, W_in + k + 1);
-  if (s_in || s_out) {
-    s = check_token_args(s_in, s_in_stride, s_out, s_out_stride, B, k, W_in);
-    if (s) return s;
-  }
-  if (dev_status && !aligned(dev_status, 4)) return fail(SPECDEC_ERR_UNSUPPORTED, "dev_status not 4-byte aligned");
   if (B == 0) return ok();
   hipStream_t st = static_cast<hipStream_t>(stream);
   specdec::VerifyLaunch vp{logits, dtype, draft, pad_in, B, k, V, W_in, tokens, n_acc,
                            bonus, pad_out, w_new, workspace, dev_status};
   hipError_t e = timed(SPECDEC_KERNEL_VERIFY, st, [&] { return specdec::launch_verify(vp, st); });
   if (e != hipSuccess) return hip_fail(e, "verify launch");
-  specdec::RealignLaunch rp{};
-  rp.src = src->data;
-  rp.dst = dst->data;
-  rp.src_cap = src->cap;
-  rp.dst_cap = dst->cap;
-  rp.L = src->L;
-  rp.B = src->B;
-  rp.H = src->H;
-  rp.D = src->D;
-  rp.k = k;
-  rp.W_in = W_in;
-  rp.pad_in = pad_in;
-  rp.n_acc = n_acc;
-  rp.w_new = w_new;
-  rp.dev_status = dev_status;
-  rp.in_place = in_place;
-  rp.pos = pos;
-  rp.mask = mask;
-  rp.pm_cap = pm_cap;
-  rp.pad_out = pad_out;
-  rp.s_in = s_in;
-  rp.s_out = s_out;
-  rp.s_in_stride = s_in_stride;
-  rp.s_out_stride = s_out_stride;
-  rp.tokens = tokens;
-  rp.pad_id = pad_id;
-  e = timed(SPECDEC_KERNEL_REALIGN, st, [&] { return specdec::launch_realign(rp, st); });
-  if (e != hipSuccess) return hip_fail(e, "realign launch");
-  if (w_new_host) {
-    e = hipMemcpyAsync(w_new_host, w_new, sizeof(int32_t), hipMemcpyDeviceToHost, st);
-    if (e != hipSuccess) return hip_fail(e, "w_new copy");
-    e = hipStreamSynchronize(st);
-    if (e != hipSuccess) return hip_fail(e, "stream synchronize");
-  }
-  return ok();
+  return step_realign(k, W_in, src, dst, in_place, pad_in, tokens, n_acc, pad_out, w_new, pos, mask, pm_cap, s_in,
+                      s_in_stride, s_out, s_out_stride, pad_id, dev_status, w_new_host, st);
+}
+
+specdec_status_t specdec_step_sample(const void* logits, const void* draft_logits, int32_t dtype,
+                                     const int32_t* draft, const int32_t* pad_in, const float* u_accept,
+                                     const float* u_sample, float temperature, int32_t B, int32_t k, int32_t V,
+                                     int32_t W_in, const specdec_kv_t* src, const specdec_kv_t* dst,
+                                     int32_t* tokens, int32_t* n_acc, int32_t* bonus, int32_t* pad_out,
+                                     int32_t* w_new, int64_t* pos, uint8_t* mask, int64_t pm_cap,
+                                     const int32_t* s_in, int64_t s_in_stride, int32_t* s_out,
+                                     int64_t s_out_stride, int32_t pad_id, void* workspace,
+                                     size_t workspace_bytes, uint32_t* dev_status, int32_t* w_new_host,
+                                     void* stream) {
+  float c = 0.0f;
+  specdec_status_t s = check_sample_args(logits, draft_logits, dtype, draft, pad_in, u_accept, u_sample, temperature, B,
+                                         k, V, W_in, tokens, n_acc, bonus, pad_out, w_new, workspace, workspace_bytes,
+                                         dev_status, &c);
+  if (s) return s;
+  bool in_place = false;
+  s = check_step_rest(B, k, W_in, src, dst, pad_in, n_acc, pad_out, w_new, pos, mask, pm_cap, s_in, s_in_stride, s_out,
+                      s_out_stride, dev_status, &in_place);
+  if (s) return s;
+  if (B == 0) return ok();
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  specdec::SampleLaunch sp{logits, draft_logits, dtype, draft, pad_in, u_accept, u_sample, c,
+                           B, k, V, W_in, tokens, n_acc, bonus, pad_out, w_new, workspace, dev_status};
+  hipError_t e = timed(SPECDEC_KERNEL_SAMPLE, st, [&] { return specdec::launch_verify_sample(sp, st); });
+  if (e != hipSuccess) return hip_fail(e, "stochastic verify launch");
+  return step_realign(k, W_in, src, dst, in_place, pad_in, tokens, n_acc, pad_out, w_new, pos, mask, pm_cap, s_in,
+                      s_in_stride, s_out, s_out_stride, pad_id, dev_status, w_new_host, st);
 }
 
 specdec_status_t specdec_gather_batch(const specdec_kv_t* pool, const int32_t* pool_tok, int64_t pool_tok_stride,

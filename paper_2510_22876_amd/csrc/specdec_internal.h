@@ -113,6 +113,31 @@ struct WritebackLaunch {
   uint32_t* dev_status;
 };
 
+// Stochastic verification (speculative sampling at temperature T > 0).
+struct SampleLaunch {
+  const void* logits;        // [B][k+1][V]
+  const void* draft_logits;  // [B][k][V]
+  int dtype;
+  const int32_t* draft;
+  const int32_t* pad_in;
+  const float* u_accept;
+  const float* u_sample;
+  float c;                   // log2(e) / T
+  int32_t B, k, V, W_in;
+  int32_t* tokens;
+  int32_t* n_acc;
+  int32_t* bonus;
+  int32_t* pad_out;
+  int32_t* w_new;
+  void* workspace;           // [header][per-chunk (max, sum): B*(2k+1)*chunks float2]
+  uint32_t* dev_status;
+};
+
+// Chunking of the stochastic verification's row statistics.
+int64_t sample_chunk_elems(int64_t rows, int64_t V);
+int64_t sample_chunks(int64_t rows, int64_t V);
+hipError_t launch_verify_sample(const SampleLaunch& p, hipStream_t stream);
+
 hipError_t launch_gather(const GatherLaunch& p, hipStream_t stream);
 hipError_t launch_writeback(const WritebackLaunch& p, hipStream_t stream);
 

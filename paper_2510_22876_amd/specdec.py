@@ -17,16 +17,16 @@ _LIB_PATH = Path(__file__).resolve().parent / "libspecdec.so"
 OK, ERR_INVALID_ARGUMENT, ERR_UNSUPPORTED, ERR_HIP, ERR_WORKSPACE = 0, 1, 2, 3, 4
 F32, BF16, F16 = 0, 1, 2
 DTYPE_OF = {torch.float32: F32, torch.bfloat16: BF16, torch.float16: F16}
-KERNEL_VERIFY, KERNEL_REALIGN, KERNEL_POSMASK, KERNEL_GATHER, KERNEL_WRITEBACK = 0, 1, 2, 3, 4
-TIMING_ALL = 31
+KERNEL_VERIFY, KERNEL_REALIGN, KERNEL_POSMASK, KERNEL_GATHER, KERNEL_WRITEBACK, KERNEL_SAMPLE = 0, 1, 2, 3, 4, 5
+TIMING_ALL = 63
 DEV_BAD_PAD_IN, DEV_BAD_ACCEPT, DEV_BAD_WIDTH, DEV_BAD_PAD_OUT = 1, 2, 4, 8
-DEV_BAD_SLOT, DEV_SLOT_LEN = 0x10, 0x20
+DEV_BAD_SLOT, DEV_SLOT_LEN, DEV_BAD_UNIFORM = 0x10, 0x20, 0x40
 WRITEBACK_FULL, WRITEBACK_APPEND = 0, 1
 
 EXPORTED = (
     "specdec_abi_version", "specdec_last_error", "specdec_workspace_bytes", "specdec_workspace_init",
-    "specdec_verify_greedy", "specdec_realign_kv", "specdec_build_posmask", "specdec_realign_tokens",
-    "specdec_step", "specdec_gather_batch", "specdec_scatter_accepted",
+    "specdec_verify_greedy", "specdec_sample_workspace_bytes", "specdec_verify_sample", "specdec_realign_kv", "specdec_build_posmask", "specdec_realign_tokens",
+    "specdec_step", "specdec_step_sample", "specdec_gather_batch", "specdec_scatter_accepted",
     "specdec_sched_create", "specdec_sched_destroy", "specdec_sched_next_batch", "specdec_sched_commit",
     "specdec_sched_lengths", "specdec_sched_active",
     "specdec_timing_enable", "specdec_timing_reset", "specdec_timing_query",
@@ -68,6 +68,12 @@ def _load(path: Path = _LIB_PATH) -> ctypes.CDLL:
     lib.specdec_realign_tokens.argtypes = [P, i64, P, i64, P, P, P, P, i32, i32, i32, i32, P, P]
     lib.specdec_step.argtypes = [P, i32, P, P, i32, i32, i32, i32, pKV, pKV, P, P, P, P, P, P, P, i64,
                                  P, i64, P, i64, i32, P, sz, P, P, P]
+    lib.specdec_sample_workspace_bytes.argtypes = [i32, i32, i32]
+    lib.specdec_sample_workspace_bytes.restype = sz
+    lib.specdec_verify_sample.argtypes = [P, P, i32, P, P, P, P, ctypes.c_float, i32, i32, i32, i32, P, P, P, P, P,
+                                          P, sz, P, P]
+    lib.specdec_step_sample.argtypes = [P, P, i32, P, P, P, P, ctypes.c_float, i32, i32, i32, i32, pKV, pKV, P, P, P,
+                                        P, P, P, P, i64, P, i64, P, i64, i32, P, sz, P, P, P]
     lib.specdec_gather_batch.argtypes = [pKV, P, i64, P, P, i32, i32, i32, pKV, P, i64, i32, P, P, P, i64, P, P]
     lib.specdec_scatter_accepted.argtypes = [pKV, P, P, P, P, i32, i32, i32, pKV, P, i64, P, P, i64, i32, P, P]
     lib.specdec_sched_create.argtypes = [P, i32, i32, i32, i32, i32, i32, ctypes.POINTER(P)]
@@ -83,7 +89,8 @@ def _load(path: Path = _LIB_PATH) -> ctypes.CDLL:
     for name in ("specdec_workspace_init", "specdec_verify_greedy", "specdec_realign_kv",
                  "specdec_build_posmask", "specdec_realign_tokens", "specdec_step", "specdec_timing_enable",
                  "specdec_timing_reset", "specdec_timing_query", "specdec_gather_batch",
-                 "specdec_scatter_accepted", "specdec_sched_create", "specdec_sched_next_batch",
+                 "specdec_scatter_accepted", "specdec_sched_create", "specdec_sched_next_batch", "specdec_verify_sample",
+                 "specdec_step_sample",
                  "specdec_sched_commit", "specdec_sched_lengths"):
         getattr(lib, name).restype = ctypes.c_int
     return lib
@@ -186,6 +193,44 @@ def specdec_verify_greedy(logits, draft, pad_in, W_in: int, tokens, n_acc, bonus
         _p(logits), DTYPE_OF[logits.dtype], _p(draft), _p(pad_in), B, kp1 - 1, V, W_in,
         _p(tokens), _p(n_acc), _p(bonus), _p(pad_out), _p(w_new),
         _p(workspace), workspace.numel() * workspace.element_size(), _p(dev_status), _stream(stream)))
+
+
+def sample_workspace_bytes(B: int, k: int, V: int) -> int:
+    return lib.specdec_sample_workspace_bytes(B, k, V)
+
+
+def alloc_sample_workspace(B: int, k: int, V: int, device="cuda") -> torch.Tensor:
+    """A workspace tensor for specdec_verify_sample (needs no initialisation)."""
+    n = sample_workspace_bytes(B, k, V)
+    return torch.empty((n + 7) // 8, dtype=torch.int64, device=device)
+
+
+def specdec_verify_sample(logits, draft_logits, draft, pad_in, u_accept, u_sample, temperature: float, W_in: int,
+                          tokens, n_acc, bonus, pad_out, w_new, workspace, dev_status=None, stream=None) -> None:
+    """Stochastic (T > 0) verification by speculative sampling with the
+    caller's uniforms (u_accept [B][k], u_sample [B], float32)."""
+    if logits.dim() != 3 or logits.dtype not in DTYPE_OF or not logits.is_cuda or not logits.is_contiguous():
+        raise ValueError("logits must be a contiguous device tensor [B][k+1][V] of float32/bfloat16/float16")
+    B, kp1, V = logits.shape
+    k = kp1 - 1
+    _req("draft_logits", draft_logits, (B, k, V), logits.dtype)
+    _req("draft", draft, (B, k), torch.int32)
+    _req("pad_in", pad_in, (B,), torch.int32)
+    _req("u_accept", u_accept, (B, k), torch.float32)
+    _req("u_sample", u_sample, (B,), torch.float32)
+    _req("tokens", tokens, (B, kp1), torch.int32)
+    _req("n_acc", n_acc, (B,), torch.int32)
+    _req("bonus", bonus, (B,), torch.int32, optional=True)
+    _req("pad_out", pad_out, (B,), torch.int32)
+    _req("w_new", w_new, (1,), torch.int32)
+    _req("dev_status", dev_status, (1,), torch.int32, optional=True)
+    nb = workspace.numel() * workspace.element_size()
+    if nb < sample_workspace_bytes(B, k, V) or not workspace.is_cuda:
+        raise ValueError("workspace too small")
+    _check(lib.specdec_verify_sample(_p(logits), _p(draft_logits), DTYPE_OF[logits.dtype], _p(draft), _p(pad_in),
+                                     _p(u_accept), _p(u_sample), float(temperature), B, k, V, W_in, _p(tokens),
+                                     _p(n_acc), _p(bonus), _p(pad_out), _p(w_new), _p(workspace), nb,
+                                     _p(dev_status), _stream(stream)))
 
 
 def specdec_realign_kv(src, dst, k: int, W_in: int, pad_in, n_acc, w_new, dev_status=None,
@@ -363,6 +408,46 @@ class Scheduler:
 
     def has_active(self) -> bool:
         return lib.specdec_sched_active(self._h) > 0
+
+
+def specdec_step_sample(logits, draft_logits, draft, pad_in, u_accept, u_sample, temperature: float, W_in: int,
+                        src, dst, tokens, n_acc, bonus, pad_out, w_new, pos, mask, workspace, dev_status=None,
+                        sync_w_new: bool = False, stream=None, s_in=None, s_out=None, pad_id: int = 0):
+    """The fused step with stochastic verification (speculative sampling with
+    the caller's uniforms); returns L' as a Python int when ``sync_w_new``."""
+    B, kp1, V = logits.shape
+    k = kp1 - 1
+    if logits.dtype not in DTYPE_OF or not logits.is_cuda or not logits.is_contiguous():
+        raise ValueError("logits must be a contiguous device tensor [B][k+1][V] of float32/bfloat16/float16")
+    _req("draft_logits", draft_logits, (B, k, V), logits.dtype)
+    for name, t, shape, dt in (("draft", draft, (B, k), torch.int32), ("pad_in", pad_in, (B,), torch.int32),
+                               ("u_accept", u_accept, (B, k), torch.float32), ("u_sample", u_sample, (B,), torch.float32),
+                               ("tokens", tokens, (B, kp1), torch.int32), ("n_acc", n_acc, (B,), torch.int32),
+                               ("pad_out", pad_out, (B,), torch.int32), ("w_new", w_new, (1,), torch.int32)):
+        _req(name, t, shape, dt)
+    _req("bonus", bonus, (B,), torch.int32, optional=True)
+    _req("dev_status", dev_status, (1,), torch.int32, optional=True)
+    sdesc, ddesc = kv_desc(src), kv_desc(dst)
+    if sdesc.B != B:
+        raise ValueError("cache rows differ from logit rows")
+    _req("pos", pos, (B, pos.shape[1]), torch.int64)
+    _req("mask", mask, (B, pos.shape[1]), torch.uint8)
+    if (s_in is None) != (s_out is None):
+        raise ValueError("give both s_in and s_out, or neither")
+    if s_in is not None:
+        _req("s_in", s_in, (B, s_in.shape[1]), torch.int32)
+        _req("s_out", s_out, (B, s_out.shape[1]), torch.int32)
+    nb = workspace.numel() * workspace.element_size()
+    if nb < sample_workspace_bytes(B, k, V) or not workspace.is_cuda:
+        raise ValueError("workspace too small")
+    host = ctypes.c_int32(-1)
+    _check(lib.specdec_step_sample(
+        _p(logits), _p(draft_logits), DTYPE_OF[logits.dtype], _p(draft), _p(pad_in), _p(u_accept), _p(u_sample),
+        float(temperature), B, k, V, W_in, ctypes.byref(sdesc), ctypes.byref(ddesc), _p(tokens), _p(n_acc), _p(bonus),
+        _p(pad_out), _p(w_new), _p(pos), _p(mask), pos.shape[1], _p(s_in), s_in.shape[1] if s_in is not None else 0,
+        _p(s_out), s_out.shape[1] if s_out is not None else 0, pad_id, _p(workspace), nb, _p(dev_status),
+        ctypes.byref(host) if sync_w_new else None, _stream(stream)))
+    return host.value if sync_w_new else None
 
 
 def timing_enable(on=True) -> None:

@@ -363,3 +363,35 @@ def make_pool(w: Workload, lens: np.ndarray, cap: int, tok_stride: int, seed: in
     for s in range(N):
         tok[s, : lens[s] + 1] = r.integers(0, max(w.V, 1), size=int(lens[s]) + 1)
     return pool, torch.as_tensor(tok, device=device)
+
+
+# ---- stochastic verification inputs ----------------------------------------------
+
+_T_SAMPLE_TARGET, _T_SAMPLE_NOISE, _T_SAMPLE_DRAFT, _T_SAMPLE_U = 30, 31, 32, 33
+
+
+def sampled_inputs(w: Workload, seed: int = 0, step: int = 0, device="cpu", temperature: float = 1.0,
+                   noise: float = 1.0):
+    """Inputs of one stochastic verification: target logits [B,k+1,V] ~
+    N(0, std^2) and draft logits = the first k target rows + N(0, noise^2)
+    (both rounded to the workload's logit dtype), so the draft model is a
+    perturbed copy of the target: at T = 1 and noise 1 with std 2, each draft
+    is accepted with probability about 0.6 (1 - the total-variation distance
+    of the two softmaxes); drafts drawn from the draft distribution q; and the
+    uniforms u_accept [B,k], u_sample [B] in [0, 1).  Returns (logits,
+    draft_logits, draft int32, u_accept, u_sample)."""
+    dt = TORCH_DT[w.logit_dtype]
+    B, k, V = w.B, w.k, w.V
+    g = torch.Generator(device=device)
+    g.manual_seed(_torch_seed(seed, _T_SAMPLE_TARGET, step))
+    target = torch.randn((B, k + 1, V), generator=g, device=device, dtype=torch.float32) * w.logit_std
+    g.manual_seed(_torch_seed(seed, _T_SAMPLE_NOISE, step))
+    dlog = target[:, :k] + torch.randn((B, k, V), generator=g, device=device, dtype=torch.float32) * noise
+    logits, draft_logits = target.to(dt), dlog.to(dt)
+    q = torch.softmax(draft_logits.float() / temperature, dim=-1).reshape(B * k, V) if k else None
+    g.manual_seed(_torch_seed(seed, _T_SAMPLE_DRAFT, step))
+    draft = (torch.multinomial(q, 1, generator=g).reshape(B, k).to(torch.int32) if k
+             else torch.zeros((B, 0), dtype=torch.int32, device=device))
+    g.manual_seed(_torch_seed(seed, _T_SAMPLE_U, step))
+    u = torch.rand((B, k + 1), generator=g, device=device, dtype=torch.float32)
+    return logits, draft_logits, draft, u[:, :k].contiguous(), u[:, k].contiguous()

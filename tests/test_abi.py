@@ -182,9 +182,10 @@ def test_realign_tokens_rejects(sd):
 
 def test_timing_query_rejects_unknown_kernel(sd):
     assert sd.lib.specdec_timing_query(7, None, None) == 1
+    assert sd.lib.specdec_timing_query(6, None, None) == 1
     assert sd.lib.specdec_timing_enable(0) == 0
-    assert sd.lib.specdec_timing_enable(31) == 0
-    assert sd.lib.specdec_timing_enable(32) == 1
+    assert sd.lib.specdec_timing_enable(63) == 0
+    assert sd.lib.specdec_timing_enable(64) == 1
     assert sd.lib.specdec_timing_enable(0) == 0
     assert sd.lib.specdec_timing_enable(-1) == 1
 
@@ -269,3 +270,33 @@ def test_scatter_rejects(sd):
     assert _scatter(sd, lens=None) == 1
     assert _scatter(sd, B=0, batch=K(B=0, cap=32), pads=None, tokens=None, n_acc=None, slots=None,
                     lens=None) == 0
+
+
+def _sample(sd, **over):
+    args = dict(logits=A, draft_logits=A + (1 << 28), dtype=1, draft=A, pad_in=A, u_accept=A, u_sample=A, T=0.8,
+                B=2, k=3, V=100, W_in=10, tokens=A, n_acc=A, bonus=A, pad_out=A, w_new=A, ws=A,
+                ws_bytes=sd.sample_workspace_bytes(2, 3, 100), status=None, stream=None)
+    args.update(over)
+    return sd.lib.specdec_verify_sample(*args.values())
+
+
+@pytest.mark.parametrize("over,code", [
+    (dict(B=-1), 1), (dict(k=65), 1), (dict(V=0), 1), (dict(W_in=3), 1), (dict(dtype=5), 2),
+    (dict(T=0.0), 1), (dict(T=-1.0), 1), (dict(T=float("inf")), 1), (dict(T=float("nan")), 1), (dict(T=1e-39), 1),
+    (dict(logits=None), 1), (dict(draft_logits=None), 1), (dict(u_accept=None), 1), (dict(u_sample=None), 1),
+    (dict(draft=None), 1), (dict(w_new=None), 1), (dict(logits=A + 1), 2), (dict(u_sample=A + 2), 2),
+    (dict(ws=None), 4), (dict(ws=A + 4), 4), (dict(ws_bytes=64), 4), (dict(B=40000, k=20), 1),
+])
+def test_verify_sample_rejects(sd, over, code):
+    _no_gpu()
+    assert _sample(sd, **over) == code
+    assert sd.lib.specdec_last_error().decode() != ""
+
+
+def test_verify_sample_empty_and_workspace(sd):
+    _no_gpu()
+    assert _sample(sd, B=0, logits=None, draft_logits=None, draft=None, pad_in=None, u_accept=None, u_sample=None,
+                   tokens=None, n_acc=None, pad_out=None, w_new=None, ws=None) == 0
+    # k = 0 needs no draft tensors
+    assert sd.sample_workspace_bytes(8, 5, 32000) == 256 + 8 * 11 * 16 * 8
+    assert sd.sample_workspace_bytes(-1, 0, 5) == 0 and sd.sample_workspace_bytes(1, 65, 5) == 0
