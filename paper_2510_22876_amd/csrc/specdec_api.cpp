@@ -425,7 +425,9 @@ specdec_status_t specdec_verify_greedy(const void* logits, int32_t dtype, const 
 size_t specdec_sample_workspace_bytes(int32_t B, int32_t k, int32_t V) {
   if (B < 0 || B > SPECDEC_MAX_B || k < 0 || k > SPECDEC_MAX_K || V < 1) return 0;
   const int64_t rows = static_cast<int64_t>(B) * (2 * k + 1);
-  return specdec::kWsHeaderBytes + static_cast<size_t>(rows * specdec::sample_chunks(rows, V)) * 8u;
+  // chunk statistics of every row, then per (sequence, chunk) the two masses and two last indices
+  return specdec::kWsHeaderBytes + static_cast<size_t>((rows + 2 * static_cast<int64_t>(B)) *
+                                                       specdec::sample_chunks(rows, V)) * 8u;
 }
 
 specdec_status_t specdec_verify_sample(const void* logits, const void* draft_logits, int32_t dtype,

@@ -129,7 +129,7 @@ struct SampleLaunch {
   int32_t* bonus;
   int32_t* pad_out;
   int32_t* w_new;
-  void* workspace;           // [header][per-chunk (max, sum): B*(2k+1)*chunks float2]
+  void* workspace;           // [header][chunk (max, sum): B*(2k+1)*chunks float2][masses, last indices]
   uint32_t* dev_status;
 };
 
