@@ -74,6 +74,7 @@ typedef enum { SPECDEC_F32 = 0, SPECDEC_BF16 = 1, SPECDEC_F16 = 2 } specdec_dtyp
 #define SPECDEC_MAX_ROWS 1048576      /* B*(k+1)                                   */
 #define SPECDEC_MAX_WIDTH 16777216    /* W_in, cap and pm_cap                      */
 #define SPECDEC_MAX_D 4096
+#define SPECDEC_MAX_SAMPLE_V 8388608  /* vocabulary of stochastic verification          */
 
 /* A bf16 KV cache [L][2][B][H][cap][D], contiguous, D fastest.  One
  * (layer, K/V, row, head) "span" is cap*D contiguous elements.  `data` is a
@@ -167,7 +168,8 @@ specdec_status_t specdec_verify_greedy(const void* logits, int32_t dtype, const 
  * Arithmetic is fp32 (exp2 of scaled differences from the row maximum, sums
  * in a fixed parallel order): a decision whose fp64 margin is within the
  * fp32 rounding of these sums may differ from an fp64 evaluation.
- * Limits as specdec_verify_greedy, with B*(2k+1) <= SPECDEC_MAX_ROWS.
+ * Limits as specdec_verify_greedy, with B*(2k+1) <= SPECDEC_MAX_ROWS and
+ * V <= SPECDEC_MAX_SAMPLE_V.
  */
 size_t specdec_sample_workspace_bytes(int32_t B, int32_t k, int32_t V);
 

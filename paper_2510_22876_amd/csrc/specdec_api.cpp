@@ -244,7 +244,8 @@ specdec_status_t check_sample_args(const void* logits, const void* draft_logits,
                                    size_t workspace_bytes, const uint32_t* dev_status, float* c_out) {
   if (B < 0 || B > SPECDEC_MAX_B) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "B=%d outside [0,%d]", B, SPECDEC_MAX_B);
   if (k < 0 || k > SPECDEC_MAX_K) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "k=%d outside [0,%d]", k, SPECDEC_MAX_K);
-  if (V < 1) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "V=%d must be >= 1", V);
+  if (V < 1 || V > SPECDEC_MAX_SAMPLE_V)
+    return fail(SPECDEC_ERR_INVALID_ARGUMENT, "V=%d outside [1, %d]", V, SPECDEC_MAX_SAMPLE_V);
   if (W_in < k + 1 || W_in > SPECDEC_MAX_WIDTH)
     return fail(SPECDEC_ERR_INVALID_ARGUMENT, "W_in=%d outside [k+1=%d, %d]", W_in, k + 1, SPECDEC_MAX_WIDTH);
   const int eb = logit_bytes(dtype);
@@ -423,11 +424,16 @@ specdec_status_t specdec_verify_greedy(const void* logits, int32_t dtype, const 
 }
 
 size_t specdec_sample_workspace_bytes(int32_t B, int32_t k, int32_t V) {
-  if (B < 0 || B > SPECDEC_MAX_B || k < 0 || k > SPECDEC_MAX_K || V < 1) return 0;
+  if (B < 0 || B > SPECDEC_MAX_B || k < 0 || k > SPECDEC_MAX_K || V < 1 || V > SPECDEC_MAX_SAMPLE_V) return 0;
   const int64_t rows = static_cast<int64_t>(B) * (2 * k + 1);
-  // chunk statistics of every row, then per (sequence, chunk) the two masses and two last indices
-  return specdec::kWsHeaderBytes + static_cast<size_t>((rows + 2 * static_cast<int64_t>(B)) *
-                                                       specdec::sample_chunks(rows, V)) * 8u;
+  // chunk statistics of every row, then per (sequence, chunk) the two last
+  // indices and per (sequence, chunk, tile of 2048 logits) the two masses
+  const int64_t chunks = specdec::sample_chunks(rows, V);
+  const int64_t mc = specdec::sample_mass_chunk_elems(V);
+  const int64_t mchunks = (V + mc - 1) / mc;
+  const int64_t tiles = (mc + 2047) / 2048;
+  return specdec::kWsHeaderBytes + static_cast<size_t>(B) * 16u +
+         static_cast<size_t>(rows * chunks + B * mchunks * (1 + tiles)) * 8u;
 }
 
 specdec_status_t specdec_verify_sample(const void* logits, const void* draft_logits, int32_t dtype,

@@ -298,5 +298,5 @@ def test_verify_sample_empty_and_workspace(sd):
     assert _sample(sd, B=0, logits=None, draft_logits=None, draft=None, pad_in=None, u_accept=None, u_sample=None,
                    tokens=None, n_acc=None, pad_out=None, w_new=None, ws=None) == 0
     # k = 0 needs no draft tensors
-    assert sd.sample_workspace_bytes(8, 5, 32000) == 256 + (8 * 11 + 2 * 8) * 16 * 8
+    assert sd.sample_workspace_bytes(8, 5, 32000) == 256 + 8 * 16 + (8 * 11 + 8 + 8 * 1) * 16 * 8
     assert sd.sample_workspace_bytes(-1, 0, 5) == 0 and sd.sample_workspace_bytes(1, 65, 5) == 0

@@ -148,6 +148,8 @@ CASES = [
     (6, 3, 1, "f32", 1.0, "uniform"),           # V = 1
     (64, 4, 151936, "bf16", 0.7, "sampled"),    # stress-shaped vocabulary
     (8, 5, 32000, "bf16", 0.05, "greedy"),      # near-greedy
+    (3, 1, 1000000, "f32", 0.9, "sampled"),     # 64 chunks of 8 tiles
+    (2, 2, 5000000, "bf16", 1.0, "sampled"),    # 39 tiles per chunk
 ]
 
 
