@@ -68,6 +68,10 @@ class Oracle:
         lib.oracle_verify_sample.argtypes = [P, P, ctypes.c_int, P, P, P, P, ctypes.c_double, i32, i32, i64, i32,
                                              P, P, P, P, P]
         lib.oracle_verify_sample.restype = ctypes.c_int
+        lib.oracle_rollback.argtypes = [P, P, P, i32, i32, i32, P, P, P, P]
+        lib.oracle_rollback.restype = ctypes.c_int
+        lib.oracle_varlen_rollback.argtypes = [P, P, i64, i32, i32, i32, P, P, i32, i32, P, P]
+        lib.oracle_varlen_rollback.restype = ctypes.c_int
         self.lib = lib
 
 
@@ -173,6 +177,44 @@ def verify_sample(logits, draft_logits, dtype: str, draft, pad_in, u_accept, u_s
     if rc:
         raise OracleError(f"oracle_verify_sample rejected its arguments (code {rc})")
     return dict(tokens=tokens, n_acc=n_acc, bonus=bonus, pad_out=pad_out, w_new=int(w_new[0]))
+
+
+def rollback(tokens, n_acc, pad_in, W_in: int, oracle: Oracle | None = None):
+    """Family A rollback: every row truncated to the batch-minimum accepted
+    count m; returns dict(n_acc (all m), bonus = tokens[i][m], pad_out, w_new)
+    by Eq. (1) and Eq. (2) with a_i = m + 1."""
+    tk = _c(np.asarray(tokens), np.int32)
+    B, kp1 = tk.shape
+    na = _c(np.asarray(n_acc).reshape(B), np.int32)
+    pad = _c(np.asarray(pad_in).reshape(B), np.int32)
+    out = dict(n_acc=np.zeros(B, np.int32), bonus=np.zeros(B, np.int32), pad_out=np.zeros(B, np.int32))
+    w = np.zeros(1, np.int32)
+    rc = _load(oracle).oracle_rollback(_ptr(tk), _ptr(na), _ptr(pad), B, kp1 - 1, W_in, _ptr(out["n_acc"]),
+                                       _ptr(out["bonus"]), _ptr(out["pad_out"]), _ptr(w))
+    if rc:
+        raise OracleError(f"oracle_rollback rejected its arguments (code {rc})")
+    out["w_new"] = int(w[0])
+    return out
+
+
+def varlen_rollback(src, cu_in, n_acc, k: int, dst=None, oracle: Oracle | None = None):
+    """Family B rollback on a flat cache [L][2][T_cap][H][D] (uint16 bf16
+    bits): sequence i keeps its first len_i - (k - n_acc[i]) rows, compacted;
+    returns (dst, cu_out int32 [B+1], pos int64 [T_cap] (rows beyond cu_out[B]
+    are -1))."""
+    sb = _kv_bits(src) if not isinstance(src, np.ndarray) else _c(src, np.uint16)
+    nl, two, T_cap, H, D = sb.shape
+    cu = _c(np.asarray(cu_in).reshape(-1), np.int32)
+    B = cu.size - 1
+    na = _c(np.asarray(n_acc).reshape(B), np.int32)
+    out = np.zeros_like(sb) if dst is None else dst
+    cu_out = np.zeros(B + 1, np.int32)
+    pos = np.full(T_cap, -1, np.int64)
+    rc = _load(oracle).oracle_varlen_rollback(_ptr(sb), _ptr(out), T_cap, nl, H, D, _ptr(cu), _ptr(na), B, k,
+                                              _ptr(cu_out), _ptr(pos))
+    if rc:
+        raise OracleError(f"oracle_varlen_rollback rejected its arguments (code {rc})")
+    return out, cu_out, pos
 
 
 def _kv_bits(kv):

@@ -511,3 +511,73 @@ int oracle_verify_sample(const void* logits, const void* draft_logits, int dtype
   *w_new = Lp;
   return OR_OK;
 }
+
+/* ---- rollback (Family A) and variable-length rollback (Family B) ------------ */
+
+/*
+ * Rollback (Section 2, "Family A: contiguous layout"): every row is truncated
+ * to the batch-minimum accepted count m = min_i n_acc[i], so every row appends
+ * the same a = m + 1 cache entries and the same tokens[i][0 .. m] (for a row
+ * that accepted more, tokens[i][m] is the target's prediction at slot m, equal
+ * to its draft there).  The width and paddings then follow Eq. (1) and
+ * Eq. (2) with a_i = m + 1 for every row; all offsets are equal (zero when the
+ * minimum input padding is 0, Corollary B.4), so no cached entry moves.
+ * Verified tokens beyond m are discarded.
+ */
+int oracle_rollback(const int32_t* tokens, const int32_t* n_acc, const int32_t* pad_in, int32_t B, int32_t k,
+                    int32_t W_in, int32_t* n_acc_out, int32_t* bonus_out, int32_t* pad_out, int32_t* w_new) {
+  if (B < 0 || k < 0 || W_in < k + 1) return OR_EINVAL;
+  const int32_t L = W_in - (k + 1);
+  int32_t m = k;
+  for (int32_t i = 0; i < B; ++i) {
+    if (pad_in[i] < 0 || pad_in[i] > L || n_acc[i] < 0 || n_acc[i] > k) return OR_EINVAL;
+    if (n_acc[i] < m) m = n_acc[i];
+  }
+  int32_t Lp = 0;
+  for (int32_t i = 0; i < B; ++i) {
+    n_acc_out[i] = m;
+    bonus_out[i] = tokens[(int64_t)i * (k + 1) + m];
+    if ((L - pad_in[i]) + m + 1 > Lp) Lp = (L - pad_in[i]) + m + 1;   /* Eq. (1) */
+  }
+  for (int32_t i = 0; i < B; ++i) pad_out[i] = pad_in[i] + ((Lp - L) - (m + 1));   /* Eq. (2) */
+  *w_new = B > 0 ? Lp : 0;
+  return OR_OK;
+}
+
+/*
+ * Variable-length rollback (Section 2, "Family B: variable-length layout"):
+ * the cache is a flat buffer per (layer, K/V), [T][H][D], sequence i holding
+ * rows [cu_in[i], cu_in[i+1]): its cached entries followed by its k+1 verify
+ * window entries.  I1 does not arise; I2 requires the rejected entries to be
+ * rolled back: sequence i keeps its first len_i - (k - n_acc[i]) rows (the
+ * window entries of the pending token and the accepted drafts) and the
+ * buffer is compacted, cu_out being the running sum of the kept lengths.
+ * Position ids are each kept row's index within its sequence.  Rows of the
+ * output beyond cu_out[B] are left as they are.
+ *   src, dst  bf16 bits [n_layers][2][T_cap][H][D] (dst separate from src)
+ *   pos       int64 [T_cap]: positions for rows [0, cu_out[B])
+ */
+int oracle_varlen_rollback(const uint16_t* src, uint16_t* dst, int64_t T_cap, int32_t n_layers, int32_t H, int32_t D,
+                           const int32_t* cu_in, const int32_t* n_acc, int32_t B, int32_t k, int32_t* cu_out,
+                           int64_t* pos) {
+  if (B < 0 || k < 0 || n_layers < 0 || H < 0 || D <= 0 || T_cap < 0) return OR_EINVAL;
+  if (cu_in[0] < 0) return OR_EINVAL;
+  for (int32_t i = 0; i < B; ++i) {
+    const int64_t len = (int64_t)cu_in[i + 1] - cu_in[i];
+    if (len < k + 1 || cu_in[i + 1] > T_cap || n_acc[i] < 0 || n_acc[i] > k) return OR_EINVAL;
+  }
+  const int64_t row = (int64_t)H * D;
+  cu_out[0] = 0;
+  for (int32_t i = 0; i < B; ++i) {
+    const int64_t keep = (int64_t)cu_in[i + 1] - cu_in[i] - (k - n_acc[i]);
+    cu_out[i + 1] = cu_out[i] + (int32_t)keep;
+    for (int32_t l = 0; l < n_layers; ++l)
+      for (int32_t kv = 0; kv < 2; ++kv) {
+        const uint16_t* s = src + ((int64_t)l * 2 + kv) * T_cap * row + (int64_t)cu_in[i] * row;
+        uint16_t* d = dst + ((int64_t)l * 2 + kv) * T_cap * row + (int64_t)cu_out[i] * row;
+        memcpy(d, s, sizeof(uint16_t) * (size_t)(keep * row));
+      }
+    for (int64_t t = 0; t < keep; ++t) pos[cu_out[i] + t] = t;
+  }
+  return OR_OK;
+}

@@ -56,6 +56,9 @@ class OracleBackend:
     def verify(self, logits, draft, pads, W_in):
         return oracle.verify(logits, "f32", draft, pads, W_in)
 
+    def rollback(self, tokens, n_acc, pads, W_in):
+        return oracle.rollback(tokens, n_acc, pads, W_in)
+
     def scatter(self, batch, pads, tokens, n_acc, slots, Lb, pool, pool_tok, lens, batch_tok):
         oracle.scatter_accepted(batch, pads, tokens, n_acc, slots, Lb, pool, pool_tok, lens, batch_tok)
 
@@ -134,10 +137,12 @@ def run_exspec(be, model: ToyModel, prompts, sched, k: int, max_new: int) -> Loo
     return LoopResult(gen, trace, pool_h, tok_h, lens_h)
 
 
-def run_eqspec(be, model: ToyModel, prompts, B: int, k: int, max_new: int) -> LoopResult:
+def run_eqspec(be, model: ToyModel, prompts, B: int, k: int, max_new: int, rollback: bool = False) -> LoopResult:
     """Algorithm 1: consecutive groups of B prompts, each decoded as one fixed
     batch, realigned after every verification, until every row has generated
-    max_new tokens."""
+    max_new tokens.  With ``rollback`` every round is truncated to the batch's
+    minimum accepted count first (Family A rollback); the trace then records
+    the accepted counts before truncation."""
     gen = [None] * len(prompts)
     trace = []
     for g0 in range(0, len(prompts), B):
@@ -161,11 +166,15 @@ def run_eqspec(be, model: ToyModel, prompts, B: int, k: int, max_new: int) -> Lo
             draft, logits = _model_round(model, be, kv_d, s_d, np.asarray(be.to_host(pads_d)), W0, k, pos, mask)
             W_in = W0 + k + 1
             v = be.verify(be.from_host(logits), be.from_host(draft), pads_d, W_in)
+            if rollback:
+                verified = np.asarray(be.to_host(v["n_acc"]), np.int32)
+                v = dict(v, **be.rollback(v["tokens"], v["n_acc"], pads_d, W_in))
             w_new = int(np.asarray(be.to_host(v["w_new"])).reshape(-1)[0])
             kv_d, s_d = be.realign(kv_d, k, W_in, pads_d, v["n_acc"], v["w_new"], v["tokens"], s_d, PAD_ID)
             n_acc = np.asarray(be.to_host(v["n_acc"]), np.int32)
             made += n_acc + 1
-            trace.append((list(range(g0, g0 + nb)), W0, False, False, [int(x) for x in n_acc]))
+            trace.append((list(range(g0, g0 + nb)), W0, False, False,
+                          [int(x) for x in (verified if rollback else n_acc)]))
             pads_d = v["pad_out"]
             W0 = w_new
             if W0 + k + 1 > cap:

@@ -783,6 +783,114 @@ def pin_sample_special_cases(o=None):
     checker.check_geometry(pad, a["n_acc"], a["pad_out"], a["w_new"], W_in, k)
 
 
+# ---- rollback (Family A) and variable-length rollback (Family B) ----------------------------------
+
+def pin_rollback_list_model(o=None):
+    """Family A rollback: every row keeps the batch-minimum accepted count m and
+    appends tokens[i][0..m]; with Eq. (1)-(2) at a_i = m + 1 every offset is
+    equal (zero when the minimum padding is 0, Corollary B.4), so realigning
+    the cache moves no entry, and the realigned rows equal a list model that
+    keeps c_i + m + 1 entries."""
+    rng = np.random.default_rng(41)
+    for trial in range(20):
+        B, k = int(rng.integers(1, 7)), int(rng.integers(0, 5))
+        L = int(rng.integers(k + 1, 20))
+        W_in = L + k + 1
+        pad = rng.integers(0, L + 1, size=B).astype(np.int32)
+        if trial % 2 == 0:
+            pad[rng.integers(B)] = 0
+        tokens = rng.integers(0, 100, size=(B, k + 1)).astype(np.int32)
+        n_acc = rng.integers(0, k + 1, size=B).astype(np.int32)
+        r = oracle.rollback(tokens, n_acc, pad, W_in, oracle=o)
+        m = int(n_acc.min())
+        assert np.all(r["n_acc"] == m) and np.array_equal(r["bonus"], tokens[:, m])
+        c = L - pad
+        assert r["w_new"] == int((c + m + 1).max())
+        delta = r["pad_out"] - pad
+        assert np.all(delta == delta[0]) and (pad.min() > 0 or delta[0] == 0)
+        # the cache: a list model per row, and no move at all when the offsets are zero
+        kv = rng.integers(1, 0x7F00, size=(1, 2, B, 2, W_in, 8), dtype=np.uint16)
+        for i in range(B):
+            kv[:, :, i, :, : pad[i], :] = 0
+        out = oracle.realign_kv(kv, k, W_in, pad, r["n_acc"], r["w_new"], oracle=o)
+        for i in range(B):
+            seq = [kv[:, :, i, :, j, :] for j in range(pad[i], L + m + 1)]
+            rows = [out[:, :, i, :, j, :] for j in range(r["pad_out"][i], r["w_new"])]
+            assert len(seq) == len(rows) and all(np.array_equal(a, b) for a, b in zip(seq, rows))
+        if pad.min() == 0:
+            assert np.array_equal(out[..., : r["w_new"], :], kv[..., : r["w_new"], :])
+
+
+def pin_rollback_output_equivalence(o=None):
+    """Family A rollback is correct (Corollary B.2 still holds) but discards
+    verified tokens: a rollback decoding loop over the toy model generates what
+    sequential greedy decoding generates, in more rounds than dynamic padding."""
+    from tests import exspec_loop as el
+    for seed, (N, B, k) in enumerate([(6, 3, 4), (4, 4, 3)]):
+        model, prompts = _toy_setup(200 + seed, N, equal_groups=0, lo=2, hi=20)
+        res = el.run_eqspec(el.OracleBackend(), model, prompts, B, k, 10, rollback=True)
+        el.check_equivalence(model, prompts, res, 10)
+        dyn = el.run_eqspec(el.OracleBackend(), model, prompts, B, k, 10)
+        wasted = sum(sum(a) - len(a) * min(a) for _, _, _, _, a in res.trace)
+        assert wasted > 0 and len(res.trace) >= len(dyn.trace)
+
+
+def _varlen_case(rng, B, k, L, H, D, extra=5):
+    c = rng.integers(0, 12, size=B)
+    lens = c + k + 1
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    T_cap = int(cu[-1]) + extra
+    src = rng.integers(1, 0x7F00, size=(L, 2, T_cap, H, D), dtype=np.uint16)
+    n_acc = rng.integers(0, k + 1, size=B).astype(np.int32)
+    return c, cu, src, n_acc, T_cap
+
+
+def pin_varlen_list_model(o=None):
+    """Family B rollback: each sequence, read as a list of rows, keeps its first
+    c_i + n_acc_i + 1 rows in order; the offsets are the running sum of the kept
+    lengths, each kept row's position id is its index in its sequence, and rows
+    beyond the new total are not written."""
+    rng = np.random.default_rng(42)
+    for trial in range(12):
+        B, k = int(rng.integers(1, 6)), int(rng.integers(0, 5))
+        c, cu, src, n_acc, T_cap = _varlen_case(rng, B, k, 2, int(rng.integers(1, 3)), 8)
+        dst0 = np.full_like(src, 0xABCD)
+        out, cu_out, pos = oracle.varlen_rollback(src, cu, n_acc, k, dst=dst0, oracle=o)
+        expect_cu = [0]
+        for i in range(B):
+            seq = [src[:, :, r] for r in range(cu[i], cu[i + 1])][: c[i] + n_acc[i] + 1]
+            got = [out[:, :, r] for r in range(cu_out[i], cu_out[i + 1])]
+            assert len(seq) == len(got) and all(np.array_equal(a, b) for a, b in zip(seq, got))
+            assert list(pos[cu_out[i]: cu_out[i + 1]]) == list(range(len(seq)))
+            expect_cu.append(expect_cu[-1] + len(seq))
+        assert list(cu_out) == expect_cu
+        assert np.all(out[:, :, cu_out[-1]:] == 0xABCD) and np.all(pos[cu_out[-1]:] == -1)
+
+
+def pin_varlen_equals_padded_realign(o=None):
+    """The two layouts agree (Theorem B.1's relocation): a variable-length
+    buffer rolled back, and the same sequences left-padded into a rectangular
+    batch (windows at [L, L+k+1)) and realigned by EqSpec's unpad-append-repad,
+    hold the same rows for every sequence."""
+    rng = np.random.default_rng(43)
+    for trial in range(8):
+        B, k, H, D = int(rng.integers(1, 6)), int(rng.integers(0, 5)), 2, 8
+        c, cu, src, n_acc, T_cap = _varlen_case(rng, B, k, 1, H, D)
+        out, cu_out, pos = oracle.varlen_rollback(src, cu, n_acc, k, oracle=o)
+        L = int(c.max())
+        W_in = L + k + 1
+        batch = np.zeros((1, 2, B, H, W_in, D), np.uint16)
+        pad = (L - c).astype(np.int32)
+        for i in range(B):
+            batch[:, :, i, :, pad[i]:, :] = np.moveaxis(src[:, :, cu[i]: cu[i + 1]], 2, 3)
+        v = _verify_from_accepts(pad, n_acc, k, W_in, o=o)
+        re = oracle.realign_kv(batch, k, W_in, pad, v["n_acc"], v["w_new"], oracle=o)
+        for i in range(B):
+            a = np.moveaxis(re[:, :, i, :, v["pad_out"][i]: v["w_new"], :], 3, 2)
+            b = out[:, :, cu_out[i]: cu_out[i + 1]]
+            assert np.array_equal(a, b)
+
+
 ALL_PINS = [
     pin_argmax_bruteforce, pin_argmax_torch, pin_argmax_specials, pin_widening_pairs,
     pin_verify_planted, pin_verify_alg3_vectorised, pin_width_exhaustive,
@@ -792,4 +900,6 @@ ALL_PINS = [
     pin_scatter_appends_to_batch_row, pin_exspec_output_equivalence, pin_eqspec_output_equivalence,
     pin_scheduler_properties, pin_scheduler_grouping_rate,
     pin_sample_preserves_target_distribution, pin_sample_special_cases,
+    pin_rollback_list_model, pin_rollback_output_equivalence, pin_varlen_list_model,
+    pin_varlen_equals_padded_realign,
 ]

@@ -77,6 +77,17 @@ MUTANTS = {
     "sample_draft_logits_of_target": ("softmax_row((const char*)draft_logits + ((int64_t)i * k + r) * V * eb",
                                       "softmax_row((const char*)logits + ((int64_t)i * (k + 1) + r) * V * eb"),
     "sample_accepted_tokens_not_drafts": ("r < acc ? draft[(int64_t)i * k + r] :", "r < acc ? (int32_t)x_out :"),
+    # rollback (Family A) and variable-length rollback (Family B)
+    "rollback_ignores_minimum": ("if (n_acc[i] < m) m = n_acc[i];", "m = n_acc[i];"),
+    "rollback_bonus_from_own_count": ("bonus_out[i] = tokens[(int64_t)i * (k + 1) + m];",
+                                      "bonus_out[i] = tokens[(int64_t)i * (k + 1) + n_acc[i]];"),
+    "rollback_keeps_padding": ("pad_out[i] = pad_in[i] + ((Lp - L) - (m + 1));", "pad_out[i] = pad_in[i];"),
+    "varlen_keep_without_bonus": ("const int64_t keep = (int64_t)cu_in[i + 1] - cu_in[i] - (k - n_acc[i]);",
+                                  "const int64_t keep = (int64_t)cu_in[i + 1] - cu_in[i] - (k - n_acc[i]) - 1;"),
+    "varlen_offsets_not_cumulative": ("cu_out[i + 1] = cu_out[i] + (int32_t)keep;", "cu_out[i + 1] = (int32_t)keep;"),
+    "varlen_positions_from_one": ("for (int64_t t = 0; t < keep; ++t) pos[cu_out[i] + t] = t;",
+                                  "for (int64_t t = 0; t < keep; ++t) pos[cu_out[i] + t] = t + 1;"),
+    "varlen_source_at_output_offset": ("T_cap * row + (int64_t)cu_in[i] * row;", "T_cap * row + (int64_t)cu_out[i] * row;"),
 }
 
 # Plausible slips in the scheduler (oracle/exspec.py), caught by the
