@@ -46,7 +46,7 @@
 extern "C" {
 #endif
 
-#define SPECDEC_ABI_VERSION 4
+#define SPECDEC_ABI_VERSION 5
 
 typedef enum {
   SPECDEC_OK = 0,
@@ -425,6 +425,69 @@ specdec_status_t specdec_step_sample(const void* logits, const void* draft_logit
                                      void* workspace, size_t workspace_bytes, uint32_t* dev_status,
                                      int32_t* w_new_host, void* stream);
 
+/* ---- rollback: the other correct strategies of Section 2 -------------------- */
+
+/*
+ * Family A rollback (Section 2, "Family A: contiguous layout"): every row is
+ * truncated to the batch-minimum accepted count m = min_i n_acc_in[i], so
+ * every row appends tokens[i][0 .. m] and m + 1 cache entries; the width and
+ * paddings follow Eq. (1) and Eq. (2) with a_i = m + 1 for every row, so all
+ * offsets are equal (zero when the minimum input padding is 0, Corollary
+ * B.4) and specdec_realign_kv in place moves no cached entry.  Correct, but
+ * the verified tokens beyond m are discarded.
+ *
+ *   tokens      int32 [B][k+1], n_acc_in and pad_in int32 [B]: the outputs and
+ *               inputs of specdec_verify_greedy / specdec_verify_sample.
+ *   n_acc_out   int32 [B] out (all m; may equal n_acc_in), bonus_out int32 [B]
+ *               out (tokens[i][m]), pad_out int32 [B] out (may equal pad_in),
+ *               w_new int32 [1] out.
+ * Rows with pad_in outside [0, W_in - k - 1] or n_acc_in outside [0, k] are
+ * flagged (SPECDEC_DEV_BAD_PAD_IN / _BAD_ACCEPT), left out of m and the width,
+ * and get pad_out = -1.
+ */
+specdec_status_t specdec_rollback(const int32_t* tokens, const int32_t* n_acc_in,
+                                  const int32_t* pad_in, int32_t B, int32_t k, int32_t W_in,
+                                  int32_t* n_acc_out, int32_t* bonus_out, int32_t* pad_out,
+                                  int32_t* w_new, uint32_t* dev_status, void* stream);
+
+/* A flat variable-length bf16 cache [L][2][T_cap][H][D], contiguous: the
+ * rows of all sequences of a (layer, K/V) one after another, one row =
+ * H*D elements (a multiple of 8).  `data` is a device pointer, 16-byte
+ * aligned. */
+typedef struct specdec_varlen {
+  void* data;
+  int32_t L, H, D;
+  int64_t T_cap;
+} specdec_varlen_t;
+
+/*
+ * Family B rollback (Section 2, "Family B: variable-length layout"): I1 does
+ * not arise, but I2 requires the rejected entries to be rolled back.  Sequence
+ * i holds rows [cu_in[i], cu_in[i+1]) of the flat buffer: its cached entries
+ * followed by its k+1 verify window entries.  It keeps its first
+ * cu_in[i+1] - cu_in[i] - (k - n_acc[i]) rows (the entries of the pending
+ * token and the accepted drafts), compacted into dst at cu_out[i] =
+ * the running sum of the kept lengths; pos[r] = the index of row r within its
+ * sequence for r < cu_out[B].  Rows and positions beyond cu_out[B] are left
+ * as they are.
+ *
+ *   src, dst    equal L, H, D; dst->T_cap >= src->T_cap; must not overlap.
+ *   cu_in       int32 [B+1], nondecreasing, cu_in[B] <= src->T_cap.
+ *   n_acc       int32 [B], from verification.
+ *   max_len     host bound on every sequence's length cu_in[i+1] - cu_in[i]
+ *               (sizes the grid), >= k + 1; values above src->T_cap act as
+ *               src->T_cap.
+ *   cu_out      int32 [B+1] out; pos int64 [pos_cap] out (may be NULL),
+ *               pos_cap >= src->T_cap.
+ * A sequence shorter than k + 1 rows or longer than max_len, outside the
+ * buffer, or with n_acc outside [0, k] keeps no row and is flagged
+ * (SPECDEC_DEV_BAD_WIDTH / _BAD_ACCEPT).
+ */
+specdec_status_t specdec_varlen_rollback(const specdec_varlen_t* src, const specdec_varlen_t* dst,
+                                         const int32_t* cu_in, const int32_t* n_acc, int32_t B,
+                                         int32_t k, int32_t max_len, int32_t* cu_out, int64_t* pos,
+                                         int64_t pos_cap, uint32_t* dev_status, void* stream);
+
 /*
  * Kernel timers (for measurement; off by default).  specdec_timing_enable
  * takes a mask of kernels (bit 1 << SPECDEC_KERNEL_*; 0 turns the timers
@@ -433,8 +496,8 @@ specdec_status_t specdec_step_sample(const void* logits, const void* draft_logit
  * specdec_timing_query waits for the recorded events, adds their durations to
  * the totals of `kernel` (0 = verify, 1 = realign, with the fused position ids
  * / mask in specdec_step, 2 = position ids / mask alone, 3 = batch gather,
- * 4 = write-back, 5 = stochastic verification) and returns the totals since
- * the last reset.
+ * 4 = write-back, 5 = stochastic verification, 6 = variable-length rollback)
+ * and returns the totals since the last reset.
  */
 #define SPECDEC_KERNEL_VERIFY 0
 #define SPECDEC_KERNEL_REALIGN 1
@@ -442,7 +505,8 @@ specdec_status_t specdec_step_sample(const void* logits, const void* draft_logit
 #define SPECDEC_KERNEL_GATHER 3
 #define SPECDEC_KERNEL_WRITEBACK 4
 #define SPECDEC_KERNEL_SAMPLE 5
-#define SPECDEC_TIMING_ALL 63
+#define SPECDEC_KERNEL_VARLEN 6
+#define SPECDEC_TIMING_ALL 127
 specdec_status_t specdec_timing_enable(int32_t kernel_mask);
 specdec_status_t specdec_timing_reset(void);
 specdec_status_t specdec_timing_query(int32_t kernel, double* total_ms, int64_t* launches);

@@ -59,7 +59,7 @@ int logit_bytes(int32_t dtype) {
 
 // ---- kernel timers -------------------------------------------------------------
 
-constexpr int kTimedKernels = 6;
+constexpr int kTimedKernels = 7;
 
 struct TimedLaunch {
   int kernel;
@@ -693,6 +693,77 @@ specdec_status_t specdec_scatter_accepted(const specdec_kv_t* batch, const int32
   hipStream_t st = static_cast<hipStream_t>(stream);
   hipError_t e = timed(SPECDEC_KERNEL_WRITEBACK, st, [&] { return specdec::launch_writeback(p, st); });
   if (e != hipSuccess) return hip_fail(e, "write-back launch");
+  return ok();
+}
+
+specdec_status_t specdec_rollback(const int32_t* tokens, const int32_t* n_acc_in, const int32_t* pad_in, int32_t B,
+                                  int32_t k, int32_t W_in, int32_t* n_acc_out, int32_t* bonus_out, int32_t* pad_out,
+                                  int32_t* w_new, uint32_t* dev_status, void* stream) {
+  if (B < 0 || B > SPECDEC_MAX_B) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "B=%d outside [0,%d]", B, SPECDEC_MAX_B);
+  if (k < 0 || k > SPECDEC_MAX_K) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "k=%d outside [0,%d]", k, SPECDEC_MAX_K);
+  if (W_in < k + 1 || W_in > SPECDEC_MAX_WIDTH)
+    return fail(SPECDEC_ERR_INVALID_ARGUMENT, "W_in=%d outside [k+1=%d, %d]", W_in, k + 1, SPECDEC_MAX_WIDTH);
+  if (B == 0) return ok();
+  if (!tokens || !n_acc_in || !pad_in || !n_acc_out || !bonus_out || !pad_out || !w_new)
+    return fail(SPECDEC_ERR_INVALID_ARGUMENT, "NULL tensor pointer");
+  const void* w4[] = {tokens, n_acc_in, pad_in, n_acc_out, bonus_out, pad_out, w_new, dev_status};
+  for (const void* q : w4)
+    if (q && !aligned(q, 4)) return fail(SPECDEC_ERR_UNSUPPORTED, "4-byte tensor not 4-byte aligned");
+  const int64_t b4 = 4 * static_cast<int64_t>(B);
+  if (ranges_overlap(bonus_out, b4, n_acc_in, b4) || ranges_overlap(bonus_out, b4, pad_in, b4) ||
+      ranges_overlap(bonus_out, b4, tokens, b4 * (k + 1)) || ranges_overlap(n_acc_out, b4, tokens, b4 * (k + 1)) ||
+      ranges_overlap(pad_out, b4, tokens, b4 * (k + 1)) || ranges_overlap(n_acc_out, b4, pad_out, b4) ||
+      ranges_overlap(bonus_out, b4, n_acc_out, b4) || ranges_overlap(bonus_out, b4, pad_out, b4) ||
+      (n_acc_out != n_acc_in && ranges_overlap(n_acc_out, b4, n_acc_in, b4)) ||
+      (pad_out != pad_in && ranges_overlap(pad_out, b4, pad_in, b4)) ||
+      ranges_overlap(n_acc_out, b4, pad_in, b4) || ranges_overlap(pad_out, b4, n_acc_in, b4))
+    return fail(SPECDEC_ERR_INVALID_ARGUMENT, "outputs overlap the inputs other than in place");
+  specdec::RollbackLaunch p{tokens, n_acc_in, pad_in, B, k, W_in, n_acc_out, bonus_out, pad_out, w_new, dev_status};
+  hipError_t e = specdec::launch_rollback(p, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "rollback launch");
+  return ok();
+}
+
+specdec_status_t specdec_varlen_rollback(const specdec_varlen_t* src, const specdec_varlen_t* dst,
+                                         const int32_t* cu_in, const int32_t* n_acc, int32_t B, int32_t k,
+                                         int32_t max_len, int32_t* cu_out, int64_t* pos, int64_t pos_cap,
+                                         uint32_t* dev_status, void* stream) {
+  if (!src || !dst) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "NULL descriptor");
+  if (B < 0 || B > SPECDEC_MAX_B) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "B=%d outside [0,%d]", B, SPECDEC_MAX_B);
+  if (k < 0 || k > SPECDEC_MAX_K) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "k=%d outside [0,%d]", k, SPECDEC_MAX_K);
+  if (src->L != dst->L || src->H != dst->H || src->D != dst->D)
+    return fail(SPECDEC_ERR_INVALID_ARGUMENT, "src and dst shapes differ");
+  if (src->L < 0 || src->H < 1 || src->D < 1 || src->D > SPECDEC_MAX_D)
+    return fail(SPECDEC_ERR_INVALID_ARGUMENT, "L, H or D out of range");
+  const int64_t row = static_cast<int64_t>(src->H) * src->D;
+  if (row % 8 != 0) return fail(SPECDEC_ERR_UNSUPPORTED, "H*D=%lld: rows must be whole 16-byte vectors", (long long)row);
+  if (src->T_cap < 0 || src->T_cap > 0x7FFFFFFFLL || dst->T_cap < src->T_cap)
+    return fail(SPECDEC_ERR_INVALID_ARGUMENT, "T_cap out of range or dst->T_cap < src->T_cap");
+  if (max_len < k + 1) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "max_len=%d < k+1", max_len);
+  if (max_len > src->T_cap) max_len = static_cast<int32_t>(src->T_cap);   // no sequence is longer
+  if (B == 0) return ok();
+  if (!cu_in || !n_acc || !cu_out) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "NULL cu_in / n_acc / cu_out");
+  if (!aligned(cu_in, 4) || !aligned(n_acc, 4) || !aligned(cu_out, 4) || (pos && !aligned(pos, 8)) ||
+      (dev_status && !aligned(dev_status, 4)))
+    return fail(SPECDEC_ERR_UNSUPPORTED, "index tensor misaligned");
+  if (pos && pos_cap < src->T_cap) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "pos_cap < src T_cap");
+  const int64_t bytes_src = static_cast<int64_t>(src->L) * 2 * src->T_cap * row * 2;
+  const int64_t bytes_dst = static_cast<int64_t>(dst->L) * 2 * dst->T_cap * row * 2;
+  if (src->L > 0 && src->T_cap > 0) {
+    if (!src->data || !dst->data) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "NULL cache data");
+    if (!aligned(src->data, 16) || !aligned(dst->data, 16)) return fail(SPECDEC_ERR_UNSUPPORTED, "cache not 16-byte aligned");
+    if (ranges_overlap(src->data, bytes_src, dst->data, bytes_dst))
+      return fail(SPECDEC_ERR_INVALID_ARGUMENT, "src and dst caches overlap");
+  }
+  const int64_t c4 = 4 * (static_cast<int64_t>(B) + 1);
+  if (ranges_overlap(cu_out, c4, cu_in, c4) || ranges_overlap(cu_out, c4, n_acc, 4 * static_cast<int64_t>(B)))
+    return fail(SPECDEC_ERR_INVALID_ARGUMENT, "cu_out overlaps cu_in or n_acc");
+  if (static_cast<int64_t>(src->L) * 2 * B > 0xFFFFFFFFLL) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "too many spans");
+  specdec::VarlenLaunch p{src->data, dst->data, src->T_cap, dst->T_cap, src->L, src->H, src->D, cu_in, n_acc,
+                          B, k, max_len, cu_out, pos, dev_status};
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  hipError_t e = timed(SPECDEC_KERNEL_VARLEN, st, [&] { return specdec::launch_varlen_rollback(p, st); });
+  if (e != hipSuccess) return hip_fail(e, "variable-length rollback launch");
   return ok();
 }
 

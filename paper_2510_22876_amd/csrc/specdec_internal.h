@@ -139,6 +139,36 @@ int64_t sample_chunks(int64_t rows, int64_t V);
 int64_t sample_mass_chunk_elems(int64_t V);
 hipError_t launch_verify_sample(const SampleLaunch& p, hipStream_t stream);
 
+// Family A rollback (truncation to the batch-minimum accepted count).
+struct RollbackLaunch {
+  const int32_t* tokens;
+  const int32_t* n_acc_in;
+  const int32_t* pad_in;
+  int32_t B, k, W_in;
+  int32_t* n_acc_out;
+  int32_t* bonus_out;
+  int32_t* pad_out;
+  int32_t* w_new;
+  uint32_t* dev_status;
+};
+
+// Family B rollback (compaction of a flat [L][2][T][H][D] cache).
+struct VarlenLaunch {
+  const void* src;
+  void* dst;
+  int64_t src_T, dst_T;
+  int32_t L, H, D;
+  const int32_t* cu_in;
+  const int32_t* n_acc;
+  int32_t B, k, max_len;
+  int32_t* cu_out;
+  int64_t* pos;              // may be null
+  uint32_t* dev_status;
+};
+
+hipError_t launch_rollback(const RollbackLaunch& p, hipStream_t stream);
+hipError_t launch_varlen_rollback(const VarlenLaunch& p, hipStream_t stream);
+
 hipError_t launch_gather(const GatherLaunch& p, hipStream_t stream);
 hipError_t launch_writeback(const WritebackLaunch& p, hipStream_t stream);
 

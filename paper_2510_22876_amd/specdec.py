@@ -18,7 +18,8 @@ OK, ERR_INVALID_ARGUMENT, ERR_UNSUPPORTED, ERR_HIP, ERR_WORKSPACE = 0, 1, 2, 3, 
 F32, BF16, F16 = 0, 1, 2
 DTYPE_OF = {torch.float32: F32, torch.bfloat16: BF16, torch.float16: F16}
 KERNEL_VERIFY, KERNEL_REALIGN, KERNEL_POSMASK, KERNEL_GATHER, KERNEL_WRITEBACK, KERNEL_SAMPLE = 0, 1, 2, 3, 4, 5
-TIMING_ALL = 63
+KERNEL_VARLEN = 6
+TIMING_ALL = 127
 DEV_BAD_PAD_IN, DEV_BAD_ACCEPT, DEV_BAD_WIDTH, DEV_BAD_PAD_OUT = 1, 2, 4, 8
 DEV_BAD_SLOT, DEV_SLOT_LEN, DEV_BAD_UNIFORM = 0x10, 0x20, 0x40
 WRITEBACK_FULL, WRITEBACK_APPEND = 0, 1
@@ -27,6 +28,7 @@ EXPORTED = (
     "specdec_abi_version", "specdec_last_error", "specdec_workspace_bytes", "specdec_workspace_init",
     "specdec_verify_greedy", "specdec_sample_workspace_bytes", "specdec_verify_sample", "specdec_realign_kv", "specdec_build_posmask", "specdec_realign_tokens",
     "specdec_step", "specdec_step_sample", "specdec_gather_batch", "specdec_scatter_accepted",
+    "specdec_rollback", "specdec_varlen_rollback",
     "specdec_sched_create", "specdec_sched_destroy", "specdec_sched_next_batch", "specdec_sched_commit",
     "specdec_sched_lengths", "specdec_sched_active",
     "specdec_timing_enable", "specdec_timing_reset", "specdec_timing_query",
@@ -43,6 +45,12 @@ class KV(ctypes.Structure):
     """specdec_kv_t: bf16 cache [L][2][B][H][cap][D]."""
     _fields_ = [("data", ctypes.c_void_p), ("L", ctypes.c_int32), ("B", ctypes.c_int32),
                 ("H", ctypes.c_int32), ("D", ctypes.c_int32), ("cap", ctypes.c_int64)]
+
+
+class Varlen(ctypes.Structure):
+    """specdec_varlen_t: flat bf16 cache [L][2][T_cap][H][D]."""
+    _fields_ = [("data", ctypes.c_void_p), ("L", ctypes.c_int32), ("H", ctypes.c_int32), ("D", ctypes.c_int32),
+                ("T_cap", ctypes.c_int64)]
 
 
 class BatchInfo(ctypes.Structure):
@@ -74,6 +82,9 @@ def _load(path: Path = _LIB_PATH) -> ctypes.CDLL:
                                           P, sz, P, P]
     lib.specdec_step_sample.argtypes = [P, P, i32, P, P, P, P, ctypes.c_float, i32, i32, i32, i32, pKV, pKV, P, P, P,
                                         P, P, P, P, i64, P, i64, P, i64, i32, P, sz, P, P, P]
+    lib.specdec_rollback.argtypes = [P, P, P, i32, i32, i32, P, P, P, P, P, P]
+    pVL = ctypes.POINTER(Varlen)
+    lib.specdec_varlen_rollback.argtypes = [pVL, pVL, P, P, i32, i32, i32, P, P, i64, P, P]
     lib.specdec_gather_batch.argtypes = [pKV, P, i64, P, P, i32, i32, i32, pKV, P, i64, i32, P, P, P, i64, P, P]
     lib.specdec_scatter_accepted.argtypes = [pKV, P, P, P, P, i32, i32, i32, pKV, P, i64, P, P, i64, i32, P, P]
     lib.specdec_sched_create.argtypes = [P, i32, i32, i32, i32, i32, i32, ctypes.POINTER(P)]
@@ -90,7 +101,7 @@ def _load(path: Path = _LIB_PATH) -> ctypes.CDLL:
                  "specdec_build_posmask", "specdec_realign_tokens", "specdec_step", "specdec_timing_enable",
                  "specdec_timing_reset", "specdec_timing_query", "specdec_gather_batch",
                  "specdec_scatter_accepted", "specdec_sched_create", "specdec_sched_next_batch", "specdec_verify_sample",
-                 "specdec_step_sample",
+                 "specdec_step_sample", "specdec_rollback", "specdec_varlen_rollback",
                  "specdec_sched_commit", "specdec_sched_lengths"):
         getattr(lib, name).restype = ctypes.c_int
     return lib
@@ -448,6 +459,44 @@ def specdec_step_sample(logits, draft_logits, draft, pad_in, u_accept, u_sample,
         _p(s_out), s_out.shape[1] if s_out is not None else 0, pad_id, _p(workspace), nb, _p(dev_status),
         ctypes.byref(host) if sync_w_new else None, _stream(stream)))
     return host.value if sync_w_new else None
+
+
+def specdec_rollback(tokens, n_acc_in, pad_in, W_in: int, n_acc_out, bonus_out, pad_out, w_new, dev_status=None,
+                     stream=None) -> None:
+    """Family A rollback: every row truncated to the batch-minimum accepted count."""
+    B, kp1 = tokens.shape
+    for name, t, shape in (("tokens", tokens, (B, kp1)), ("n_acc_in", n_acc_in, (B,)), ("pad_in", pad_in, (B,)),
+                           ("n_acc_out", n_acc_out, (B,)), ("bonus_out", bonus_out, (B,)), ("pad_out", pad_out, (B,)),
+                           ("w_new", w_new, (1,))):
+        _req(name, t, shape, torch.int32)
+    _req("dev_status", dev_status, (1,), torch.int32, optional=True)
+    _check(lib.specdec_rollback(_p(tokens), _p(n_acc_in), _p(pad_in), B, kp1 - 1, W_in, _p(n_acc_out), _p(bonus_out),
+                                _p(pad_out), _p(w_new), _p(dev_status), _stream(stream)))
+
+
+def varlen_desc(t: torch.Tensor) -> Varlen:
+    """Descriptor of a contiguous bf16 flat cache [L][2][T_cap][H][D]."""
+    if t.dim() != 5 or t.shape[1] != 2:
+        raise ValueError("flat cache must be [L][2][T_cap][H][D]")
+    if t.dtype != torch.bfloat16 or not t.is_contiguous() or not t.is_cuda:
+        raise ValueError("flat cache must be a contiguous bfloat16 device tensor")
+    L, _, T, H, D = t.shape
+    return Varlen(t.data_ptr(), L, H, D, T)
+
+
+def specdec_varlen_rollback(src, dst, cu_in, n_acc, k: int, max_len: int, cu_out, pos=None, dev_status=None,
+                            stream=None) -> None:
+    """Family B rollback: compaction of a flat cache by cumulative lengths."""
+    s, d = varlen_desc(src), varlen_desc(dst)
+    B = cu_in.numel() - 1
+    _req("cu_in", cu_in, (B + 1,), torch.int32)
+    _req("n_acc", n_acc, (B,), torch.int32)
+    _req("cu_out", cu_out, (B + 1,), torch.int32)
+    _req("pos", pos, (pos.numel() if pos is not None else 0,), torch.int64, optional=True)
+    _req("dev_status", dev_status, (1,), torch.int32, optional=True)
+    _check(lib.specdec_varlen_rollback(ctypes.byref(s), ctypes.byref(d), _p(cu_in), _p(n_acc), B, k, max_len,
+                                       _p(cu_out), _p(pos), pos.numel() if pos is not None else 0, _p(dev_status),
+                                       _stream(stream)))
 
 
 def timing_enable(on=True) -> None:

@@ -284,6 +284,16 @@ class HipBackend:
         self.check_status()
         return dict(tokens=o.tokens, n_acc=o.n_acc, bonus=o.bonus, pad_out=o.pad_out, w_new=o.w_new)
 
+    def rollback(self, tokens, n_acc, pads, W_in):
+        B = int(n_acc.numel())
+        i32 = dict(dtype=torch.int32, device=self.dev)
+        out = dict(n_acc=torch.empty(B, **i32), bonus=torch.empty(B, **i32), pad_out=torch.empty(B, **i32),
+                   w_new=torch.empty(1, **i32))
+        self.sd.specdec_rollback(tokens, n_acc, pads, W_in, out["n_acc"], out["bonus"], out["pad_out"], out["w_new"],
+                                 self.status)
+        self.check_status()
+        return out
+
     def scatter(self, batch, pads, tokens, n_acc, slots, Lb, pool, pool_tok, lens, batch_tok):
         self.sd.specdec_scatter_accepted(batch, pads, tokens, n_acc, slots, Lb, pool, pool_tok, lens,
                                          batch_tok=batch_tok, mode=self.writeback, dev_status=self.status)

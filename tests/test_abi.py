@@ -182,10 +182,10 @@ def test_realign_tokens_rejects(sd):
 
 def test_timing_query_rejects_unknown_kernel(sd):
     assert sd.lib.specdec_timing_query(7, None, None) == 1
-    assert sd.lib.specdec_timing_query(6, None, None) == 1
+    assert sd.lib.specdec_timing_query(7, None, None) == 1
     assert sd.lib.specdec_timing_enable(0) == 0
-    assert sd.lib.specdec_timing_enable(63) == 0
-    assert sd.lib.specdec_timing_enable(64) == 1
+    assert sd.lib.specdec_timing_enable(127) == 0
+    assert sd.lib.specdec_timing_enable(128) == 1
     assert sd.lib.specdec_timing_enable(0) == 0
     assert sd.lib.specdec_timing_enable(-1) == 1
 
@@ -300,3 +300,45 @@ def test_verify_sample_empty_and_workspace(sd):
     # k = 0 needs no draft tensors
     assert sd.sample_workspace_bytes(8, 5, 32000) == 256 + 8 * 16 + (8 * 11 + 8 + 8 * 1) * 16 * 8
     assert sd.sample_workspace_bytes(-1, 0, 5) == 0 and sd.sample_workspace_bytes(1, 65, 5) == 0
+
+
+def test_rollback_rejects(sd):
+    _no_gpu()
+    f = sd.lib.specdec_rollback
+    T, N, PI, NO, BO, PO, W = A, A + 4096, A + 8192, A + 12288, A + 16384, A + 20480, A + 24576
+    assert f(T, N, PI, -1, 3, 10, NO, BO, PO, W, None, None) == 1
+    assert f(T, N, PI, 2, 65, 100, NO, BO, PO, W, None, None) == 1
+    assert f(T, N, PI, 2, 3, 3, NO, BO, PO, W, None, None) == 1          # W_in < k+1
+    assert f(T, None, PI, 2, 3, 10, NO, BO, PO, W, None, None) == 1
+    assert f(T, N, PI, 2, 3, 10, NO, BO + 2, PO, W, None, None) == 2
+    assert f(T, N, PI, 2, 3, 10, NO, N, PO, W, None, None) == 1          # bonus_out over n_acc_in
+    assert f(T, N, PI, 2, 3, 10, N + 4, BO, PO, W, None, None) == 1      # partial overlap, not in place
+    assert f(T, N, PI, 2, 3, 10, NO, BO, T + 8, W, None, None) == 1      # pad_out over tokens
+    assert f(None, None, None, 0, 3, 10, None, None, None, None, None, None) == 0
+
+
+def _vdesc(sd, data=A, L=2, H=2, D=8, T=100):
+    return sd.Varlen(data, L, H, D, T)
+
+
+def test_varlen_rollback_rejects(sd):
+    _no_gpu()
+    f = sd.lib.specdec_varlen_rollback
+    S, Dd = _vdesc(sd), _vdesc(sd, data=A + (1 << 30))
+    CI, NA, CO, PS = A + (2 << 30), A + (3 << 30), A + (4 << 30), A + (5 << 30)
+
+    def call(src=S, dst=Dd, cu_in=CI, n_acc=NA, B=3, k=2, max_len=20, cu_out=CO, pos=PS, pos_cap=100):
+        return f(ctypes.byref(src), ctypes.byref(dst), cu_in, n_acc, B, k, max_len, cu_out, pos, pos_cap, None, None)
+    assert f(None, ctypes.byref(Dd), CI, NA, 3, 2, 20, CO, PS, 100, None, None) == 1
+    assert call(dst=_vdesc(sd, data=A + (1 << 30), H=3)) == 1              # shapes differ
+    assert call(src=_vdesc(sd, D=4, H=1), dst=_vdesc(sd, data=A + (1 << 30), D=4, H=1)) == 2   # H*D not 8k
+    assert call(dst=_vdesc(sd, data=A + (1 << 30), T=99)) == 1             # dst smaller
+    assert call(max_len=2) == 1                                            # < k+1
+    assert call(B=-1) == 1 and call(k=65) == 1
+    assert call(cu_out=None) == 1 and call(cu_in=None) == 1
+    assert call(pos=PS + 4) == 2
+    assert call(pos_cap=99) == 1
+    assert call(dst=_vdesc(sd, data=A + 4096)) == 1                        # caches overlap
+    assert call(cu_out=CI + 4) == 1                                        # cu_out over cu_in
+    assert call(src=_vdesc(sd, data=A + 8), dst=_vdesc(sd, data=A + (1 << 30))) == 2
+    assert call(B=0, cu_in=None, n_acc=None, cu_out=None) == 0
