@@ -16,6 +16,7 @@ the CPU oracle timed on a bounded sample of the same step.
   python bench.py [--steps K] [--warmup W] [--workload NAME] [--variant oop|inplace]
   python bench.py --path exspec [--exspec-batch ragged|same]
   python bench.py --verify sample [--temperature T]
+  python bench.py --path varlen        # Family B rollback of a flat cache
   python bench.py --copy-calibration GIB   # plain device copy, for counter scaling
 
 ``--path exspec`` measures EXSpec's step instead (Algorithm 2 without the
@@ -43,9 +44,11 @@ PEAK_HBM_GBS = 8000.0
 METRIC = "verify+realign steps/s and achieved HBM GB/s (% peak), B=8 7B-shaped KV"
 METRIC_EXSPEC = "EXSpec gather+verify+write-back steps/s and achieved HBM GB/s (% peak), B=8 7B-shaped KV"
 METRIC_SAMPLE = "stochastic verify+realign steps/s and achieved HBM GB/s (% peak), B=8 7B-shaped KV"
+METRIC_VARLEN = "variable-length rollback steps/s and achieved HBM GB/s (% peak), B=8 7B-shaped KV"
 CSRC = ROOT / "paper_2510_22876_amd" / "csrc"
 KERNEL_SRCS = [CSRC / f for f in ("specdec_kernels.hip", "span_copy.h", "posmask.h")]
 GATHER_SRCS = [CSRC / f for f in ("exspec_kernels.hip", "span_copy.h", "posmask.h")]
+VARLEN_SRCS = [CSRC / f for f in ("rollback_kernels.hip", "span_copy.h")]
 
 
 def log(*a):
@@ -305,6 +308,82 @@ def bench_exspec(args, w):
     print(json.dumps(line), flush=True)
 
 
+def bench_varlen(args, w):
+    """Family B rollback on one GPU: the workload's sequences (cached entries
+    from its prompt distribution, plus the k+1 window rows each) in a flat
+    [L][2][T][H][D] cache, greedy verification, then the compaction that rolls
+    back each sequence's rejected window rows into a second buffer, with the
+    new offsets and position ids."""
+    import torch
+    from paper_2510_22876_amd import specdec as sd
+    from paper_2510_22876_amd import workloads as wl
+
+    B, k = w.B, w.k
+    n = wl.prompt_lengths(w, args.seed)
+    lens = n + k + 1
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    T = int(cu[-1])
+    g = torch.Generator(device="cuda")
+    g.manual_seed(args.seed + 12345)
+    src = torch.randn((w.L, 2, T, w.H, w.D), generator=g, device="cuda").to(torch.bfloat16)
+    dst = torch.empty_like(src)
+    logits, draft, *_ = wl.logits_and_drafts(w, args.seed, 0, device="cuda")
+    bufs = sd.StepBuffers(B, k, w.V, 8, "cuda")
+    cu_d = torch.as_tensor(cu, device="cuda")
+    cu_out = torch.empty(B + 1, dtype=torch.int32, device="cuda")
+    pos = torch.empty(T, dtype=torch.int64, device="cuda")
+    zeros = torch.zeros(B, dtype=torch.int32, device="cuda")
+    max_len = int(lens.max())
+    desc = (f"{w.name} as a flat cache: B={B} sequences, cached lengths {w.prompt} + k+1={k + 1} window rows, "
+            f"T={T}; k={k} V={w.V} {w.logit_dtype} logits; KV L={w.L} H={w.H} D={w.D} bf16; out-of-place compaction")
+    log(f"[bench] varlen: {desc}")
+
+    def step():
+        sd.specdec_verify_greedy(logits, draft, zeros, k + 1, bufs.tokens, bufs.n_acc, bufs.bonus, bufs.pad_out,
+                                 bufs.w_new, bufs.workspace, bufs.dev_status)
+        sd.specdec_varlen_rollback(src, dst, cu_d, bufs.n_acc, k, max_len, cu_out, pos, bufs.dev_status)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    if int(bufs.dev_status.cpu()[0]) != 0:
+        raise RuntimeError("device flagged invalid values")
+    n_acc = bufs.n_acc.cpu().numpy()
+    K = args.steps
+    sd.timing_reset()
+    sd.timing_enable(1 << sd.KERNEL_VARLEN)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(K):
+        step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    sd.timing_enable(False)
+    v_ms, v_n = sd.timing_query(sd.KERNEL_VARLEN)
+    assert v_n == K
+    E = w.L * 2 * w.H * w.D * 2
+    keep = lens - (k - n_acc)
+    algo = 2 * int(keep.sum()) * E + 4 * (2 * B + 1) + 4 * B + 8 * int(keep.sum())
+    vms = v_ms / K
+    achieved = algo / (vms * 1e-3) / 1e9
+    ms_per_step = elapsed / K * 1e3
+    traffic, traffic_src = read_traffic_summary(w.name, "oop", kernel="varlen", srcs=VARLEN_SRCS)
+    log(f"[bench] varlen n_acc={n_acc.tolist()} compaction {vms:.4f} ms ({algo / 1e9:.3f} GB, {achieved:.0f} GB/s), "
+        f"step {ms_per_step:.4f} ms; traffic: {traffic_src}")
+    line = {
+        "metric": METRIC_VARLEN, "value": K / elapsed, "unit": "steps/s", "n_gpus": 1, "steps": K,
+        "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": desc, "B": B, "k": k, "V": w.V, "L": w.L, "H": w.H, "D": w.D, "T": T,
+                   "seed": args.seed, "compaction_ms": round(vms, 5)},
+        "roofline": {"bound": "hbm", "kernel": "varlen offsets + compaction (+ positions)", "achieved": round(achieved, 1),
+                     "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4),
+                     "traffic": traffic, "algorithmic_bytes": algo},
+        "cpu_baseline": None,
+    }
+    print(json.dumps(line), flush=True)
+
+
 def copy_calibration(gib: float):
     import torch
     n = int(gib * (1 << 30))
@@ -343,7 +422,7 @@ def main():
     ap.add_argument("--verify", choices=["greedy", "sample"], default="greedy",
                     help="greedy verification (default) or stochastic verification by speculative sampling")
     ap.add_argument("--temperature", type=float, default=1.0, help="--verify sample: the sampling temperature")
-    ap.add_argument("--path", choices=["eqspec", "exspec"], default="eqspec",
+    ap.add_argument("--path", choices=["eqspec", "exspec", "varlen"], default="eqspec",
                     help="eqspec: the verify + realign step (default); exspec: gather + verify + write-back")
     ap.add_argument("--exspec-batch", choices=["ragged", "same"], default="ragged",
                     help="exspec: a batch of prompt-distributed lengths (unpad-repad) or one length (concatenation)")
@@ -371,6 +450,9 @@ def main():
     w = wl.WORKLOADS[args.workload]
     if args.path == "exspec":
         bench_exspec(args, w)
+        return
+    if args.path == "varlen":
+        bench_varlen(args, w)
         return
     variant = args.variant
     n, W_in, pad_in, cap = wl.initial_geometry(w, args.seed)
