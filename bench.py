@@ -17,6 +17,7 @@ the CPU oracle timed on a bounded sample of the same step.
   python bench.py --path exspec [--exspec-batch ragged|same]
   python bench.py --verify sample [--temperature T]
   python bench.py --path varlen        # Family B rollback of a flat cache
+  python bench.py --path chained       # 16 chained in-place steps (per-step times)
   python bench.py --copy-calibration GIB   # plain device copy, for counter scaling
 
 ``--path exspec`` measures EXSpec's step instead (Algorithm 2 without the
@@ -107,6 +108,46 @@ def read_traffic_summary(workload: str, variant: str, kernel: str = "realign", s
     return float(m_bytes.group(1)), path.name
 
 
+def cpu_model() -> str:
+    try:
+        for ln in Path("/proc/cpuinfo").read_text().splitlines():
+            if ln.startswith("model name"):
+                return ln.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def copy_ceiling(nbytes: int, reps: int = 5) -> float:
+    """GB/s (bytes read + written) of the runtime's device-to-device memcpy
+    (``Tensor.copy_`` of contiguous bytes, which HIP serves with its blit
+    kernel) of ``nbytes`` each way on this GPU: the data-movement rate a
+    caller gets without a hand-written kernel."""
+    import torch
+    n = max(1 << 20, int(nbytes))
+    a = torch.empty(n, dtype=torch.uint8, device="cuda")
+    b = torch.empty(n, dtype=torch.uint8, device="cuda")
+    a.fill_(1)
+    b.copy_(a)
+    torch.cuda.synchronize()
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s.record()
+    for _ in range(reps):
+        b.copy_(a)
+    e.record()
+    torch.cuda.synchronize()
+    ms = s.elapsed_time(e) / reps
+    del a, b
+    torch.cuda.empty_cache()
+    return 2 * n / (ms * 1e-3) / 1e9
+
+
+def percentiles(ms):
+    a = np.sort(np.asarray(ms, dtype=np.float64))
+    return {"step_ms_p10": round(float(np.percentile(a, 10)), 5), "step_ms_p50": round(float(np.percentile(a, 50)), 5),
+            "step_ms_p90": round(float(np.percentile(a, 90)), 5)}
+
+
 def cpu_baseline(w, logits, draft, pad_in, W_in, src, budget_s: float, s_rows=None):
     """The oracle as it stands, single-threaded on the host, on a bounded
     sample: verification over every logit row, the KV realignment of whole
@@ -138,7 +179,7 @@ def cpu_baseline(w, logits, draft, pad_in, W_in, src, budget_s: float, s_rows=No
         runs += 1
     per_layer = t_real / runs
     est = t_verify + per_layer * w.L + t_pm
-    return dict(value=1.0 / est, unit="steps/s", cores=1, kind="oracle",
+    return dict(value=1.0 / est, unit="steps/s", cores=1, kind="oracle", cpu_model=cpu_model(),
                 sample=(f"oracle verify over all {w.B * (w.k + 1)} logit rows ({t_verify * 1e3:.1f} ms), "
                         f"KV realign of {runs} one-layer slabs cycling over layers 0..{nl - 1} "
                         f"({per_layer * 1e3:.1f} ms per layer, x{w.L} layers), pos/mask and token row ({t_pm * 1e3:.2f} ms); "
@@ -189,7 +230,7 @@ def cpu_baseline_exspec(w, pool, pool_tok, lens, slots, Lb, logits, draft, budge
         runs += 1
     per_layer = t_layers / runs
     est = t_verify + per_layer * w.L
-    return dict(value=1.0 / est, unit="steps/s", cores=1, kind="oracle",
+    return dict(value=1.0 / est, unit="steps/s", cores=1, kind="oracle", cpu_model=cpu_model(),
                 sample=(f"oracle verify over all {w.B * (k + 1)} logit rows ({t_verify * 1e3:.1f} ms), gather + "
                         f"whole-row write-back of {runs} one-layer pool slabs ({per_layer * 1e3:.1f} ms per layer, "
                         f"x{w.L} layers); single-threaded, scaled to one whole step ({est:.2f} s)"))
@@ -384,6 +425,112 @@ def bench_varlen(args, w):
     print(json.dumps(line), flush=True)
 
 
+def bench_chained(args, w):
+    """Chained in-place steps (the cache grows by the accepted entries each
+    step): every step verifies fresh logits, realigns the cache and token row
+    in place and writes the next verify window's entries (outside the timed
+    intervals). K timed steps run through the chain of ``w.steps`` steps,
+    restarting from the pristine input after the last; per-chain-step times
+    and bandwidths are reported."""
+    import torch
+    from paper_2510_22876_amd import specdec as sd
+    from paper_2510_22876_amd import workloads as wl
+    k, B, T = w.k, w.B, w.steps
+    n, W_in0, pad_in0, cap = wl.initial_geometry(w, args.seed)
+    desc = describe(w, "inplace") + f"; {T} chained steps, cap={cap}"
+    log(f"[bench] chained workload {desc}")
+    kv = wl.make_kv(w, pad_in0, W_in0, cap, args.seed, device="cuda")
+    pristine = kv.clone()
+    s_rows = wl.make_token_rows(w, pad_in0, W_in0, cap + 2, args.seed, -1, device="cuda")
+    pristine_s = s_rows.clone()
+    inputs = [wl.logits_and_drafts(w, args.seed, t, device="cuda")[:2] for t in range(T)]
+    bufs = sd.StepBuffers(B, k, w.V, cap + k + 1)
+    st = dict(t=0, W0=W_in0 - (k + 1), pad=pad_in0.copy())
+    pad_t = torch.as_tensor(pad_in0, device="cuda")
+
+    def restart():
+        kv.copy_(pristine)
+        s_rows.copy_(pristine_s)
+        pad_t.copy_(torch.as_tensor(pad_in0, device="cuda"))
+        st.update(t=0, W0=W_in0 - (k + 1), pad=pad_in0.copy())
+
+    def one(record=None):
+        """One chained step; returns (chain position, bytes dict, realign ms)."""
+        t = st["t"]
+        if t == T:
+            restart()
+            t = 0
+        if t > 0:
+            wl.write_window(kv, w, st["W0"], st["pad"], seed=args.seed, step=t)
+        Wi = st["W0"] + k + 1
+        logits, draft = inputs[t]
+        torch.cuda.synchronize()
+        if record:
+            record[0].record()
+        sd.specdec_step(logits, draft, pad_t, Wi, kv, kv, bufs.tokens, bufs.n_acc, bufs.bonus, bufs.pad_out,
+                        bufs.w_new, bufs.pos, bufs.mask, bufs.workspace, bufs.dev_status, s_in=s_rows,
+                        s_out=s_rows, pad_id=-1)
+        if record:
+            record[1].record()
+        torch.cuda.synchronize()
+        n_acc = bufs.n_acc.cpu().numpy()
+        w_new = int(bufs.w_new.cpu()[0])
+        by = step_bytes(w, st["pad"], Wi, n_acc, w_new, "inplace", True)
+        st.update(t=t + 1, W0=w_new, pad=bufs.pad_out.cpu().numpy().copy())
+        pad_t.copy_(bufs.pad_out)
+        return t, by
+
+    for _ in range(args.warmup):
+        one()
+    if int(bufs.dev_status.cpu()[0]) != 0:
+        raise RuntimeError("device flagged invalid values")
+    restart()
+    K = args.steps
+    per = {t: [] for t in range(T)}
+    realign = {t: [] for t in range(T)}
+    bytes_at = {}
+    elapsed = 0.0
+    for _ in range(K):
+        ev = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+        sd.timing_reset()
+        sd.timing_enable(1 << sd.KERNEL_REALIGN)
+        t, by = one(ev)
+        sd.timing_enable(False)
+        ms = ev[0].elapsed_time(ev[1])
+        rms, rn = sd.timing_query(sd.KERNEL_REALIGN)
+        assert rn == 1
+        per[t].append(ms)
+        realign[t].append(rms)
+        bytes_at[t] = by
+        elapsed += ms / 1e3
+    done = [t for t in range(T) if per[t]]
+    rbytes = sum((bytes_at[t]["realign"] + bytes_at[t]["posmask"]) * len(per[t]) for t in done)
+    rms_total = sum(sum(realign[t]) for t in done)
+    achieved = rbytes / (rms_total * 1e-3) / 1e9
+    per_step = [{"step": t, "ms": round(float(np.mean(per[t])), 5), "realign_ms": round(float(np.mean(realign[t])), 5),
+                 "realign_GBps": round((bytes_at[t]["realign"] + bytes_at[t]["posmask"]) /
+                                       (np.mean(realign[t]) * 1e-3) / 1e9, 1)} for t in done]
+    ms_all = [m for t in done for m in per[t]]
+    log(f"[bench] chained: {K} steps, mean {elapsed / K * 1e3:.4f} ms, realign {achieved:.0f} GB/s")
+    copy_gbs = copy_ceiling(rbytes // (2 * K)) if args.copy_ceiling else None
+    line = {
+        "metric": METRIC, "value": K / elapsed, "unit": "steps/s", "n_gpus": 1, "steps": K,
+        "warmup": args.warmup, "ms_per_step": elapsed / K * 1e3, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": desc, "B": B, "k": k, "V": w.V, "L": w.L, "H": w.H, "D": w.D, "chain": T,
+                   "variant": "inplace", "seed": args.seed, "token_row": True, **percentiles(ms_all),
+                   "per_step": per_step},
+        "roofline": {"bound": "hbm", "kernel": "realign_inplace (+ fused pos/mask, token row)",
+                     "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None,
+                     "algorithmic_bytes": int(rbytes // K),
+                     **({"memcpy_d2d_GBps": round(copy_gbs, 1), "vs_memcpy_d2d": round(achieved / copy_gbs, 4)}
+                        if copy_gbs else {})},
+        "cpu_baseline": None,
+    }
+    print(json.dumps(line), flush=True)
+
+
 def copy_calibration(gib: float):
     import torch
     n = int(gib * (1 << 30))
@@ -422,10 +569,13 @@ def main():
     ap.add_argument("--verify", choices=["greedy", "sample"], default="greedy",
                     help="greedy verification (default) or stochastic verification by speculative sampling")
     ap.add_argument("--temperature", type=float, default=1.0, help="--verify sample: the sampling temperature")
-    ap.add_argument("--path", choices=["eqspec", "exspec", "varlen"], default="eqspec",
-                    help="eqspec: the verify + realign step (default); exspec: gather + verify + write-back")
+    ap.add_argument("--path", choices=["eqspec", "exspec", "varlen", "chained"], default="eqspec",
+                    help="eqspec: the verify + realign step (default); exspec: gather + verify + write-back; "
+                         "varlen: Family B rollback; chained: in-place steps along a chain (per-step times)")
     ap.add_argument("--exspec-batch", choices=["ragged", "same"], default="ragged",
                     help="exspec: a batch of prompt-distributed lengths (unpad-repad) or one length (concatenation)")
+    ap.add_argument("--copy-ceiling", type=int, choices=[0, 1], default=1,
+                    help="also time the runtime's device-to-device memcpy of the realign's bytes, for comparison")
     ap.add_argument("--copy-calibration", type=float, default=0.0,
                     help="run a plain device copy of this many GiB each way and exit")
     args = ap.parse_args()
@@ -453,6 +603,9 @@ def main():
         return
     if args.path == "varlen":
         bench_varlen(args, w)
+        return
+    if args.path == "chained":
+        bench_chained(args, w if w.steps > 1 else wl.WORKLOADS["vicuna7b_chained"])
         return
     variant = args.variant
     n, W_in, pad_in, cap = wl.initial_geometry(w, args.seed)
@@ -512,6 +665,7 @@ def main():
     sd.timing_reset()
     # only the dominant kernel is bracketed inside the timed region
     sd.timing_enable(1 << sd.KERNEL_REALIGN if timers else 0)
+    step_ms = []
     if pristine is None:
         torch.cuda.synchronize()
         t0 = time.perf_counter()
@@ -530,7 +684,8 @@ def main():
             step()
             e.record()
             torch.cuda.synchronize()
-            elapsed += s.elapsed_time(e) / 1e3
+            step_ms.append(s.elapsed_time(e))
+            elapsed += step_ms[-1] / 1e3
     sd.timing_enable(False)
     realign_ms, realign_n = sd.timing_query(sd.KERNEL_REALIGN)
     # a second pass of K steps after the timed region: the verify kernels'
@@ -545,6 +700,16 @@ def main():
     torch.cuda.synchronize()
     sd.timing_enable(False)
     verify_ms, verify_n = sd.timing_query(vkern)
+    if pristine is None:
+        # the per-step distribution: events around each step of a third,
+        # back-to-back pass
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K)]
+        for s_ev, e_ev in evs:
+            s_ev.record()
+            step()
+            e_ev.record()
+        torch.cuda.synchronize()
+        step_ms = [s_ev.elapsed_time(e_ev) for s_ev, e_ev in evs]
     if not timers:
         realign_ms, realign_n = sd.timing_query(sd.KERNEL_REALIGN)
     assert realign_n == K and verify_n == K
@@ -560,6 +725,7 @@ def main():
     ms_per_step = elapsed / K * 1e3
     step_gbs = (realign_bytes + by["verify"]) / (ms_per_step * 1e-3) / 1e9
     traffic, traffic_src = read_traffic_summary(w.name, variant)
+    copy_gbs = copy_ceiling(realign_bytes // 2) if args.copy_ceiling else None
     log(f"[bench] n_acc={n_acc.tolist()} w_new={w_new} realign {realign_avg_ms:.4f} ms "
         f"({realign_bytes / 1e9:.3f} GB, {achieved:.0f} GB/s), verify {verify_avg_ms:.4f} ms "
         f"({by['verify'] / 1e6:.2f} MB), step {ms_per_step:.4f} ms ({step_gbs:.0f} GB/s); traffic: {traffic_src}")
@@ -598,6 +764,7 @@ def main():
             "step_bytes": realign_bytes + by["verify"],
             "verify_ms": round(verify_avg_ms, 5),
             "realign_ms": round(realign_avg_ms, 5),
+            **percentiles(step_ms),
         },
         "roofline": {
             "bound": "hbm",
@@ -608,6 +775,7 @@ def main():
             "frac": round(achieved / PEAK_HBM_GBS, 4),
             "traffic": traffic,
             "algorithmic_bytes": realign_bytes,
+            **({"memcpy_d2d_GBps": round(copy_gbs, 1), "vs_memcpy_d2d": round(achieved / copy_gbs, 4)} if copy_gbs else {}),
         },
         "cpu_baseline": cpu,
     }

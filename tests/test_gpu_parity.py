@@ -104,6 +104,31 @@ def test_edge_cases(name, variant):
         _full_check(run_gpu(EDGE[name], seed=seed, variant=variant))
 
 
+@pytest.mark.parametrize("variant", ["oop", "inplace"])
+def test_draft_cache_realigned_with_the_target_offsets(variant):
+    """Alg. 1 realigns every cache with one set of offsets: a draft model's
+    cache of its own (L, H, D) shape, realigned by a second call with the
+    target step's pad_in / n_acc / w_new, against the oracle element by
+    element."""
+    from paper_2510_22876_amd import specdec as sd
+    w = SMALL["vicuna7b_small"]
+    r = run_gpu(w, seed=5, variant="oop")
+    v = check_verify_vs_oracle(r)
+    wd = w.scaled(L=3, H=1, D=64)
+    src = wl.make_kv(wd, r.pad_in, r.W_in, r.cap, 7, device="cuda")
+    before = bits(src)
+    dst = src if variant == "inplace" else torch.full_like(src.view(torch.int16), SENT_KV).view(torch.bfloat16)
+    dev = lambda a: torch.as_tensor(np.asarray(a, np.int32), device="cuda")
+    status = torch.zeros(1, dtype=torch.int32, device="cuda")
+    sd.specdec_realign_kv(src, dst, w.k, r.W_in, dev(r.pad_in), dev(r.out["n_acc"]), dev([r.out["w_new"]]), status)
+    torch.cuda.synchronize()
+    assert int(status.cpu()[0]) == 0
+    W = v["w_new"]
+    exp = oracle.realign_kv(before, w.k, r.W_in, r.pad_in, v["n_acc"], W)
+    got = bits(dst)
+    assert np.array_equal(got[..., :W, :], exp[..., :W, :])
+
+
 def test_uniform_acceptance_in_place_touches_nothing():
     """Corollary B.4: every offset is zero, so the in-place step writes no KV byte."""
     w = EDGE["uniform_accept"].scaled(extra_cap=9)
