@@ -305,6 +305,7 @@ struct RealignArgs {
   uint32_t misaligned;                   // out of place: spans tiled from the group boundary below them
   uint32_t realign_blocks;               // realign workgroups in this launch
   uint32_t span_base;                    // first span of this launch
+  uint32_t nspans;                       // L * 2 * B * H
   // workgroups before the realign ones: position ids / mask, then the token row
   uint32_t extra_blocks;
   uint32_t pm_blocks;
@@ -524,12 +525,23 @@ __global__ __launch_bounds__(kTpb) void realign_inplace_kernel(RealignArgs a) {
     extra_block<kTpb>(a, blockIdx.x);
     return;
   }
-  const uint32_t span = a.span_base + (blockIdx.x - a.extra_blocks);
-  const int row = static_cast<int>((span / static_cast<uint32_t>(a.H)) % static_cast<uint32_t>(a.B));
+  // Workgroups are dispatched round-robin over the 8 XCDs, and only the rows
+  // whose padding changes do any work.  In the cache's own order a row's H
+  // spans sit on H consecutive workgroups: with H = 4 and every other row
+  // moving, all the work would land on half the XCDs.  So workgroups take
+  // the spans in groups of 8 consecutive spans (memory locality as in the
+  // cache's order), with the group's spans rotated over the XCDs by the
+  // group index: any periodic pattern of moving rows spreads over all XCDs.
+  const uint32_t rel = a.span_base + (blockIdx.x - a.extra_blocks);
+  const uint32_t grp = rel >> 3;
+  const uint32_t span =
+      static_cast<uint64_t>(grp) * 8u + 8u <= a.nspans ? (grp << 3) + ((rel + grp) & 7u) : rel;
+  const uint32_t row_u = (span / static_cast<uint32_t>(a.H)) % static_cast<uint32_t>(a.B);
+  const int row = static_cast<int>(row_u);
   RowGeom g;
   const uint32_t err = row_geometry(a, row, g);
   if (err) {
-    if (span == static_cast<uint32_t>(row) * a.H && threadIdx.x == 0 && a.dev_status) atomicOr(a.dev_status, err);
+    if (span == row_u * static_cast<uint32_t>(a.H) && threadIdx.x == 0 && a.dev_status) atomicOr(a.dev_status, err);
     return;
   }
   const int32_t s = g.pad_out - g.pad_in;
@@ -680,6 +692,7 @@ hipError_t launch_realign(const RealignLaunch& p, hipStream_t stream) {
   a.w_new = p.w_new;
   a.dev_status = p.dev_status;
   const int64_t nspans = static_cast<int64_t>(p.L) * 2 * p.B * p.H;
+  a.nspans = static_cast<uint32_t>(nspans);
   a.pos = p.pos;
   a.mask = p.mask;
   a.pad_out = p.pad_out;
