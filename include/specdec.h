@@ -128,6 +128,9 @@ specdec_status_t specdec_workspace_init(void* workspace, size_t workspace_bytes,
  *             8-byte aligned.
  * B = 0 is a no-op.  Limits: 1 <= V < 2^31, 0 <= k <= SPECDEC_MAX_K,
  * B <= SPECDEC_MAX_B, B*(k+1) <= SPECDEC_MAX_ROWS, k+1 <= W_in <= SPECDEC_MAX_WIDTH.
+ * The outputs and the workspace must not overlap each other or the inputs
+ * (a decode loop keeps pad_in and pad_out in separate buffers and swaps
+ * them); an overlap is SPECDEC_ERR_INVALID_ARGUMENT.
  */
 specdec_status_t specdec_verify_greedy(const void* logits, int32_t dtype, const int32_t* draft,
                                        const int32_t* pad_in, int32_t B, int32_t k, int32_t V,
@@ -169,7 +172,8 @@ specdec_status_t specdec_verify_greedy(const void* logits, int32_t dtype, const 
  * in a fixed parallel order): a decision whose fp64 margin is within the
  * fp32 rounding of these sums may differ from an fp64 evaluation.
  * Limits as specdec_verify_greedy, with B*(2k+1) <= SPECDEC_MAX_ROWS and
- * V <= SPECDEC_MAX_SAMPLE_V.
+ * V <= SPECDEC_MAX_SAMPLE_V; outputs and workspace must not overlap each
+ * other or the inputs, as there.
  */
 size_t specdec_sample_workspace_bytes(int32_t B, int32_t k, int32_t V);
 
@@ -217,6 +221,8 @@ specdec_status_t specdec_realign_kv(const specdec_kv_t* src, const specdec_kv_t*
  *   pos       int64 [B][pm_cap] out, 8-byte aligned; mask uint8 [B][pm_cap] out.
  *   pm_cap    row stride of pos and mask; must be >= w_new + k + 1 (checked on
  *             the device; rows that do not fit are skipped and flagged).
+ * pos and mask must not overlap each other, pad_out or w_new (nor, in
+ * specdec_step, pad_in or n_acc).
  */
 specdec_status_t specdec_build_posmask(const int32_t* pad_out, const int32_t* w_new, int32_t B,
                                        int32_t k, int64_t* pos, uint8_t* mask, int64_t pm_cap,

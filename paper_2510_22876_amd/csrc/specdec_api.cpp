@@ -7,6 +7,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <initializer_list>
 #include <mutex>
 #include <string>
 #include <vector>
@@ -103,22 +104,49 @@ hipError_t timed(int kernel, hipStream_t stream, F&& launch) {
       e = take_event(t);
     }
   }
-  if (b && e) {
-    hipError_t r = hipEventRecord(b, stream);
-    if (r != hipSuccess) return r;
-  }
-  hipError_t r = launch();
-  if (r != hipSuccess) return r;
-  if (b && e) {
-    r = hipEventRecord(e, stream);
-    if (r != hipSuccess) return r;
+  // events that end up unused go back to the pool
+  auto give_back = [&] {
     std::lock_guard<std::mutex> lk(t.mu);
-    t.pending.push_back({kernel, b, e});
+    if (b) t.pool.push_back(b);
+    if (e) t.pool.push_back(e);
+  };
+  const bool timing = b && e;
+  hipError_t r = timing ? hipEventRecord(b, stream) : hipSuccess;
+  if (r == hipSuccess) r = launch();
+  if (r == hipSuccess && timing) r = hipEventRecord(e, stream);
+  if (r != hipSuccess || !timing) {
+    give_back();
+    return r;
   }
+  std::lock_guard<std::mutex> lk(t.mu);
+  t.pending.push_back({kernel, b, e});
   return hipSuccess;
 }
 
 // ---- validation -------------------------------------------------------------------
+
+struct Region {
+  const void* p;
+  int64_t bytes;
+  const char* name;
+};
+
+// Every output region must be disjoint from every input region and from the
+// other outputs (NULL or empty regions are skipped).
+specdec_status_t check_disjoint(std::initializer_list<Region> inputs, std::initializer_list<Region> outputs) {
+  auto meet = [](const Region& a, const Region& b) {
+    if (!a.p || !b.p || a.bytes <= 0 || b.bytes <= 0) return false;
+    const uintptr_t a0 = reinterpret_cast<uintptr_t>(a.p), b0 = reinterpret_cast<uintptr_t>(b.p);
+    return a0 < b0 + static_cast<uintptr_t>(b.bytes) && b0 < a0 + static_cast<uintptr_t>(a.bytes);
+  };
+  for (auto o = outputs.begin(); o != outputs.end(); ++o) {
+    for (const Region& i : inputs)
+      if (meet(*o, i)) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "output %s overlaps input %s", o->name, i.name);
+    for (auto o2 = outputs.begin(); o2 != o; ++o2)
+      if (meet(*o, *o2)) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "outputs %s and %s overlap", o2->name, o->name);
+  }
+  return SPECDEC_OK;
+}
 
 specdec_status_t check_verify_args(const void* logits, int32_t dtype, const int32_t* draft,
                                    const int32_t* pad_in, int32_t B, int32_t k, int32_t V, int32_t W_in,
@@ -141,6 +169,14 @@ specdec_status_t check_verify_args(const void* logits, int32_t dtype, const int3
   const void* i32s[] = {draft, pad_in, tokens, n_acc, bonus, pad_out, w_new};
   for (const void* p : i32s)
     if (p && !aligned(p, 4)) return fail(SPECDEC_ERR_UNSUPPORTED, "int32 tensor not 4-byte aligned");
+  {
+    const int64_t b4 = 4 * static_cast<int64_t>(B);
+    specdec_status_t d = check_disjoint(
+        {{logits, rows * V * eb, "logits"}, {draft, b4 * k, "draft"}, {pad_in, b4, "pad_in"}},
+        {{tokens, b4 * (k + 1), "tokens"}, {n_acc, b4, "n_acc"}, {bonus, b4, "bonus"}, {pad_out, b4, "pad_out"},
+         {w_new, 4, "w_new"}, {workspace, static_cast<int64_t>(workspace_bytes), "workspace"}});
+    if (d) return d;
+  }
   const int64_t chunk = specdec::verify_chunk_elems(rows, V);
   const int64_t blocks = rows * ((V + chunk - 1) / chunk);
   if (blocks * specdec::kThreads > 0xFFFFFFFFLL) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "logits too large for one launch");
@@ -232,7 +268,9 @@ specdec_status_t check_posmask_args(const int32_t* pad_out, const int32_t* w_new
   if (!pad_out || !w_new || !pos || !mask) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "NULL pad_out / w_new / pos / mask");
   if (!aligned(pos, 8)) return fail(SPECDEC_ERR_UNSUPPORTED, "pos not 8-byte aligned");
   if (!aligned(pad_out, 4) || !aligned(w_new, 4)) return fail(SPECDEC_ERR_UNSUPPORTED, "int32 tensor not 4-byte aligned");
-  return SPECDEC_OK;
+  const int64_t n = static_cast<int64_t>(B) * pm_cap;
+  return check_disjoint({{pad_out, 4 * static_cast<int64_t>(B), "pad_out"}, {w_new, 4, "w_new"}},
+                        {{pos, 8 * n, "pos"}, {mask, n, "mask"}});
 }
 
 
@@ -267,6 +305,16 @@ specdec_status_t check_sample_args(const void* logits, const void* draft_logits,
   const void* w4[] = {draft, pad_in, u_accept, u_sample, tokens, n_acc, bonus, pad_out, w_new, dev_status};
   for (const void* q : w4)
     if (q && !aligned(q, 4)) return fail(SPECDEC_ERR_UNSUPPORTED, "4-byte tensor not 4-byte aligned");
+  {
+    const int64_t b4 = 4 * static_cast<int64_t>(B);
+    const int64_t lb = static_cast<int64_t>(B) * V * eb;
+    specdec_status_t d = check_disjoint(
+        {{logits, lb * (k + 1), "logits"}, {draft_logits, lb * k, "draft_logits"}, {draft, b4 * k, "draft"},
+         {pad_in, b4, "pad_in"}, {u_accept, b4 * k, "u_accept"}, {u_sample, b4, "u_sample"}},
+        {{tokens, b4 * (k + 1), "tokens"}, {n_acc, b4, "n_acc"}, {bonus, b4, "bonus"}, {pad_out, b4, "pad_out"},
+         {w_new, 4, "w_new"}, {workspace, static_cast<int64_t>(workspace_bytes), "workspace"}});
+    if (d) return d;
+  }
   const int64_t blocks = rows * specdec::sample_chunks(rows, V);
   if (blocks * 256 > 0xFFFFFFFFLL) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "logits too large for one launch");
   const size_t need = specdec_sample_workspace_bytes(B, k, V);
@@ -287,6 +335,9 @@ specdec_status_t check_step_rest(int32_t B, int32_t k, int32_t W_in, const specd
   if (s) return s;
   if (src->B != B) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "cache rows B=%d differ from logits rows B=%d", src->B, B);
   s = check_posmask_args(pad_out, w_new, B, k, pos, mask, pm_cap);
+  if (s) return s;
+  s = check_disjoint({{pad_in, 4 * static_cast<int64_t>(B), "pad_in"}, {n_acc, 4 * static_cast<int64_t>(B), "n_acc"}},
+                     {{pos, 8 * static_cast<int64_t>(B) * pm_cap, "pos"}, {mask, static_cast<int64_t>(B) * pm_cap, "mask"}});
   if (s) return s;
   if (B > 0 && pm_cap < static_cast<int64_t>(W_in) + k + 1)
     return fail(SPECDEC_ERR_INVALID_ARGUMENT, "pm_cap=%lld < W_in+k+1=%d", (long long)pm_cap, W_in + k + 1);
@@ -796,12 +847,17 @@ specdec_status_t specdec_timing_query(int32_t kernel, double* total_ms, int64_t*
   if (kernel < 0 || kernel >= kTimedKernels) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "unknown kernel id %d", kernel);
   Timers& t = timers();
   std::lock_guard<std::mutex> lk(t.mu);
-  for (const TimedLaunch& p : t.pending) {
+  size_t done = 0;
+  for (; done < t.pending.size(); ++done) {
+    const TimedLaunch& p = t.pending[done];
     hipError_t e = hipEventSynchronize(p.end);
-    if (e != hipSuccess) return hip_fail(e, "timer event synchronize");
     float ms = 0.f;
-    e = hipEventElapsedTime(&ms, p.begin, p.end);
-    if (e != hipSuccess) return hip_fail(e, "timer elapsed time");
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, p.begin, p.end);
+    if (e != hipSuccess) {
+      // launches already added are dropped from the queue; the failing one stays
+      t.pending.erase(t.pending.begin(), t.pending.begin() + static_cast<std::ptrdiff_t>(done));
+      return hip_fail(e, "timer event");
+    }
     t.total_ms[p.kernel] += ms;
     t.launches[p.kernel] += 1;
     t.pool.push_back(p.begin);

@@ -63,9 +63,18 @@ A = 0x10000
 P = ctypes.c_void_p
 
 
+def _a(i):
+    """Distinct dummy addresses, 16 MiB apart (buffers must not overlap)."""
+    return A + ((i + 1) << 24)
+
+
+LG, DR, PI, TK, NA, BO, PO, WN, WS, POS, MSK, DL, UA, US = (_a(i) for i in range(14))
+
+
 def _verify(sd, **over):
-    args = dict(logits=A, dtype=1, draft=A, pad_in=A, B=2, k=3, V=100, W_in=10, tokens=A, n_acc=A,
-                bonus=A, pad_out=A, w_new=A, ws=A, ws_bytes=sd.workspace_bytes(2, 3, 100), status=None, stream=None)
+    args = dict(logits=LG, dtype=1, draft=DR, pad_in=PI, B=2, k=3, V=100, W_in=10, tokens=TK, n_acc=NA,
+                bonus=BO, pad_out=PO, w_new=WN, ws=WS, ws_bytes=sd.workspace_bytes(2, 3, 100), status=None,
+                stream=None)
     args.update(over)
     return sd.lib.specdec_verify_greedy(*args.values())
 
@@ -74,9 +83,12 @@ def _verify(sd, **over):
     (dict(B=-1), 1), (dict(B=70000), 1), (dict(k=-1), 1), (dict(k=65), 1), (dict(V=0), 1),
     (dict(W_in=3), 1), (dict(W_in=1 << 25), 1), (dict(dtype=7), 2), (dict(logits=None), 1),
     (dict(draft=None), 1), (dict(pad_in=None), 1), (dict(tokens=None), 1), (dict(n_acc=None), 1),
-    (dict(pad_out=None), 1), (dict(w_new=None), 1), (dict(logits=A + 1), 2), (dict(dtype=0, logits=A + 2), 2),
-    (dict(tokens=A + 2), 2), (dict(ws=None), 4), (dict(ws=A + 4), 4), (dict(ws_bytes=16), 4),
+    (dict(pad_out=None), 1), (dict(w_new=None), 1), (dict(logits=LG + 1), 2), (dict(dtype=0, logits=LG + 2), 2),
+    (dict(tokens=TK + 2), 2), (dict(ws=None), 4), (dict(ws=WS + 4), 4), (dict(ws_bytes=16), 4),
     (dict(B=65536, k=63), 1),
+    # outputs overlapping inputs or each other (a decode loop passing pad_in as pad_out)
+    (dict(pad_out=PI), 1), (dict(n_acc=TK + 4), 1), (dict(tokens=DR), 1), (dict(w_new=PO + 4), 1),
+    (dict(ws=LG + 64), 1), (dict(bonus=NA), 1),
 ])
 def test_verify_rejects(sd, over, code):
     _no_gpu()
@@ -128,10 +140,12 @@ def test_realign_empty_cache_is_a_noop(sd):
 def test_posmask_rejects(sd):
     _no_gpu()
     f = sd.lib.specdec_build_posmask
-    assert f(A, A, 2, 3, A, A, 3, None, None) == 1         # pm_cap < k+1
-    assert f(None, A, 2, 3, A, A, 64, None, None) == 1
-    assert f(A, A, 2, 3, A + 4, A, 64, None, None) == 2    # pos not 8-byte aligned
-    assert f(A, A, -1, 3, A, A, 64, None, None) == 1
+    assert f(PO, WN, 2, 3, POS, MSK, 3, None, None) == 1         # pm_cap < k+1
+    assert f(None, WN, 2, 3, POS, MSK, 64, None, None) == 1
+    assert f(PO, WN, 2, 3, POS + 4, MSK, 64, None, None) == 2    # pos not 8-byte aligned
+    assert f(PO, WN, -1, 3, POS, MSK, 64, None, None) == 1
+    assert f(PO, WN, 2, 3, POS, POS + 1000, 64, None, None) == 1  # mask inside pos
+    assert f(PO, WN, 2, 3, PO - 8, MSK, 64, None, None) == 1     # pos over pad_out
     assert f(None, None, 0, 3, None, None, 64, None, None) == 0   # empty batch
 
 
@@ -141,10 +155,11 @@ def test_step_rejects(sd):
     ws = sd.workspace_bytes(2, 3, 100)
     S_IN, S_OUT = A + (2 << 30), A + (3 << 30)
 
-    def step(B=2, pm_cap=64, src=src, dst=dst, ws_bytes=ws, s_in=None, s_in_stride=0, s_out=None, s_out_stride=0):
-        return sd.lib.specdec_step(A, 1, A, A, B, 3, 100, 10, ctypes.byref(src), ctypes.byref(dst), A, A, A, A, A,
-                                   A, A, pm_cap, s_in, s_in_stride, s_out, s_out_stride, -1, A, ws_bytes, None,
-                                   None, None)
+    def step(B=2, pm_cap=64, src=src, dst=dst, ws_bytes=ws, s_in=None, s_in_stride=0, s_out=None, s_out_stride=0,
+             pad_out=PO, pos=POS):
+        return sd.lib.specdec_step(LG, 1, DR, PI, B, 3, 100, 10, ctypes.byref(src), ctypes.byref(dst), TK, NA, BO,
+                                   pad_out, WN, pos, MSK, pm_cap, s_in, s_in_stride, s_out, s_out_stride, -1, WS,
+                                   ws_bytes, None, None, None)
     assert step(pm_cap=13) == 1                  # pm_cap < W_in + k + 1
     assert step(src=_kv(sd, B=3), dst=_kv(sd, data=A + (1 << 30), B=3)) == 1   # cache rows differ
     assert step(ws_bytes=8) == 4
@@ -155,6 +170,8 @@ def test_step_rejects(sd):
     assert step(s_in=S_IN, s_in_stride=16, s_out=S_IN + 16, s_out_stride=16) == 1
     assert step(s_in=S_IN, s_in_stride=12, s_out=S_IN, s_out_stride=16) == 1
     assert step(s_in=S_IN + 2, s_in_stride=16, s_out=S_OUT, s_out_stride=16) == 2   # misaligned
+    assert step(pad_out=PI) == 1                 # pad_out aliasing pad_in
+    assert step(pos=NA - 8) == 1                 # pos over n_acc
 
 
 def test_realign_tokens_rejects(sd):
@@ -273,8 +290,8 @@ def test_scatter_rejects(sd):
 
 
 def _sample(sd, **over):
-    args = dict(logits=A, draft_logits=A + (1 << 28), dtype=1, draft=A, pad_in=A, u_accept=A, u_sample=A, T=0.8,
-                B=2, k=3, V=100, W_in=10, tokens=A, n_acc=A, bonus=A, pad_out=A, w_new=A, ws=A,
+    args = dict(logits=LG, draft_logits=DL, dtype=1, draft=DR, pad_in=PI, u_accept=UA, u_sample=US, T=0.8,
+                B=2, k=3, V=100, W_in=10, tokens=TK, n_acc=NA, bonus=BO, pad_out=PO, w_new=WN, ws=WS,
                 ws_bytes=sd.sample_workspace_bytes(2, 3, 100), status=None, stream=None)
     args.update(over)
     return sd.lib.specdec_verify_sample(*args.values())
@@ -284,8 +301,9 @@ def _sample(sd, **over):
     (dict(B=-1), 1), (dict(k=65), 1), (dict(V=0), 1), (dict(W_in=3), 1), (dict(dtype=5), 2),
     (dict(T=0.0), 1), (dict(T=-1.0), 1), (dict(T=float("inf")), 1), (dict(T=float("nan")), 1), (dict(T=1e-39), 1),
     (dict(logits=None), 1), (dict(draft_logits=None), 1), (dict(u_accept=None), 1), (dict(u_sample=None), 1),
-    (dict(draft=None), 1), (dict(w_new=None), 1), (dict(logits=A + 1), 2), (dict(u_sample=A + 2), 2),
-    (dict(ws=None), 4), (dict(ws=A + 4), 4), (dict(ws_bytes=64), 4), (dict(B=40000, k=20), 1),
+    (dict(draft=None), 1), (dict(w_new=None), 1), (dict(logits=LG + 1), 2), (dict(u_sample=US + 2), 2),
+    (dict(ws=None), 4), (dict(ws=WS + 4), 4), (dict(ws_bytes=64), 4), (dict(B=40000, k=20), 1),
+    (dict(pad_out=PI), 1), (dict(tokens=UA), 1), (dict(ws=DL + 128), 1),
 ])
 def test_verify_sample_rejects(sd, over, code):
     _no_gpu()
