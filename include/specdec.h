@@ -308,7 +308,9 @@ specdec_status_t specdec_step(const void* logits, int32_t dtype, const int32_t* 
  *             (both, then k is not used).
  * A row whose slot is outside [0, N) or whose length is outside [0, Lb], above
  * pool_cap or above pool_tok_stride - 1 is skipped (no byte of it written) and
- * flagged SPECDEC_DEV_BAD_SLOT.
+ * flagged SPECDEC_DEV_BAD_SLOT.  The outputs (batch cache, batch_tok, pads,
+ * pos, mask) must not overlap each other or the inputs (pool cache, pool_tok,
+ * lens, slots): SPECDEC_ERR_INVALID_ARGUMENT.
  */
 specdec_status_t specdec_gather_batch(const specdec_kv_t* pool, const int32_t* pool_tok,
                                       int64_t pool_tok_stride, const int32_t* lens,
@@ -351,7 +353,9 @@ specdec_status_t specdec_gather_batch(const specdec_kv_t* pool, const int32_t* p
  * [0, Lb], or n + a above pool_cap or above pool_tok_stride - 1 is skipped and
  * flagged (SPECDEC_DEV_BAD_SLOT / _BAD_ACCEPT / _BAD_PAD_IN).  lens[s] !=
  * Lb - pads[i] on entry is flagged SPECDEC_DEV_SLOT_LEN (the row is still
- * written back).
+ * written back).  The updated buffers (pool cache, pool_tok, lens, batch_tok)
+ * must not overlap each other or the inputs (batch cache, pads, tokens, n_acc,
+ * slots): SPECDEC_ERR_INVALID_ARGUMENT.
  */
 specdec_status_t specdec_scatter_accepted(const specdec_kv_t* batch, const int32_t* pads,
                                           const int32_t* tokens, const int32_t* n_acc,
@@ -487,7 +491,8 @@ typedef struct specdec_varlen {
  *               pos_cap >= src->T_cap.
  * A sequence shorter than k + 1 rows or longer than max_len, outside the
  * buffer, or with n_acc outside [0, k] keeps no row and is flagged
- * (SPECDEC_DEV_BAD_WIDTH / _BAD_ACCEPT).
+ * (SPECDEC_DEV_BAD_WIDTH / _BAD_ACCEPT).  cu_out, pos and dst must not overlap
+ * each other or cu_in, n_acc and src: SPECDEC_ERR_INVALID_ARGUMENT.
  */
 specdec_status_t specdec_varlen_rollback(const specdec_varlen_t* src, const specdec_varlen_t* dst,
                                          const int32_t* cu_in, const int32_t* n_acc, int32_t B,

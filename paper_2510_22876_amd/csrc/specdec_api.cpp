@@ -665,6 +665,16 @@ specdec_status_t specdec_gather_batch(const specdec_kv_t* pool, const int32_t* p
                   (long long)Lb + k + 1);
   }
   if (dev_status && !aligned(dev_status, 4)) return fail(SPECDEC_ERR_UNSUPPORTED, "dev_status not 4-byte aligned");
+  {
+    const int64_t b4 = 4 * static_cast<int64_t>(B), n = pos ? static_cast<int64_t>(B) * pm_cap : 0;
+    s = check_disjoint({{pool->data, kv_bytes(pool), "pool"},
+                        {pool_tok, batch_tok ? static_cast<int64_t>(pool->B) * pool_tok_stride * 4 : 0, "pool_tok"},
+                        {lens, 4 * static_cast<int64_t>(pool->B), "lens"}, {slots, b4, "slots"}},
+                       {{batch->data, kv_bytes(batch), "batch"},
+                        {batch_tok, batch_tok ? static_cast<int64_t>(B) * btok_stride * 4 : 0, "batch_tok"},
+                        {pads, b4, "pads"}, {pos, 8 * n, "pos"}, {mask, n, "mask"}});
+    if (s) return s;
+  }
   specdec::GatherLaunch p{};
   p.pool = pool->data;
   p.pool_cap = pool->cap;
@@ -718,6 +728,17 @@ specdec_status_t specdec_scatter_accepted(const specdec_kv_t* batch, const int32
       return fail(SPECDEC_ERR_INVALID_ARGUMENT, "batch and pool token rows overlap");
   }
   if (dev_status && !aligned(dev_status, 4)) return fail(SPECDEC_ERR_UNSUPPORTED, "dev_status not 4-byte aligned");
+  {
+    // the pool cache, pool token rows, lengths and batch token rows are updated
+    const int64_t b4 = 4 * static_cast<int64_t>(B);
+    s = check_disjoint({{batch->data, kv_bytes(batch), "batch"}, {pads, b4, "pads"},
+                        {tokens, b4 * (k + 1), "tokens"}, {n_acc, b4, "n_acc"}, {slots, b4, "slots"}},
+                       {{pool->data, kv_bytes(pool), "pool"},
+                        {pool_tok, static_cast<int64_t>(pool->B) * pool_tok_stride * 4, "pool_tok"},
+                        {lens, 4 * static_cast<int64_t>(pool->B), "lens"},
+                        {batch_tok, batch_tok ? static_cast<int64_t>(B) * btok_stride * 4 : 0, "batch_tok"}});
+    if (s) return s;
+  }
   specdec::WritebackLaunch p{};
   p.batch = batch->data;
   p.batch_cap = batch->cap;
@@ -807,8 +828,13 @@ specdec_status_t specdec_varlen_rollback(const specdec_varlen_t* src, const spec
       return fail(SPECDEC_ERR_INVALID_ARGUMENT, "src and dst caches overlap");
   }
   const int64_t c4 = 4 * (static_cast<int64_t>(B) + 1);
-  if (ranges_overlap(cu_out, c4, cu_in, c4) || ranges_overlap(cu_out, c4, n_acc, 4 * static_cast<int64_t>(B)))
-    return fail(SPECDEC_ERR_INVALID_ARGUMENT, "cu_out overlaps cu_in or n_acc");
+  {
+    const bool data = src->L > 0 && src->T_cap > 0;
+    specdec_status_t s = check_disjoint(
+        {{cu_in, c4, "cu_in"}, {n_acc, 4 * static_cast<int64_t>(B), "n_acc"}, {data ? src->data : nullptr, bytes_src, "src"}},
+        {{cu_out, c4, "cu_out"}, {pos, pos ? 8 * pos_cap : 0, "pos"}, {data ? dst->data : nullptr, bytes_dst, "dst"}});
+    if (s) return s;
+  }
   if (static_cast<int64_t>(src->L) * 2 * B > 0xFFFFFFFFLL) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "too many spans");
   specdec::VarlenLaunch p{src->data, dst->data, src->T_cap, dst->T_cap, src->L, src->H, src->D, cu_in, n_acc,
                           B, k, max_len, cu_out, pos, dev_status};

@@ -220,8 +220,8 @@ BTOK, PTOK = A + (5 << 30), A + (6 << 30)
 def _gather(sd, pool=None, batch=None, **over):
     pool = pool if pool is not None else _kv(sd, data=POOL, B=5, cap=64)
     batch = batch if batch is not None else _kv(sd, B=2, cap=32)
-    args = dict(pool_tok=PTOK, pool_tok_stride=65, lens=A, slots=A, B=2, Lb=20, k=3, batch_tok=BTOK,
-                btok_stride=21, pad_id=-1, pads=A, pos=A, mask=A, pm_cap=24, status=None, stream=None)
+    args = dict(pool_tok=PTOK, pool_tok_stride=65, lens=NA, slots=DR, B=2, Lb=20, k=3, batch_tok=BTOK,
+                btok_stride=21, pad_id=-1, pads=PO, pos=POS, mask=MSK, pm_cap=24, status=None, stream=None)
     args.update(over)
     a = list(args.values())
     return sd.lib.specdec_gather_batch(ctypes.byref(pool), *a[:7], ctypes.byref(batch), *a[7:])
@@ -237,7 +237,7 @@ def test_gather_rejects(sd):
     assert _gather(sd, pool=K(data=A + 4096, B=5, cap=64)) == 1      # pool overlaps the batch
     assert _gather(sd, pool=K(data=POOL, B=0, cap=64)) == 1          # no slot
     assert _gather(sd, lens=None) == 1
-    assert _gather(sd, slots=A + 2) == 2
+    assert _gather(sd, slots=DR + 2) == 2
     assert _gather(sd, pads=None) == 1
     assert _gather(sd, btok_stride=20) == 1                          # < Lb + 1
     assert _gather(sd, pool_tok=None) == 1                           # batch_tok without pool_tok
@@ -245,7 +245,10 @@ def test_gather_rejects(sd):
     assert _gather(sd, batch_tok=PTOK + 64) == 1                     # token rows overlap
     assert _gather(sd, pm_cap=23) == 1                               # < Lb + k + 1
     assert _gather(sd, mask=None) == 1                               # pos without mask
-    assert _gather(sd, pos=A + 4) == 2
+    assert _gather(sd, pos=POS + 4) == 2
+    assert _gather(sd, pads=NA + 4) == 1                             # pads over the lengths
+    assert _gather(sd, mask=POS + 64) == 1                           # mask inside pos
+    assert _gather(sd, pos=POOL) == 1                                # pos over the pool cache
     assert _gather(sd, k=65) == 1
     assert _gather(sd, batch=K(B=2, cap=32, D=12)) == 2
     assert _gather(sd, B=0, batch=K(B=0, cap=32), lens=None, slots=None, pads=None) == 0   # empty batch
@@ -261,8 +264,8 @@ def test_gather_valid_arguments_pass_validation(sd):
 def _scatter(sd, pool=None, batch=None, **over):
     pool = pool if pool is not None else _kv(sd, data=POOL, B=5, cap=64)
     batch = batch if batch is not None else _kv(sd, B=2, cap=32)
-    args = dict(pads=A, tokens=A, n_acc=A, slots=A, B=2, k=3, Lb=20)
-    rest = dict(pool_tok=PTOK, pool_tok_stride=65, lens=A, batch_tok=BTOK, btok_stride=25, mode=0, status=None,
+    args = dict(pads=PO, tokens=TK, n_acc=NA, slots=DR, B=2, k=3, Lb=20)
+    rest = dict(pool_tok=PTOK, pool_tok_stride=65, lens=PI, batch_tok=BTOK, btok_stride=25, mode=0, status=None,
                 stream=None)
     args.update({k: v for k, v in over.items() if k in args})
     rest.update({k: v for k, v in over.items() if k in rest})
@@ -279,7 +282,9 @@ def test_scatter_rejects(sd):
     assert _scatter(sd, pool=K(data=A + 4096, B=5, cap=64)) == 1
     assert _scatter(sd, pads=None) == 1
     assert _scatter(sd, tokens=None) == 1
-    assert _scatter(sd, n_acc=A + 2) == 2
+    assert _scatter(sd, n_acc=NA + 2) == 2
+    assert _scatter(sd, lens=NA) == 1                                # lengths over n_acc
+    assert _scatter(sd, lens=POOL + 128) == 1                        # lengths inside the pool cache
     assert _scatter(sd, pool_tok=None) == 1
     assert _scatter(sd, pool_tok_stride=0) == 1
     assert _scatter(sd, btok_stride=24) == 1                         # < Lb + k + 2
@@ -358,5 +363,7 @@ def test_varlen_rollback_rejects(sd):
     assert call(pos_cap=99) == 1
     assert call(dst=_vdesc(sd, data=A + 4096)) == 1                        # caches overlap
     assert call(cu_out=CI + 4) == 1                                        # cu_out over cu_in
+    assert call(pos=NA) == 1                                               # positions over n_acc
+    assert call(pos=A + (1 << 30) + 256) == 1                              # positions inside the dst cache
     assert call(src=_vdesc(sd, data=A + 8), dst=_vdesc(sd, data=A + (1 << 30))) == 2
     assert call(B=0, cu_in=None, n_acc=None, cu_out=None) == 0
