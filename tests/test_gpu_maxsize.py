@@ -12,6 +12,7 @@
 * The in-place realignment of one 138 GB cache whose spans hold 2.15 G
   vectors: the moving row's kept entries lie at vector offsets past 2^31
   within their spans; checked against a copy of them taken before the step.
+* Family B compaction of a flat cache of 2^31 - 8 rows.
 Caches are compared as int16 bit patterns (random bits include NaNs).
 """
 import numpy as np
@@ -151,3 +152,41 @@ def test_realign_in_place_beyond_2_31_vectors_per_span():
         assert not bool(got[:pad1 + 1].any()), f"kv {kv}: pads not +0.0"
         # row 0 does not move (its padding stays 0)
         assert torch.equal(src[0, kv, 0, 0, W_in - 4:W_in].view(torch.int16), untouched[kv].view(torch.int16))
+
+
+def test_varlen_rollback_largest_buffer():
+    """Family B compaction of a flat cache of 2^31 - 8 rows (two 69 GB
+    buffers): row offsets, positions and slab offsets near the int32 limit.
+    Checked with torch on the device against the definition (each sequence's
+    kept rows moved to the running offset, positions 0..keep-1)."""
+    from paper_2510_22876_amd import specdec as sd
+    T, k = 2**31 - 8, 1
+    src = torch.empty((1, 2, T, 1, 8), dtype=torch.bfloat16, device="cuda")
+    g = torch.Generator(device="cuda")
+    g.manual_seed(11)
+    src.view(torch.int16).random_(-32768, 32767, generator=g)
+    say(f"varlen rollback T={T}: {src.numel() * 2 / 1e9:.1f} GB per buffer")
+    dst = torch.empty_like(src)
+    i32 = dict(dtype=torch.int32, device="cuda")
+    b1 = 1_200_000_000
+    cu_in = torch.tensor([0, b1, T - 3], **i32)
+    n_acc = torch.tensor([1, 0], **i32)                 # sequence 0 keeps all its rows, sequence 1 drops one
+    keep = [b1, (T - 3 - b1) - 1]
+    cu_out = torch.full((3,), -9, **i32)
+    pos = torch.full((T,), -1, dtype=torch.int64, device="cuda")
+    status = torch.zeros(1, **i32)
+    sd.specdec_varlen_rollback(src, dst, cu_in, n_acc, k, b1, cu_out, pos, status)
+    torch.cuda.synchronize()
+    assert int(status.cpu()[0]) == 0
+    assert cu_out.cpu().tolist() == [0, keep[0], keep[0] + keep[1]]
+    starts = [0, b1]
+    o = 0
+    for i in range(2):
+        for kv in range(2):
+            got = dst[0, kv, o:o + keep[i]].view(torch.int16)
+            want = src[0, kv, starts[i]:starts[i] + keep[i]].view(torch.int16)
+            assert torch.equal(got, want), f"sequence {i} kv {kv}: rows differ"
+        assert torch.equal(pos[o:o + keep[i]], torch.arange(keep[i], dtype=torch.int64, device="cuda")), \
+            f"sequence {i}: positions"
+        o += keep[i]
+    assert bool((pos[o:] == -1).all()), "positions written beyond the kept rows"
