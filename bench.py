@@ -574,6 +574,8 @@ def main():
                          "varlen: Family B rollback; chained: in-place steps along a chain (per-step times)")
     ap.add_argument("--exspec-batch", choices=["ragged", "same"], default="ragged",
                     help="exspec: a batch of prompt-distributed lengths (unpad-repad) or one length (concatenation)")
+    ap.add_argument("--graph", action="store_true",
+                    help="capture the step in a HIP graph once and replay it in the timed loop")
     ap.add_argument("--copy-ceiling", type=int, choices=[0, 1], default=1,
                     help="also time the runtime's device-to-device memcpy of the realign's bytes, for comparison")
     ap.add_argument("--copy-calibration", type=float, default=0.0,
@@ -661,7 +663,21 @@ def main():
         raise RuntimeError("device flagged invalid values")
 
     K = args.steps
-    timers = args.kernel_timers == "on"
+    timers = args.kernel_timers == "on" and not args.graph
+    run = step
+    if args.graph:
+        # the step captured once in a HIP graph and replayed: no host work per
+        # step (kernel timers stay off inside the capture; the second pass
+        # below times the kernels eagerly)
+        sd.timing_enable(False)
+        if pristine is not None:
+            restore()
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            step()
+        torch.cuda.synchronize()
+        run = graph.replay
     sd.timing_reset()
     # only the dominant kernel is bracketed inside the timed region
     sd.timing_enable(1 << sd.KERNEL_REALIGN if timers else 0)
@@ -670,7 +686,7 @@ def main():
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         for _ in range(K):
-            step()
+            run()
         torch.cuda.synchronize()
         elapsed = time.perf_counter() - t0
     else:
@@ -681,7 +697,7 @@ def main():
         for _ in range(K):
             restore()
             s.record()
-            step()
+            run()
             e.record()
             torch.cuda.synchronize()
             step_ms.append(s.elapsed_time(e))
@@ -706,7 +722,7 @@ def main():
         evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K)]
         for s_ev, e_ev in evs:
             s_ev.record()
-            step()
+            run()
             e_ev.record()
         torch.cuda.synchronize()
         step_ms = [s_ev.elapsed_time(e_ev) for s_ev, e_ev in evs]
@@ -759,6 +775,7 @@ def main():
                                                  f"target + N(0,1), drafts drawn from q" if sample else ""),
             "B": w.B, "k": w.k, "V": w.V, "L": w.L, "H": w.H, "D": w.D, "W_in": W_in, "w_new": w_new,
             "variant": variant, "seed": args.seed, "token_row": token_row, "verify": args.verify,
+            "graph": bool(args.graph),
             **({"temperature": args.temperature, "draft_noise": 1.0} if sample else {}),
             "step_GBps": round(step_gbs, 1),
             "step_bytes": realign_bytes + by["verify"],
