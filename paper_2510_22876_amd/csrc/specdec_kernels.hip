@@ -51,12 +51,23 @@ __device__ __forceinline__ uint32_t key_f32(uint32_t u) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
+// 16-bit logits: a positive h maps to h | 0x8000, a negative one to
+// (h ^ 0xFFFF) + 1 (so -0.0 lands on +0.0's key 0x8000), a NaN to 0xFFFF.
 template <uint32_t kNanMag>  // 0x7F80 for bf16, 0x7C00 for f16
 __device__ __forceinline__ uint32_t key_16(uint32_t h) {
-  const uint32_t mag = h & 0x7FFFu;
-  if (mag > kNanMag) return 0xFFFFu;
-  if (mag == 0u) return 0x8000u;
-  return (h & 0x8000u) ? (~h & 0xFFFFu) : (h | 0x8000u);
+  if ((h & 0x7FFFu) > kNanMag) return 0xFFFFu;
+  return (h & 0x8000u) ? ((h ^ 0xFFFFu) + 1u) : (h | 0x8000u);
+}
+
+typedef short s16x2 __attribute__((ext_vector_type(2)));
+typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+
+// The keys of both halves of a word with packed 16-bit operations, exact
+// except for NaNs (which land outside the keys of -inf..+inf).
+__device__ __forceinline__ u16x2 keys2(uint32_t w) {
+  const s16x2 sign = __builtin_bit_cast(s16x2, w) >> (s16x2){15, 15};   // 0xFFFF on negative halves
+  const uint32_t m = __builtin_bit_cast(uint32_t, sign);
+  return __builtin_bit_cast(u16x2, w ^ (m | 0x80008000u)) + __builtin_bit_cast(u16x2, m & 0x00010001u);
 }
 
 struct Best {
@@ -93,15 +104,27 @@ struct Logit16 {
   __device__ static uint32_t key_at(const char* row, int64_t i) {
     return key_16<kNanMag>(*reinterpret_cast<const uint16_t*>(row + 2 * i));
   }
-  __device__ static void take_word(Best& b, uint32_t w, int32_t e) {
-    b.take(key_16<kNanMag>(w & 0xFFFFu), e);
-    b.take(key_16<kNanMag>(w >> 16), e + 1);
+  static constexpr uint32_t kPosInf = kNanMag | 0x8000u;                  // key of +inf
+  static constexpr uint32_t kNegInf = ((kNanMag | 0x8000u) ^ 0xFFFFu) + 1u;  // key of -inf
+  // Largest key of a 16-byte vector of 8 logits (0xFFFF if it holds a NaN).
+  __device__ static uint32_t vec_key(const uint4& q) {
+    const u16x2 a = keys2(q.x), b = keys2(q.y), c = keys2(q.z), d = keys2(q.w);
+    const u16x2 hi = __builtin_elementwise_max(__builtin_elementwise_max(a, b), __builtin_elementwise_max(c, d));
+    const u16x2 lo = __builtin_elementwise_min(__builtin_elementwise_min(a, b), __builtin_elementwise_min(c, d));
+    const uint32_t vmax = hi.x > hi.y ? hi.x : hi.y;
+    const uint32_t vmin = lo.x < lo.y ? lo.x : lo.y;
+    return (vmax > kPosInf || vmin < kNegInf) ? 0xFFFFu : vmax;
   }
-  __device__ static void take_vec(Best& b, const uint4& q, int32_t e) {
-    take_word(b, q.x, e);
-    take_word(b, q.y, e + 2);
-    take_word(b, q.z, e + 4);
-    take_word(b, q.w, e + 6);
+  // The lowest element of vector q (first element index e) whose key is k.
+  __device__ static void take_in_vec(Best& b, const uint4& q, uint32_t k, int32_t e) {
+    const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+    int32_t at = e + 7;
+#pragma unroll
+    for (int j = 7; j >= 0; --j) {
+      const uint32_t h = (w[j >> 1] >> (16 * (j & 1))) & 0xFFFFu;
+      if (key_16<kNanMag>(h) == k) at = e + j;
+    }
+    b.take(k, at);
   }
 };
 template <>
@@ -159,17 +182,44 @@ __device__ __forceinline__ void scan_range(const char* row, int64_t beg, int64_t
   const int64_t a1 = a0 + nvec * kPerVec;
   if (tid < head) b.take(T::key_at(row, beg + tid), static_cast<int32_t>(beg + tid));
   const uint4* vp = reinterpret_cast<const uint4*>(row + a0 * T::kBytes);
-  for (int64_t v0 = 0; v0 < nvec; v0 += kThreads * kUnroll) {
-    uint4 q[kUnroll];
+  if constexpr (T::kBytes == 2) {
+    // per vector only its largest key; the first vector (lowest index) holding
+    // this thread's largest key is kept in registers and searched at the end
+    uint32_t vk = 0u;
+    int32_t ve = -1;
+    uint4 vq = make_uint4(0u, 0u, 0u, 0u);
+    for (int64_t v0 = 0; v0 < nvec; v0 += kThreads * kUnroll) {
+      uint4 q[kUnroll];
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      const int64_t v = v0 + u * kThreads + tid;
-      q[u] = v < nvec ? vp[v] : make_uint4(0u, 0u, 0u, 0u);
+      for (int u = 0; u < kUnroll; ++u) {
+        const int64_t v = v0 + u * kThreads + tid;
+        q[u] = v < nvec ? vp[v] : make_uint4(0u, 0u, 0u, 0u);
+      }
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) {
+        const int64_t v = v0 + u * kThreads + tid;
+        const uint32_t k = T::vec_key(q[u]);
+        if (v < nvec && k > vk) {
+          vk = k;
+          ve = static_cast<int32_t>(a0 + v * kPerVec);
+          vq = q[u];
+        }
+      }
     }
+    if (ve >= 0) T::take_in_vec(b, vq, vk, ve);
+  } else {
+    for (int64_t v0 = 0; v0 < nvec; v0 += kThreads * kUnroll) {
+      uint4 q[kUnroll];
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      const int64_t v = v0 + u * kThreads + tid;
-      if (v < nvec) T::take_vec(b, q[u], static_cast<int32_t>(a0 + v * kPerVec));
+      for (int u = 0; u < kUnroll; ++u) {
+        const int64_t v = v0 + u * kThreads + tid;
+        q[u] = v < nvec ? vp[v] : make_uint4(0u, 0u, 0u, 0u);
+      }
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) {
+        const int64_t v = v0 + u * kThreads + tid;
+        if (v < nvec) T::take_vec(b, q[u], static_cast<int32_t>(a0 + v * kPerVec));
+      }
     }
   }
   if (tid < end - a1) b.take(T::key_at(row, a1 + tid), static_cast<int32_t>(a1 + tid));
