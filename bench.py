@@ -148,17 +148,24 @@ def percentiles(ms):
             "step_ms_p90": round(float(np.percentile(a, 90)), 5)}
 
 
-def cpu_baseline(w, logits, draft, pad_in, W_in, src, budget_s: float, s_rows=None):
+def cpu_baseline(w, logits, draft, pad_in, W_in, src, budget_s: float, s_rows=None, sample=None):
     """The oracle as it stands, single-threaded on the host, on a bounded
-    sample: verification over every logit row, the KV realignment of whole
-    layer slabs (cycling over up to two layers until ``budget_s`` seconds of
-    work), position ids / mask and the token row; scaled to one whole step."""
+    sample: verification over every logit row (greedy, or stochastic when
+    ``sample`` = (draft_logits, u_accept, u_sample, temperature)), the KV
+    realignment of whole layer slabs (cycling over up to two layers until
+    ``budget_s`` seconds of work), position ids / mask and the token row;
+    scaled to one whole step."""
     import oracle
     k = w.k
     lg = logits.cpu()
     dr = draft.cpu().numpy()
     t0 = time.perf_counter()
-    v = oracle.verify(lg, w.logit_dtype, dr, pad_in, W_in)
+    if sample is None:
+        v = oracle.verify(lg, w.logit_dtype, dr, pad_in, W_in)
+    else:
+        dlg, ua, us, temp = sample
+        v = oracle.verify_sample(lg, dlg.cpu(), w.logit_dtype, dr, pad_in, ua.cpu().numpy(), us.cpu().numpy(),
+                                 temp, W_in)
     t_verify = time.perf_counter() - t0
     t0 = time.perf_counter()
     oracle.posmask(v["pad_out"], v["w_new"], k)
@@ -180,7 +187,8 @@ def cpu_baseline(w, logits, draft, pad_in, W_in, src, budget_s: float, s_rows=No
     per_layer = t_real / runs
     est = t_verify + per_layer * w.L + t_pm
     return dict(value=1.0 / est, unit="steps/s", cores=1, kind="oracle", cpu_model=cpu_model(),
-                sample=(f"oracle verify over all {w.B * (w.k + 1)} logit rows ({t_verify * 1e3:.1f} ms), "
+                sample=(f"oracle {'stochastic ' if sample is not None else ''}verify over all "
+                        f"{w.B * (w.k + 1) + (w.B * w.k if sample is not None else 0)} logit rows ({t_verify * 1e3:.1f} ms), "
                         f"KV realign of {runs} one-layer slabs cycling over layers 0..{nl - 1} "
                         f"({per_layer * 1e3:.1f} ms per layer, x{w.L} layers), pos/mask and token row ({t_pm * 1e3:.2f} ms); "
                         f"single-threaded, scaled to one whole step ({est:.2f} s)"))
@@ -411,6 +419,10 @@ def bench_varlen(args, w):
     traffic, traffic_src = read_traffic_summary(w.name, "oop", kernel="varlen", srcs=VARLEN_SRCS)
     log(f"[bench] varlen n_acc={n_acc.tolist()} compaction {vms:.4f} ms ({algo / 1e9:.3f} GB, {achieved:.0f} GB/s), "
         f"step {ms_per_step:.4f} ms; traffic: {traffic_src}")
+    cpu = None
+    if args.cpu_baseline_seconds > 0:
+        cpu = cpu_baseline_varlen(w, logits, draft, src, cu, args.cpu_baseline_seconds)
+        log(f"[bench] cpu baseline: {cpu['value']:.4f} steps/s ({cpu['sample']})")
     line = {
         "metric": METRIC_VARLEN, "value": K / elapsed, "unit": "steps/s", "n_gpus": 1, "steps": K,
         "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": True, "scaling": "weak",
@@ -420,9 +432,35 @@ def bench_varlen(args, w):
         "roofline": {"bound": "hbm", "kernel": "varlen offsets + compaction (+ positions)", "achieved": round(achieved, 1),
                      "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4),
                      "traffic": traffic, "algorithmic_bytes": algo},
-        "cpu_baseline": None,
+        "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)
+
+
+def cpu_baseline_varlen(w, logits, draft, src, cu, budget_s):
+    """The oracle, single-threaded, on a bounded sample of the Family B step:
+    verification over every logit row, then the compaction of one-layer slabs
+    of the flat cache cycling over up to two layers until ``budget_s`` seconds
+    of work; scaled to one whole step."""
+    import oracle
+    import torch
+    k = w.k
+    t0 = time.perf_counter()
+    v = oracle.verify(logits.cpu(), w.logit_dtype, draft.cpu().numpy(), np.zeros(w.B, np.int32), k + 1)
+    t_verify = time.perf_counter() - t0
+    host = [src[l:l + 1].contiguous().view(torch.int16).cpu().numpy().view(np.uint16) for l in range(min(w.L, 2))]
+    runs, t_layers = 0, 0.0
+    while t_layers < budget_s or runs == 0:
+        t0 = time.perf_counter()
+        oracle.varlen_rollback(host[runs % len(host)], cu, v["n_acc"], k)
+        t_layers += time.perf_counter() - t0
+        runs += 1
+    per_layer = t_layers / runs
+    est = t_verify + per_layer * w.L
+    return dict(value=1.0 / est, unit="steps/s", cores=1, kind="oracle", cpu_model=cpu_model(),
+                sample=(f"oracle verify over all {w.B * (k + 1)} logit rows ({t_verify * 1e3:.1f} ms), compaction of "
+                        f"{runs} one-layer slabs of the flat cache ({per_layer * 1e3:.1f} ms per layer, x{w.L} layers); "
+                        f"single-threaded, scaled to one whole step ({est:.2f} s)"))
 
 
 def bench_chained(args, w):
@@ -512,6 +550,13 @@ def bench_chained(args, w):
                                        (np.mean(realign[t]) * 1e-3) / 1e9, 1)} for t in done]
     ms_all = [m for t in done for m in per[t]]
     log(f"[bench] chained: {K} steps, mean {elapsed / K * 1e3:.4f} ms, realign {achieved:.0f} GB/s")
+    cpu = None
+    if args.cpu_baseline_seconds > 0:
+        # the oracle on the chain's first step (its geometry, logits and cache)
+        cpu = cpu_baseline(w, inputs[0][0], inputs[0][1], pad_in0, W_in0, pristine, args.cpu_baseline_seconds,
+                           pristine_s.cpu().numpy())
+        cpu["sample"] = "the chain's first step: " + cpu["sample"]
+        log(f"[bench] cpu baseline: {cpu['value']:.4f} steps/s ({cpu['sample']})")
     copy_gbs = copy_ceiling(rbytes // (2 * K)) if args.copy_ceiling else None
     line = {
         "metric": METRIC, "value": K / elapsed, "unit": "steps/s", "n_gpus": 1, "steps": K,
@@ -526,7 +571,7 @@ def bench_chained(args, w):
                      "algorithmic_bytes": int(rbytes // K),
                      **({"memcpy_d2d_GBps": round(copy_gbs, 1), "vs_memcpy_d2d": round(achieved / copy_gbs, 4)}
                         if copy_gbs else {})},
-        "cpu_baseline": None,
+        "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)
 
@@ -747,14 +792,13 @@ def main():
         f"({by['verify'] / 1e6:.2f} MB), step {ms_per_step:.4f} ms ({step_gbs:.0f} GB/s); traffic: {traffic_src}")
 
     cpu = None
-    if args.cpu_baseline_seconds > 0 and sample:
-        log("[bench] cpu baseline skipped for --verify sample")
-    elif args.cpu_baseline_seconds > 0:
+    if args.cpu_baseline_seconds > 0:
         s_host = None
         if token_row:
             s_host = (pristine_s if pristine_s is not None else s_in).cpu().numpy()
         cpu = cpu_baseline(w, logits, draft, pad_in, W_in, pristine if pristine is not None else src,
-                           args.cpu_baseline_seconds, s_host)
+                           args.cpu_baseline_seconds, s_host,
+                           sample=(draft_logits, u_accept, u_sample, args.temperature) if sample else None)
         log(f"[bench] cpu baseline: {cpu['value']:.4f} steps/s ({cpu['sample']})")
 
     line = {
