@@ -25,7 +25,10 @@ specdec_status_t fail(specdec_status_t code, const char* fmt, ...) {
   va_start(ap, fmt);
   std::vsnprintf(buf, sizeof(buf), fmt, ap);
   va_end(ap);
-  g_last_error = buf;
+  try {
+    g_last_error = buf;
+  } catch (...) {   // no exception crosses the C ABI; the status code still reports the failure
+  }
   return code;
 }
 
@@ -37,7 +40,12 @@ specdec_status_t ok() {
 }  // namespace
 
 namespace specdec {
-void set_last_error(const char* msg) { g_last_error = msg; }
+void set_last_error(const char* msg) {
+  try {
+    g_last_error = msg;
+  } catch (...) {
+  }
+}
 void clear_last_error() { g_last_error.clear(); }
 }  // namespace specdec
 
@@ -107,8 +115,11 @@ hipError_t timed(int kernel, hipStream_t stream, F&& launch) {
   // events that end up unused go back to the pool
   auto give_back = [&] {
     std::lock_guard<std::mutex> lk(t.mu);
-    if (b) t.pool.push_back(b);
-    if (e) t.pool.push_back(e);
+    try {
+      if (b) t.pool.push_back(b);
+      if (e) t.pool.push_back(e);
+    } catch (...) {
+    }
   };
   const bool timing = b && e;
   hipError_t r = timing ? hipEventRecord(b, stream) : hipSuccess;
@@ -119,7 +130,15 @@ hipError_t timed(int kernel, hipStream_t stream, F&& launch) {
     return r;
   }
   std::lock_guard<std::mutex> lk(t.mu);
-  t.pending.push_back({kernel, b, e});
+  try {
+    t.pending.push_back({kernel, b, e});
+  } catch (...) {   // the launch stands; only its timing is lost
+    try {
+      t.pool.push_back(b);
+      t.pool.push_back(e);
+    } catch (...) {
+    }
+  }
   return hipSuccess;
 }
 
@@ -856,6 +875,11 @@ specdec_status_t specdec_timing_enable(int32_t kernel_mask) {
 specdec_status_t specdec_timing_reset(void) {
   Timers& t = timers();
   std::lock_guard<std::mutex> lk(t.mu);
+  try {
+    t.pool.reserve(t.pool.size() + 2 * t.pending.size());   // the pushes below do not allocate
+  } catch (...) {
+    return fail(SPECDEC_ERR_INVALID_ARGUMENT, "out of host memory");
+  }
   for (const TimedLaunch& p : t.pending) {
     (void)hipEventSynchronize(p.end);
     t.pool.push_back(p.begin);
@@ -873,6 +897,11 @@ specdec_status_t specdec_timing_query(int32_t kernel, double* total_ms, int64_t*
   if (kernel < 0 || kernel >= kTimedKernels) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "unknown kernel id %d", kernel);
   Timers& t = timers();
   std::lock_guard<std::mutex> lk(t.mu);
+  try {
+    t.pool.reserve(t.pool.size() + 2 * t.pending.size());   // the pushes below do not allocate
+  } catch (...) {
+    return fail(SPECDEC_ERR_INVALID_ARGUMENT, "out of host memory");
+  }
   size_t done = 0;
   for (; done < t.pending.size(); ++done) {
     const TimedLaunch& p = t.pending[done];

@@ -4,10 +4,7 @@
 // (lazy realignment, same-length grouping, unpad-repad fallback).  No GPU
 // call is made here; the batch it picks is moved by specdec_gather_batch and
 // written back by specdec_scatter_accepted.
-#include <hip/hip_runtime.h>
-
 #include <algorithm>
-#include <cstdio>
 #include <map>
 #include <new>
 #include <vector>
@@ -90,6 +87,18 @@ void choose(specdec_sched* s) {
   s->cur_info = info;
 }
 
+// Runs a body that may allocate; no exception crosses the C ABI.
+template <typename F>
+specdec_status_t guarded(F&& body) {
+  try {
+    return body();
+  } catch (const std::bad_alloc&) {
+    return sched_fail(SPECDEC_ERR_INVALID_ARGUMENT, "out of host memory");
+  } catch (...) {
+    return sched_fail(SPECDEC_ERR_INVALID_ARGUMENT, "unexpected host error");
+  }
+}
+
 }  // namespace
 
 extern "C" {
@@ -107,23 +116,29 @@ specdec_status_t specdec_sched_create(const int32_t* lens, int32_t N, int32_t wi
   for (int32_t i = 0; i < N; ++i)
     if (lens[i] < 0 || lens[i] > SPECDEC_MAX_WIDTH)
       return sched_fail(SPECDEC_ERR_INVALID_ARGUMENT, "a length is outside [0, SPECDEC_MAX_WIDTH]");
-  specdec_sched* s = new (std::nothrow) specdec_sched;
-  if (!s) return sched_fail(SPECDEC_ERR_INVALID_ARGUMENT, "out of host memory");
-  s->N = N;
-  s->window = window;
-  s->batch = batch;
-  s->max_new = max_new;
-  s->eos_id = eos_id;
-  s->len.assign(lens, lens + N);
-  s->generated.assign(N, 0);
-  s->active.assign(N, 1);
-  s->active_order.resize(N);
-  for (int32_t i = 0; i < N; ++i) s->active_order[i] = i;
-  if (sort_by_length)
-    std::stable_sort(s->active_order.begin(), s->active_order.end(),
-                     [s](int32_t a, int32_t b) { return s->len[a] < s->len[b]; });
-  *out = s;
-  return sched_ok();
+  return guarded([&] {
+    specdec_sched* s = new specdec_sched;
+    try {
+      s->N = N;
+      s->window = window;
+      s->batch = batch;
+      s->max_new = max_new;
+      s->eos_id = eos_id;
+      s->len.assign(lens, lens + N);
+      s->generated.assign(N, 0);
+      s->active.assign(N, 1);
+      s->active_order.resize(N);
+      for (int32_t i = 0; i < N; ++i) s->active_order[i] = i;
+      if (sort_by_length)
+        std::stable_sort(s->active_order.begin(), s->active_order.end(),
+                         [s](int32_t a, int32_t b) { return s->len[a] < s->len[b]; });
+    } catch (...) {
+      delete s;
+      throw;
+    }
+    *out = s;
+    return sched_ok();
+  });
 }
 
 void specdec_sched_destroy(specdec_sched_t* s) { delete s; }
@@ -132,7 +147,11 @@ specdec_status_t specdec_sched_next_batch(specdec_sched_t* s, int32_t* slots, in
                                           specdec_batch_info_t* info) {
   if (!s || !slots || !info) return sched_fail(SPECDEC_ERR_INVALID_ARGUMENT, "NULL scheduler / slots / info");
   if (!s->has_cur) {
-    choose(s);
+    const specdec_status_t st = guarded([&] {
+      choose(s);
+      return SPECDEC_OK;
+    });
+    if (st) return st;
     s->has_cur = s->cur_info.B > 0;
   }
   *info = s->cur_info;
@@ -174,7 +193,17 @@ specdec_status_t specdec_sched_commit(specdec_sched_t* s, const int32_t* n_acc, 
                                          [s](int32_t q) { return !s->active[q]; }),
                           s->active_order.end());
   s->has_prev = uniform;
-  if (uniform) s->prev = s->cur;
+  if (uniform) {
+    const specdec_status_t st = guarded([&] {
+      s->prev = s->cur;
+      return SPECDEC_OK;
+    });
+    if (st) {
+      s->has_prev = false;
+      s->has_cur = false;
+      return st;
+    }
+  }
   s->has_cur = false;
   return sched_ok();
 }

@@ -50,9 +50,10 @@ class _Job:
                                      s_in=self.s_in, s_out=self.s_out, pad_id=PAD_ID, stream=self.stream)
                 self.stream.synchronize()
                 w = int(b.w_new.cpu()[0])
+                width = w + W.k + 1                # the columns the step writes
                 self.results.append(dict(tokens=b.tokens.cpu().numpy(), n_acc=b.n_acc.cpu().numpy(),
-                                         pad_out=b.pad_out.cpu().numpy(), w=w, pos=b.pos.cpu().numpy(),
-                                         mask=b.mask.cpu().numpy(), kv=bits(self.dst[..., :w, :]),
+                                         pad_out=b.pad_out.cpu().numpy(), w=w, pos=b.pos.cpu().numpy()[:, :width],
+                                         mask=b.mask.cpu().numpy()[:, :width], kv=bits(self.dst[..., :w, :]),
                                          s=self.s_out.cpu().numpy()[:, :w + 1], status=int(b.dev_status.cpu()[0])))
             # a call that fails validation: the error text is this thread's own
             rc = self.sd.lib.specdec_build_posmask(None, None, W.B, W.k, None, None, self.tag, None, None)
