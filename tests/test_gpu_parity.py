@@ -129,6 +129,20 @@ def test_draft_cache_realigned_with_the_target_offsets(variant):
     assert np.array_equal(got[..., :W, :], exp[..., :W, :])
 
 
+@pytest.mark.parametrize("variant,items", [("oop", 64 * 600), ("inplace", 256 * 30)])
+def test_realign_split_over_launches(monkeypatch, variant, items):
+    """The realignment (with pos/mask and the token row) split over many
+    launches when one launch may hold only `items` work-items: a few spans
+    per launch, so the in-place kernel's XCD rotation maps workgroups of one
+    launch onto spans of others; still every span is moved once."""
+    monkeypatch.setenv("SPECDEC_MAX_LAUNCH_ITEMS", str(items))
+    try:
+        for seed in (0, 5):
+            _full_check(run_gpu(SMALL["vicuna7b_small"], seed=seed, variant=variant, tokens=variant))
+    finally:
+        monkeypatch.delenv("SPECDEC_MAX_LAUNCH_ITEMS", raising=False)
+
+
 def test_uniform_acceptance_in_place_touches_nothing():
     """Corollary B.4: every offset is zero, so the in-place step writes no KV byte."""
     w = EDGE["uniform_accept"].scaled(extra_cap=9)
