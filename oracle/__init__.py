@@ -42,6 +42,8 @@ class Oracle:
     """ctypes handle on one build of the oracle library (tests load mutant builds too)."""
 
     def __init__(self, path: Path | str | None = None):
+        if path is None and os.environ.get("SPECDEC_ORACLE_LIB"):
+            path = os.environ["SPECDEC_ORACLE_LIB"]      # another build, e.g. with sanitizers
         if path is None:
             if not _LIB_PATH.exists():
                 build(force=False)

@@ -8,11 +8,14 @@ it has not been built; there is no fallback.
 from __future__ import annotations
 
 import ctypes
+import os
 from pathlib import Path
 
 import torch
 
-_LIB_PATH = Path(__file__).resolve().parent / "libspecdec.so"
+# SPECDEC_LIB selects another build of the library (for instance one with a
+# host-side sanitizer); the default is the in-tree build.
+_LIB_PATH = Path(os.environ.get("SPECDEC_LIB") or Path(__file__).resolve().parent / "libspecdec.so")
 
 OK, ERR_INVALID_ARGUMENT, ERR_UNSUPPORTED, ERR_HIP, ERR_WORKSPACE = 0, 1, 2, 3, 4
 F32, BF16, F16 = 0, 1, 2
