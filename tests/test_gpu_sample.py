@@ -95,8 +95,15 @@ def _row(v, i):
 
 
 def check_against_oracle(tl, dl, dtype, draft, pad, ua, us, T, W_in, got):
-    """Exact agreement, or agreement with the oracle at an edge of the fp32
-    band; returns the number of rows that needed the band."""
+    """Exact agreement, or agreement with the oracle somewhere in the fp32
+    band; returns the number of rows that needed the band.
+
+    The accept tests are decided on u_accept, which the band moves by
+    a relative delta_a; the drawn token is the inversion of u_sample, which
+    it moves by delta_s / m (m = the mass of the weights sampled from).  For
+    a fixed accept outcome the token is non-decreasing in u_sample, so every
+    token between the oracle's draws at the two ends of the band is one that
+    some u_sample in the band produces."""
     B, kp1, V = tl.shape
     k = kp1 - 1
     args = (tl, dl, dtype, draft, pad)
@@ -111,21 +118,29 @@ def check_against_oracle(tl, dl, dtype, draft, pad, ua, us, T, W_in, got):
         if _row(got, i) == _row(nom, i):
             continue
         if edges is None:
-            edges = []
+            j = nom["n_acc"]
+            mass = np.ones(B)
+            rej = j < k
+            if k:
+                r = np.minimum(j, k - 1)
+                mass[rej] = np.maximum(p[np.arange(B), r] - q[np.arange(B), r], 0).sum(-1)[rej]
+            ds = DS / np.maximum(mass, 1e-3)
+            edges = {}
             for sa in (-1, 0, 1):
+                ua2 = np.clip(ua * (1 + sa * DA), 0, np.float32(0.99999994)).astype(np.float32)
                 for ss in (-1, 0, 1):
-                    j = nom["n_acc"]
-                    mass = np.ones(B)
-                    rej = j < k
-                    if k:
-                        r = np.minimum(j, k - 1)
-                        mass[rej] = np.maximum(p[np.arange(B), r] - q[np.arange(B), r], 0).sum(-1)[rej]
-                    ds = DS / np.maximum(mass, 1e-3)
-                    ua2 = np.clip(ua * (1 + sa * DA), 0, np.float32(0.99999994)).astype(np.float32)
                     us2 = np.clip(us + ss * ds, 0, np.float32(0.99999994)).astype(np.float32)
-                    edges.append(oracle.verify_sample(*args, ua2, us2, T, W_in))
-        assert any(_row(got, i) == _row(e, i) for e in edges), \
-            f"row {i}: GPU {_row(got, i)} vs oracle {_row(nom, i)} (outside the fp32 band)"
+                    edges[sa, ss] = oracle.verify_sample(*args, ua2, us2, T, W_in)
+        n_got, toks = _row(got, i)
+        ok = False
+        for sa in (-1, 0, 1):
+            lo, hi = _row(edges[sa, -1], i), _row(edges[sa, 1], i)
+            if lo[0] != n_got or lo[1][:n_got] != toks[:n_got]:
+                continue
+            ok = lo[1][n_got] <= toks[n_got] <= hi[1][n_got]
+            if ok:
+                break
+        assert ok, f"row {i}: GPU {(n_got, toks)} vs oracle {_row(nom, i)} (outside the fp32 band)"
         banded += 1
     # geometry follows from the accepted counts exactly
     checker.check_geometry(pad, got["n_acc"], got["pad_out"], got["w_new"], W_in, k)
