@@ -177,6 +177,35 @@ def test_special_logit_values():
         assert r.out["tokens"][0, 0] == 5 and r.out["tokens"][1, 0] == 0 and r.out["tokens"][2, 0] == 10
 
 
+@pytest.mark.parametrize("dt", ["bf16", "f16"])
+def test_nan_bit_patterns_16bit(dt):
+    """16-bit NaNs of either sign and any payload rank above every number and
+    the first one wins, inside 16-byte vectors and in unaligned heads / tails
+    (rows of 1001 logits); a row whose only NaN is negative, and a row of
+    -inf with one negative NaN."""
+    V = 1001
+    w = _small("tiny", B=6, k=2, V=V, W_in=None, prompt=("uniform", 2, 9)).scaled(logit_dtype=dt)
+    neg = [0xFF81, 0xFFC0, 0xFFFF] if dt == "bf16" else [0xFC01, 0xFE00, 0xFFFF]
+    pos = [0x7F81, 0x7FC0, 0x7FFF] if dt == "bf16" else [0x7C01, 0x7E00, 0x7FFF]
+    x = (torch.randn((w.B, w.k + 1, V)) * 0.5).to(wl.TORCH_DT[dt]).view(torch.int16)
+    def put(i, r, j, bits):
+        x[i, r, j] = bits - 65536 if bits >= 32768 else bits
+    put(0, 0, 500, neg[0]); put(0, 0, 700, pos[1])          # negative first: index 500
+    put(0, 1, 3, neg[1])                                     # only NaN, in a row's head
+    put(0, 2, V - 1, neg[2]); put(0, 2, 998, pos[0])         # the positive one comes first
+    for j, b in zip((100, 101, 102), neg):                  # a run of payloads in one vector
+        put(1, 0, j, b)
+    x[1, 1] = torch.tensor(0xFF80 if dt == "bf16" else 0xFC00, dtype=torch.int32).to(torch.int16)  # -inf row
+    put(1, 1, 640, neg[0])
+    put(2, 0, 0, neg[2])                                     # at index 0
+    logits = x.view(wl.TORCH_DT[dt]).cuda()
+    draft = torch.randint(0, V, (w.B, w.k), dtype=torch.int32)
+    r = run_gpu(w, logits=logits, draft=draft.cuda())
+    _full_check(r)
+    t = r.out["tokens"]
+    assert (t[0, 0], t[0, 1], t[0, 2], t[1, 0], t[1, 1], t[2, 0]) == (500, 3, 998, 100, 640, 0)
+
+
 def test_unaligned_logits_pointer():
     w = _small("gqa8b", B=3, V=997, L=1, H=1, D=8, prompt=("uniform", 1, 30))
     logits, draft, *_ = wl.logits_and_drafts(w, 0, 0, device="cuda")
