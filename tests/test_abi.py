@@ -367,3 +367,18 @@ def test_varlen_rollback_rejects(sd):
     assert call(pos=A + (1 << 30) + 256) == 1                              # positions inside the dst cache
     assert call(src=_vdesc(sd, data=A + 8), dst=_vdesc(sd, data=A + (1 << 30))) == 2
     assert call(B=0, cu_in=None, n_acc=None, cu_out=None) == 0
+
+
+def test_missing_library_fails_loudly(tmp_path):
+    """With no built library the binding refuses to import (no fallback path),
+    and so do the smoke check and the benchmark, which go through it."""
+    import os
+    import subprocess
+    import sys
+    env = dict(os.environ, SPECDEC_LIB=str(tmp_path / "libspecdec.so"))
+    for code in ("from paper_2510_22876_amd import specdec",
+                 "import __graft_entry__ as g; g.smoke()"):
+        r = subprocess.run([sys.executable, "-c", code], cwd=ROOT, env=env, capture_output=True, text=True,
+                           timeout=300)
+        assert r.returncode != 0, code
+        assert "is not built" in r.stderr, r.stderr[-2000:]
