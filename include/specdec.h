@@ -27,6 +27,10 @@
  *   row whose values are out of range is left untouched and a bit is set in
  *   the optional `dev_status` word (device uint32, may be NULL; bits are
  *   OR-ed in and never cleared by the library).
+ * - No output (a destination cache or token row and the `dev_status` word
+ *   included) may overlap an input or another output; inputs may overlap
+ *   each other.  A cache or token row realigned in place is one buffer, read
+ *   and written by the same call.  An overlap is SPECDEC_ERR_INVALID_ARGUMENT.
  *
  * Terms: B rows, k draft tokens per row, V vocabulary entries.  W_in is the
  * width of the cache handed to the step, counted in cache columns and
@@ -203,7 +207,8 @@ specdec_status_t specdec_verify_sample(const void* logits, const void* draft_log
  *             not rewritten); it moves only rows whose padding changes.
  *             Otherwise the two caches must not overlap.
  *   pad_in, n_acc  int32 [B] (device); w_new int32 [1] (device): the outputs
- *             of specdec_verify_greedy for this step.
+ *             of specdec_verify_greedy for this step; none of them may lie
+ *             inside dst.
  */
 specdec_status_t specdec_realign_kv(const specdec_kv_t* src, const specdec_kv_t* dst, int32_t k,
                                     int32_t W_in, const int32_t* pad_in, const int32_t* n_acc,
@@ -222,7 +227,7 @@ specdec_status_t specdec_realign_kv(const specdec_kv_t* src, const specdec_kv_t*
  *   pm_cap    row stride of pos and mask; must be >= w_new + k + 1 (checked on
  *             the device; rows that do not fit are skipped and flagged).
  * pos and mask must not overlap each other, pad_out or w_new (nor, in
- * specdec_step, pad_in or n_acc).
+ * specdec_step, any other buffer of the step).
  */
 specdec_status_t specdec_build_posmask(const int32_t* pad_out, const int32_t* w_new, int32_t B,
                                        int32_t k, int64_t* pos, uint8_t* mask, int64_t pm_cap,
@@ -245,7 +250,8 @@ specdec_status_t specdec_build_posmask(const int32_t* pad_out, const int32_t* w_
  *             [0, pad_in[i]) need not hold pad_id); otherwise the two must not
  *             overlap.
  *   tokens    int32 [B][k+1], pad_in, n_acc int32 [B], w_new int32 [1]: the
- *             outputs of specdec_verify_greedy for this step.
+ *             outputs of specdec_verify_greedy for this step; none of them
+ *             may lie inside s_out.
  */
 specdec_status_t specdec_realign_tokens(const int32_t* s_in, int64_t s_in_stride, int32_t* s_out,
                                         int64_t s_out_stride, const int32_t* tokens,
@@ -257,8 +263,12 @@ specdec_status_t specdec_realign_tokens(const int32_t* s_in, int64_t s_in_stride
  * The whole step on one stream: specdec_verify_greedy, then one fused launch
  * of the cache realignment, the position ids / mask and (when s_in is not
  * NULL) the token row realignment.  Arguments as above; pm_cap must be
- * >= W_in + k + 1.  If `w_new_host` (host int32*) is not NULL, the stream is
- * synchronised and L' is copied there.
+ * >= W_in + k + 1.  Every output (tokens, n_acc, bonus, pad_out, w_new, the
+ * workspace, pos, mask, dst, s_out, dev_status) stands apart from every
+ * input (logits, draft, pad_in, src, s_in) and from the other outputs,
+ * except that dst may be src and s_out may be s_in (in place).  If
+ * `w_new_host` (host int32*) is not NULL, the stream is synchronised and L'
+ * is copied there.
  */
 specdec_status_t specdec_step(const void* logits, int32_t dtype, const int32_t* draft,
                               const int32_t* pad_in, int32_t B, int32_t k, int32_t V,

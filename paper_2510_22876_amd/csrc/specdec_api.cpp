@@ -5,6 +5,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cmath>
+#include <cstdint>
 #include <cstdarg>
 #include <cstdio>
 #include <initializer_list>
@@ -151,27 +152,36 @@ struct Region {
 };
 
 // Every output region must be disjoint from every input region and from the
-// other outputs (NULL or empty regions are skipped).
-specdec_status_t check_disjoint(std::initializer_list<Region> inputs, std::initializer_list<Region> outputs) {
+// other outputs (NULL or empty regions are skipped; inputs may overlap each
+// other).  A buffer updated in place is listed once, as an output.
+specdec_status_t check_disjoint(const Region* in, size_t nin, const Region* out, size_t nout) {
   auto meet = [](const Region& a, const Region& b) {
     if (!a.p || !b.p || a.bytes <= 0 || b.bytes <= 0) return false;
     const uintptr_t a0 = reinterpret_cast<uintptr_t>(a.p), b0 = reinterpret_cast<uintptr_t>(b.p);
     return a0 < b0 + static_cast<uintptr_t>(b.bytes) && b0 < a0 + static_cast<uintptr_t>(a.bytes);
   };
-  for (auto o = outputs.begin(); o != outputs.end(); ++o) {
-    for (const Region& i : inputs)
-      if (meet(*o, i)) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "output %s overlaps input %s", o->name, i.name);
-    for (auto o2 = outputs.begin(); o2 != o; ++o2)
-      if (meet(*o, *o2)) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "outputs %s and %s overlap", o2->name, o->name);
+  for (size_t o = 0; o < nout; ++o) {
+    for (size_t i = 0; i < nin; ++i)
+      if (meet(out[o], in[i]))
+        return fail(SPECDEC_ERR_INVALID_ARGUMENT, "output %s overlaps input %s", out[o].name, in[i].name);
+    for (size_t o2 = 0; o2 < o; ++o2)
+      if (meet(out[o], out[o2]))
+        return fail(SPECDEC_ERR_INVALID_ARGUMENT, "outputs %s and %s overlap", out[o2].name, out[o].name);
   }
   return SPECDEC_OK;
 }
+
+specdec_status_t check_disjoint(std::initializer_list<Region> inputs, std::initializer_list<Region> outputs) {
+  return check_disjoint(inputs.begin(), inputs.size(), outputs.begin(), outputs.size());
+}
+
+int64_t clamp_bytes(size_t n) { return n > static_cast<size_t>(INT64_MAX) ? INT64_MAX : static_cast<int64_t>(n); }
 
 specdec_status_t check_verify_args(const void* logits, int32_t dtype, const int32_t* draft,
                                    const int32_t* pad_in, int32_t B, int32_t k, int32_t V, int32_t W_in,
                                    const int32_t* tokens, const int32_t* n_acc, const int32_t* bonus,
                                    const int32_t* pad_out, const int32_t* w_new, const void* workspace,
-                                   size_t workspace_bytes) {
+                                   size_t workspace_bytes, const uint32_t* dev_status) {
   if (B < 0 || B > SPECDEC_MAX_B) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "B=%d outside [0,%d]", B, SPECDEC_MAX_B);
   if (k < 0 || k > SPECDEC_MAX_K) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "k=%d outside [0,%d]", k, SPECDEC_MAX_K);
   if (V < 1) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "V=%d must be >= 1", V);
@@ -188,12 +198,14 @@ specdec_status_t check_verify_args(const void* logits, int32_t dtype, const int3
   const void* i32s[] = {draft, pad_in, tokens, n_acc, bonus, pad_out, w_new};
   for (const void* p : i32s)
     if (p && !aligned(p, 4)) return fail(SPECDEC_ERR_UNSUPPORTED, "int32 tensor not 4-byte aligned");
+  if (dev_status && !aligned(dev_status, 4)) return fail(SPECDEC_ERR_UNSUPPORTED, "dev_status not 4-byte aligned");
   {
     const int64_t b4 = 4 * static_cast<int64_t>(B);
     specdec_status_t d = check_disjoint(
         {{logits, rows * V * eb, "logits"}, {draft, b4 * k, "draft"}, {pad_in, b4, "pad_in"}},
         {{tokens, b4 * (k + 1), "tokens"}, {n_acc, b4, "n_acc"}, {bonus, b4, "bonus"}, {pad_out, b4, "pad_out"},
-         {w_new, 4, "w_new"}, {workspace, static_cast<int64_t>(workspace_bytes), "workspace"}});
+         {w_new, 4, "w_new"}, {workspace, clamp_bytes(workspace_bytes), "workspace"},
+         {dev_status, 4, "dev_status"}});
     if (d) return d;
   }
   const int64_t chunk = specdec::verify_chunk_elems(rows, V);
@@ -278,7 +290,8 @@ specdec_status_t check_token_args(const int32_t* s_in, int64_t s_in_stride, cons
 }
 
 specdec_status_t check_posmask_args(const int32_t* pad_out, const int32_t* w_new, int32_t B, int32_t k,
-                                    const int64_t* pos, const uint8_t* mask, int64_t pm_cap) {
+                                    const int64_t* pos, const uint8_t* mask, int64_t pm_cap,
+                                    const uint32_t* dev_status) {
   if (B < 0 || B > SPECDEC_MAX_B) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "B=%d outside [0,%d]", B, SPECDEC_MAX_B);
   if (k < 0 || k > SPECDEC_MAX_K) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "k=%d outside [0,%d]", k, SPECDEC_MAX_K);
   if (pm_cap < k + 1 || pm_cap > SPECDEC_MAX_WIDTH + SPECDEC_MAX_K + 1)
@@ -287,9 +300,10 @@ specdec_status_t check_posmask_args(const int32_t* pad_out, const int32_t* w_new
   if (!pad_out || !w_new || !pos || !mask) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "NULL pad_out / w_new / pos / mask");
   if (!aligned(pos, 8)) return fail(SPECDEC_ERR_UNSUPPORTED, "pos not 8-byte aligned");
   if (!aligned(pad_out, 4) || !aligned(w_new, 4)) return fail(SPECDEC_ERR_UNSUPPORTED, "int32 tensor not 4-byte aligned");
+  if (dev_status && !aligned(dev_status, 4)) return fail(SPECDEC_ERR_UNSUPPORTED, "dev_status not 4-byte aligned");
   const int64_t n = static_cast<int64_t>(B) * pm_cap;
   return check_disjoint({{pad_out, 4 * static_cast<int64_t>(B), "pad_out"}, {w_new, 4, "w_new"}},
-                        {{pos, 8 * n, "pos"}, {mask, n, "mask"}});
+                        {{pos, 8 * n, "pos"}, {mask, n, "mask"}, {dev_status, 4, "dev_status"}});
 }
 
 
@@ -331,7 +345,8 @@ specdec_status_t check_sample_args(const void* logits, const void* draft_logits,
         {{logits, lb * (k + 1), "logits"}, {draft_logits, lb * k, "draft_logits"}, {draft, b4 * k, "draft"},
          {pad_in, b4, "pad_in"}, {u_accept, b4 * k, "u_accept"}, {u_sample, b4, "u_sample"}},
         {{tokens, b4 * (k + 1), "tokens"}, {n_acc, b4, "n_acc"}, {bonus, b4, "bonus"}, {pad_out, b4, "pad_out"},
-         {w_new, 4, "w_new"}, {workspace, static_cast<int64_t>(workspace_bytes), "workspace"}});
+         {w_new, 4, "w_new"}, {workspace, clamp_bytes(workspace_bytes), "workspace"},
+         {dev_status, 4, "dev_status"}});
     if (d) return d;
   }
   const int64_t blocks = rows * specdec::sample_chunks(rows, V);
@@ -353,10 +368,7 @@ specdec_status_t check_step_rest(int32_t B, int32_t k, int32_t W_in, const specd
   specdec_status_t s = check_realign_args(src, dst, k, W_in, pad_in, n_acc, w_new, in_place);
   if (s) return s;
   if (src->B != B) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "cache rows B=%d differ from logits rows B=%d", src->B, B);
-  s = check_posmask_args(pad_out, w_new, B, k, pos, mask, pm_cap);
-  if (s) return s;
-  s = check_disjoint({{pad_in, 4 * static_cast<int64_t>(B), "pad_in"}, {n_acc, 4 * static_cast<int64_t>(B), "n_acc"}},
-                     {{pos, 8 * static_cast<int64_t>(B) * pm_cap, "pos"}, {mask, static_cast<int64_t>(B) * pm_cap, "mask"}});
+  s = check_posmask_args(pad_out, w_new, B, k, pos, mask, pm_cap, dev_status);
   if (s) return s;
   if (B > 0 && pm_cap < static_cast<int64_t>(W_in) + k + 1)
     return fail(SPECDEC_ERR_INVALID_ARGUMENT, "pm_cap=%lld < W_in+k+1=%d", (long long)pm_cap, W_in + k + 1);
@@ -366,6 +378,52 @@ specdec_status_t check_step_rest(int32_t B, int32_t k, int32_t W_in, const specd
   }
   if (dev_status && !aligned(dev_status, 4)) return fail(SPECDEC_ERR_UNSUPPORTED, "dev_status not 4-byte aligned");
   return SPECDEC_OK;
+}
+
+// Every buffer of a fused step against every output: the verification inputs,
+// the source cache and token row, then the verification outputs, workspace,
+// position ids / mask, destination cache and token row and the status word.
+// A cache or token row realigned in place is listed once, as an output.
+struct StepInputs {
+  const void* logits;
+  int64_t logit_bytes;            // target logits [B][k+1][V]
+  const void* draft_logits;       // [B][k][V] (stochastic verification) or NULL
+  int64_t draft_logit_bytes;
+  const int32_t* draft;
+  const int32_t* pad_in;
+  const float* u_accept;          // [B][k] or NULL
+  const float* u_sample;          // [B] or NULL
+};
+
+specdec_status_t check_step_disjoint(const StepInputs& v, int32_t B, int32_t k, const specdec_kv_t* src,
+                                     const specdec_kv_t* dst, bool in_place, const int32_t* tokens,
+                                     const int32_t* n_acc, const int32_t* bonus, const int32_t* pad_out,
+                                     const int32_t* w_new, const void* workspace, size_t workspace_bytes,
+                                     const int64_t* pos, const uint8_t* mask, int64_t pm_cap, const int32_t* s_in,
+                                     int64_t s_in_stride, const int32_t* s_out, int64_t s_out_stride,
+                                     const uint32_t* dev_status) {
+  const int64_t b4 = 4 * static_cast<int64_t>(B), pm = static_cast<int64_t>(B) * pm_cap;
+  const bool tok_in_place = s_in == s_out;
+  const Region in[] = {{v.logits, v.logit_bytes, "logits"},
+                       {v.draft_logits, v.draft_logit_bytes, "draft_logits"},
+                       {v.draft, b4 * k, "draft"},
+                       {v.pad_in, b4, "pad_in"},
+                       {v.u_accept, b4 * k, "u_accept"},
+                       {v.u_sample, b4, "u_sample"},
+                       {in_place ? nullptr : src->data, kv_bytes(src), "src cache"},
+                       {tok_in_place ? nullptr : s_in, s_in ? b4 * s_in_stride : 0, "s_in"}};
+  const Region out[] = {{tokens, b4 * (k + 1), "tokens"},
+                        {n_acc, b4, "n_acc"},
+                        {bonus, b4, "bonus"},
+                        {pad_out, b4, "pad_out"},
+                        {w_new, 4, "w_new"},
+                        {workspace, clamp_bytes(workspace_bytes), "workspace"},
+                        {pos, 8 * pm, "pos"},
+                        {mask, pm, "mask"},
+                        {dst->data, kv_bytes(dst), "dst cache"},
+                        {s_out, s_out ? b4 * s_out_stride : 0, "s_out"},
+                        {dev_status, 4, "dev_status"}};
+  return check_disjoint(in, sizeof(in) / sizeof(in[0]), out, sizeof(out) / sizeof(out[0]));
 }
 
 // The realignment launch of a fused step (cache, position ids / mask, token
@@ -481,10 +539,9 @@ specdec_status_t specdec_verify_greedy(const void* logits, int32_t dtype, const 
                                        int32_t* w_new, void* workspace, size_t workspace_bytes,
                                        uint32_t* dev_status, void* stream) {
   specdec_status_t s = check_verify_args(logits, dtype, draft, pad_in, B, k, V, W_in, tokens, n_acc, bonus,
-                                         pad_out, w_new, workspace, workspace_bytes);
+                                         pad_out, w_new, workspace, workspace_bytes, dev_status);
   if (s) return s;
   if (B == 0) return ok();
-  if (dev_status && !aligned(dev_status, 4)) return fail(SPECDEC_ERR_UNSUPPORTED, "dev_status not 4-byte aligned");
   specdec::VerifyLaunch p{logits, dtype, draft, pad_in, B, k, V, W_in, tokens, n_acc,
                           bonus, pad_out, w_new, workspace, dev_status};
   hipStream_t st = static_cast<hipStream_t>(stream);
@@ -533,6 +590,13 @@ specdec_status_t specdec_realign_kv(const specdec_kv_t* src, const specdec_kv_t*
   if (s) return s;
   if (static_cast<int64_t>(src->L) * src->B * src->H == 0) return ok();
   if (dev_status && !aligned(dev_status, 4)) return fail(SPECDEC_ERR_UNSUPPORTED, "dev_status not 4-byte aligned");
+  {
+    const int64_t b4 = 4 * static_cast<int64_t>(src->B);
+    s = check_disjoint({{pad_in, b4, "pad_in"}, {n_acc, b4, "n_acc"}, {w_new, 4, "w_new"},
+                        {in_place ? nullptr : src->data, kv_bytes(src), "src cache"}},
+                       {{dst->data, kv_bytes(dst), "dst cache"}, {dev_status, 4, "dev_status"}});
+    if (s) return s;
+  }
   specdec::RealignLaunch p{};
   p.src = src->data;
   p.dst = dst->data;
@@ -558,10 +622,9 @@ specdec_status_t specdec_realign_kv(const specdec_kv_t* src, const specdec_kv_t*
 specdec_status_t specdec_build_posmask(const int32_t* pad_out, const int32_t* w_new, int32_t B, int32_t k,
                                        int64_t* pos, uint8_t* mask, int64_t pm_cap, uint32_t* dev_status,
                                        void* stream) {
-  specdec_status_t s = check_posmask_args(pad_out, w_new, B, k, pos, mask, pm_cap);
+  specdec_status_t s = check_posmask_args(pad_out, w_new, B, k, pos, mask, pm_cap, dev_status);
   if (s) return s;
   if (B == 0) return ok();
-  if (dev_status && !aligned(dev_status, 4)) return fail(SPECDEC_ERR_UNSUPPORTED, "dev_status not 4-byte aligned");
   specdec::PosmaskLaunch p{pad_out, w_new, B, k, pos, mask, pm_cap, pm_cap, dev_status};
   hipStream_t st = static_cast<hipStream_t>(stream);
   hipError_t e = timed(SPECDEC_KERNEL_POSMASK, st, [&] { return specdec::launch_posmask(p, st); });
@@ -584,6 +647,13 @@ specdec_status_t specdec_realign_tokens(const int32_t* s_in, int64_t s_in_stride
   if (!aligned(tokens, 4) || !aligned(pad_in, 4) || !aligned(n_acc, 4) || !aligned(w_new, 4))
     return fail(SPECDEC_ERR_UNSUPPORTED, "int32 tensor not 4-byte aligned");
   if (dev_status && !aligned(dev_status, 4)) return fail(SPECDEC_ERR_UNSUPPORTED, "dev_status not 4-byte aligned");
+  {
+    const int64_t b4 = 4 * static_cast<int64_t>(B);
+    s = check_disjoint({{tokens, b4 * (k + 1), "tokens"}, {pad_in, b4, "pad_in"}, {n_acc, b4, "n_acc"},
+                        {w_new, 4, "w_new"}, {s_in == s_out ? nullptr : s_in, b4 * s_in_stride, "s_in"}},
+                       {{s_out, b4 * s_out_stride, "s_out"}, {dev_status, 4, "dev_status"}});
+    if (s) return s;
+  }
   specdec::RealignLaunch p{};
   p.B = B;
   p.k = k;
@@ -612,12 +682,19 @@ specdec_status_t specdec_step(const void* logits, int32_t dtype, const int32_t* 
                               int32_t pad_id, void* workspace, size_t workspace_bytes, uint32_t* dev_status,
                               int32_t* w_new_host, void* stream) {
   specdec_status_t s = check_verify_args(logits, dtype, draft, pad_in, B, k, V, W_in, tokens, n_acc, bonus,
-                                         pad_out, w_new, workspace, workspace_bytes);
+                                         pad_out, w_new, workspace, workspace_bytes, dev_status);
   if (s) return s;
   bool in_place = false;
   s = check_step_rest(B, k, W_in, src, dst, pad_in, n_acc, pad_out, w_new, pos, mask, pm_cap, s_in, s_in_stride, s_out,
                       s_out_stride, dev_status, &in_place);
   if (s) return s;
+  {
+    const StepInputs v{logits, static_cast<int64_t>(B) * (k + 1) * V * logit_bytes(dtype), nullptr, 0, draft, pad_in,
+                       nullptr, nullptr};
+    s = check_step_disjoint(v, B, k, src, dst, in_place, tokens, n_acc, bonus, pad_out, w_new, workspace,
+                            workspace_bytes, pos, mask, pm_cap, s_in, s_in_stride, s_out, s_out_stride, dev_status);
+    if (s) return s;
+  }
   if (B == 0) return ok();
   hipStream_t st = static_cast<hipStream_t>(stream);
   specdec::VerifyLaunch vp{logits, dtype, draft, pad_in, B, k, V, W_in, tokens, n_acc,
@@ -647,6 +724,13 @@ specdec_status_t specdec_step_sample(const void* logits, const void* draft_logit
   s = check_step_rest(B, k, W_in, src, dst, pad_in, n_acc, pad_out, w_new, pos, mask, pm_cap, s_in, s_in_stride, s_out,
                       s_out_stride, dev_status, &in_place);
   if (s) return s;
+  {
+    const int64_t lb = static_cast<int64_t>(B) * V * logit_bytes(dtype);
+    const StepInputs v{logits, lb * (k + 1), draft_logits, lb * k, draft, pad_in, u_accept, u_sample};
+    s = check_step_disjoint(v, B, k, src, dst, in_place, tokens, n_acc, bonus, pad_out, w_new, workspace,
+                            workspace_bytes, pos, mask, pm_cap, s_in, s_in_stride, s_out, s_out_stride, dev_status);
+    if (s) return s;
+  }
   if (B == 0) return ok();
   hipStream_t st = static_cast<hipStream_t>(stream);
   specdec::SampleLaunch sp{logits, draft_logits, dtype, draft, pad_in, u_accept, u_sample, c,
@@ -691,7 +775,7 @@ specdec_status_t specdec_gather_batch(const specdec_kv_t* pool, const int32_t* p
                         {lens, 4 * static_cast<int64_t>(pool->B), "lens"}, {slots, b4, "slots"}},
                        {{batch->data, kv_bytes(batch), "batch"},
                         {batch_tok, batch_tok ? static_cast<int64_t>(B) * btok_stride * 4 : 0, "batch_tok"},
-                        {pads, b4, "pads"}, {pos, 8 * n, "pos"}, {mask, n, "mask"}});
+                        {pads, b4, "pads"}, {pos, 8 * n, "pos"}, {mask, n, "mask"}, {dev_status, 4, "dev_status"}});
     if (s) return s;
   }
   specdec::GatherLaunch p{};
@@ -755,7 +839,8 @@ specdec_status_t specdec_scatter_accepted(const specdec_kv_t* batch, const int32
                        {{pool->data, kv_bytes(pool), "pool"},
                         {pool_tok, static_cast<int64_t>(pool->B) * pool_tok_stride * 4, "pool_tok"},
                         {lens, 4 * static_cast<int64_t>(pool->B), "lens"},
-                        {batch_tok, batch_tok ? static_cast<int64_t>(B) * btok_stride * 4 : 0, "batch_tok"}});
+                        {batch_tok, batch_tok ? static_cast<int64_t>(B) * btok_stride * 4 : 0, "batch_tok"},
+                        {dev_status, 4, "dev_status"}});
     if (s) return s;
   }
   specdec::WritebackLaunch p{};
@@ -809,6 +894,15 @@ specdec_status_t specdec_rollback(const int32_t* tokens, const int32_t* n_acc_in
       (pad_out != pad_in && ranges_overlap(pad_out, b4, pad_in, b4)) ||
       ranges_overlap(n_acc_out, b4, pad_in, b4) || ranges_overlap(pad_out, b4, n_acc_in, b4))
     return fail(SPECDEC_ERR_INVALID_ARGUMENT, "outputs overlap the inputs other than in place");
+  {
+    // n_acc and the paddings may be updated in place; the width and the
+    // status word must stand apart from everything
+    const specdec_status_t s = check_disjoint(
+        {{tokens, b4 * (k + 1), "tokens"}, {n_acc_in, b4, "n_acc_in"}, {pad_in, b4, "pad_in"},
+         {n_acc_out, b4, "n_acc_out"}, {bonus_out, b4, "bonus_out"}, {pad_out, b4, "pad_out"}},
+        {{w_new, 4, "w_new"}, {dev_status, 4, "dev_status"}});
+    if (s) return s;
+  }
   specdec::RollbackLaunch p{tokens, n_acc_in, pad_in, B, k, W_in, n_acc_out, bonus_out, pad_out, w_new, dev_status};
   hipError_t e = specdec::launch_rollback(p, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "rollback launch");
@@ -851,7 +945,8 @@ specdec_status_t specdec_varlen_rollback(const specdec_varlen_t* src, const spec
     const bool data = src->L > 0 && src->T_cap > 0;
     specdec_status_t s = check_disjoint(
         {{cu_in, c4, "cu_in"}, {n_acc, 4 * static_cast<int64_t>(B), "n_acc"}, {data ? src->data : nullptr, bytes_src, "src"}},
-        {{cu_out, c4, "cu_out"}, {pos, pos ? 8 * pos_cap : 0, "pos"}, {data ? dst->data : nullptr, bytes_dst, "dst"}});
+        {{cu_out, c4, "cu_out"}, {pos, pos ? 8 * pos_cap : 0, "pos"}, {data ? dst->data : nullptr, bytes_dst, "dst"},
+         {dev_status, 4, "dev_status"}});
     if (s) return s;
   }
   if (static_cast<int64_t>(src->L) * 2 * B > 0xFFFFFFFFLL) return fail(SPECDEC_ERR_INVALID_ARGUMENT, "too many spans");

@@ -369,6 +369,66 @@ def test_varlen_rollback_rejects(sd):
     assert call(B=0, cu_in=None, n_acc=None, cu_out=None) == 0
 
 
+def _overlap(sd, rc):
+    assert rc == 1 and "overlap" in sd.lib.specdec_last_error().decode(), sd.lib.specdec_last_error().decode()
+
+
+def test_every_output_stands_apart(sd):
+    """Caches, token rows and the status word are outputs like the others: an
+    output over any input or over another output is refused before anything
+    is enqueued.  (An in-place cache or token row counts once, as an output:
+    the GPU tests run those cases.)"""
+    _no_gpu()
+    CACHE = A + (1 << 30)                    # the dst cache spans 32 KiB from here
+    S_IN, S_OUT = A + (2 << 30), A + (3 << 30)
+    _overlap(sd, _verify(sd, status=TK))  # status word over tokens
+    _overlap(sd, _verify(sd, status=WS + 256))  # status word inside the workspace
+    _overlap(sd, _sample(sd, status=US))
+    # realignment alone: device values inside the destination, the status word too
+    _overlap(sd, _realign(sd, pad_in=CACHE + 64))
+    _overlap(sd, _realign(sd, w_new=CACHE + 32764))
+    _overlap(sd, _realign(sd, src=_kv(sd, data=CACHE), dst=_kv(sd, data=CACHE), n_acc=CACHE + 4096))  # in place
+    f = sd.lib.specdec_realign_kv
+    src, dst = _kv(sd), _kv(sd, data=CACHE)
+    _overlap(sd, f(ctypes.byref(src), ctypes.byref(dst), 3, 10, PI, NA, WN, CACHE + 16, None))   # status word
+    # position ids / mask
+    _overlap(sd, sd.lib.specdec_build_posmask(PO, WN, 2, 3, POS, MSK, 64, MSK + 8, None))
+    # token row alone
+    g = sd.lib.specdec_realign_tokens
+    _overlap(sd, g(S_IN, 7, S_OUT, 11, S_OUT + 8, PI, NA, WN, 2, 3, 10, -1, None, None))  # tokens inside s_out
+    _overlap(sd, g(S_IN, 7, S_OUT, 11, TK, PI, NA, WN, 2, 3, 10, -1, S_OUT + 4, None))  # status inside s_out
+    _overlap(sd, g(S_IN, 16, S_IN, 16, TK, S_IN + 8, NA, WN, 2, 3, 10, -1, None, None))  # in place over pad_in
+    # fused steps
+    ws = sd.workspace_bytes(2, 3, 100)
+
+    def step(logits=LG, tokens=TK, n_acc=NA, pos=POS, status=None, src=None, dst=None, s_in=None, s_out=None,
+             stride=16, pad_in=PI):
+        src = src if src is not None else _kv(sd)
+        dst = dst if dst is not None else _kv(sd, data=CACHE)
+        return sd.lib.specdec_step(logits, 1, DR, pad_in, 2, 3, 100, 10, ctypes.byref(src), ctypes.byref(dst), tokens,
+                                   n_acc, BO, PO, WN, pos, MSK, 64, s_in, stride, s_out, stride, -1, WS, ws,
+                                   status, None, None)
+    _overlap(sd, step(tokens=CACHE + 1024))  # verification output inside the dst cache
+    _overlap(sd, step(logits=CACHE))  # logits inside the dst cache
+    _overlap(sd, step(status=NA))  # status word over n_acc
+    _overlap(sd, step(pos=A + 256))  # positions over the source cache
+    _overlap(sd, step(s_in=S_IN, s_out=TK))  # token row over tokens
+    _overlap(sd, step(s_in=S_IN, s_out=S_OUT, pos=S_IN + 64))  # positions over the old token row
+    _overlap(sd, step(src=_kv(sd, data=CACHE), pad_in=CACHE + 8))  # in place, pad_in inside the cache
+    sws = sd.sample_workspace_bytes(2, 3, 100)
+    src, dst = _kv(sd), _kv(sd, data=CACHE)
+    h = sd.lib.specdec_step_sample
+    _overlap(sd, h(LG, DL, 1, DR, PI, UA, CACHE + 512, 0.8, 2, 3, 100, 10, ctypes.byref(src), ctypes.byref(dst), TK, NA, BO,
+             PO, WN, POS, MSK, 64, None, 0, None, 0, -1, WS, sws, None, None, None))  # u_sample in the cache
+    _overlap(sd, h(LG, DL, 1, DR, PI, UA, US, 0.8, 2, 3, 100, 10, ctypes.byref(src), ctypes.byref(dst), TK, NA, BO,
+             PO, WN, POS, MSK, 64, None, 0, None, 0, -1, WS, sws, DL + 4, None, None))  # status word over draft logits
+    # Family A rollback: the width and the status word stand apart
+    r = sd.lib.specdec_rollback
+    T, N, P_, NO, B_, PO_, W = A, A + 4096, A + 8192, A + 12288, A + 16384, A + 20480, A + 24576
+    _overlap(sd, r(T, N, P_, 2, 3, 10, NO, B_, PO_, N, None, None))  # w_new over n_acc_in
+    _overlap(sd, r(T, N, P_, 2, 3, 10, NO, B_, PO_, W, NO + 4, None))  # status word over n_acc_out
+
+
 def test_missing_library_fails_loudly(tmp_path):
     """With no built library the binding refuses to import (no fallback path),
     and so do the smoke check and the benchmark, which go through it."""
