@@ -31,6 +31,10 @@
  *   included) may overlap an input or another output; inputs may overlap
  *   each other.  A cache or token row realigned in place is one buffer, read
  *   and written by the same call.  An overlap is SPECDEC_ERR_INVALID_ARGUMENT.
+ * - One launch holds fewer than 2^32 work-items; larger caches are moved by
+ *   several launches of the same kernel on the same stream.  The environment
+ *   variable SPECDEC_MAX_LAUNCH_ITEMS (a positive integer) lowers that cap, so
+ *   the multi-launch path can be tested at small sizes; results are the same.
  *
  * Terms: B rows, k draft tokens per row, V vocabulary entries.  W_in is the
  * width of the cache handed to the step, counted in cache columns and
