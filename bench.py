@@ -341,7 +341,7 @@ def bench_exspec(args, w):
     elapsed = timed_pass(K, 1 << sd.KERNEL_GATHER)
     gather_ms, gather_n = sd.timing_query(sd.KERNEL_GATHER)
     timed_pass(K, (1 << sd.KERNEL_VERIFY) | (1 << sd.KERNEL_WRITEBACK))
-    verify_ms, verify_n = sd.timing_query(vkern)
+    verify_ms, verify_n = sd.timing_query(sd.KERNEL_VERIFY)
     wb_ms, wb_n = sd.timing_query(sd.KERNEL_WRITEBACK)
     assert gather_n == K and verify_n == K and wb_n == K
     by = exspec_bytes(w, lens[:B], Lb, n_acc)
