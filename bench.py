@@ -92,19 +92,23 @@ def step_bytes(w, pad_in, W_in, n_acc, w_new, variant, token_row=True):
     return dict(realign=realign, posmask=posmask, verify=verify)
 
 
-def read_traffic_summary(workload: str, variant: str, kernel: str = "realign", srcs=None):
+def read_traffic_summary(workload: str, variant: str, alg_bytes: int, kernel: str = "realign", srcs=None):
     """HBM bytes per launch of the measured kernel from the committed rocprofv3
-    counter summary, if it was taken on the current kernel source."""
+    counter summary, if it was taken on the current kernel source and on a
+    launch with the same algorithmic bytes as this run's (the same step)."""
     path = ROOT / "profiles" / f"{kernel}_{variant}_{workload}_hbm_counters.md"
     if not path.exists():
         return None, "no counter summary"
     text = path.read_text()
     m_hash = re.search(r"kernel_source_sha256_16:\s*([0-9a-f]+)", text)
     m_bytes = re.search(r"hbm_bytes_per_launch:\s*([0-9.eE+]+)", text)
-    if not m_hash or not m_bytes:
+    m_alg = re.search(r"Algorithmic bytes per launch \(bench.py\):\s*(\d+)", text)
+    if not m_hash or not m_bytes or not m_alg:
         return None, "summary unreadable"
     if m_hash.group(1) != kernel_source_hash(srcs):
         return None, "kernel changed since the counters were taken"
+    if int(m_alg.group(1)) != int(alg_bytes):
+        return None, f"counters taken on another step ({m_alg.group(1)} algorithmic bytes)"
     return float(m_bytes.group(1)), path.name
 
 
@@ -350,7 +354,7 @@ def bench_exspec(args, w):
     ms_per_step = elapsed / K * 1e3
     total_bytes = by["gather"] + by["writeback"] + by["verify"]
     variant = "same" if args.exspec_batch == "same" else "ragged"
-    traffic, traffic_src = read_traffic_summary(w.name, variant, kernel="gather", srcs=GATHER_SRCS)
+    traffic, traffic_src = read_traffic_summary(w.name, variant, by["gather"], kernel="gather", srcs=GATHER_SRCS)
     log(f"[bench] exspec n_acc={n_acc.tolist()} gather {g_ms:.4f} ms ({by['gather'] / 1e9:.3f} GB, {achieved:.0f} GB/s), "
         f"verify {verify_ms / K:.4f} ms, write-back {wb_ms / K:.4f} ms ({by['writeback'] / 1e6:.2f} MB), "
         f"step {ms_per_step:.4f} ms; traffic: {traffic_src}")
@@ -446,7 +450,7 @@ def bench_varlen(args, w):
     vms = v_ms / K
     achieved = algo / (vms * 1e-3) / 1e9
     ms_per_step = elapsed / K * 1e3
-    traffic, traffic_src = read_traffic_summary(w.name, "oop", kernel="varlen", srcs=VARLEN_SRCS)
+    traffic, traffic_src = read_traffic_summary(w.name, "oop", algo, kernel="varlen", srcs=VARLEN_SRCS)
     log(f"[bench] varlen n_acc={n_acc.tolist()} compaction {vms:.4f} ms ({algo / 1e9:.3f} GB, {achieved:.0f} GB/s), "
         f"step {ms_per_step:.4f} ms; traffic: {traffic_src}")
     cpu = None
@@ -815,7 +819,7 @@ def main():
     achieved = realign_bytes / (realign_avg_ms * 1e-3) / 1e9
     ms_per_step = elapsed / K * 1e3
     step_gbs = (realign_bytes + by["verify"]) / (ms_per_step * 1e-3) / 1e9
-    traffic, traffic_src = read_traffic_summary(w.name, variant)
+    traffic, traffic_src = read_traffic_summary(w.name, variant, realign_bytes)
     copy_gbs = copy_ceiling(realign_bytes // 2) if args.copy_ceiling else None
     log(f"[bench] n_acc={n_acc.tolist()} w_new={w_new} realign {realign_avg_ms:.4f} ms "
         f"({realign_bytes / 1e9:.3f} GB, {achieved:.0f} GB/s), verify {verify_avg_ms:.4f} ms "

@@ -26,3 +26,27 @@ def test_help_lists_the_paths():
     assert r.returncode == 0
     for word in ("exspec", "varlen", "chained", "--verify", "--graph", "--variant"):
         assert word in r.stdout, word
+
+
+def test_traffic_comes_only_from_counters_of_the_same_step():
+    """bench.py takes `roofline.traffic` from a committed counter summary only
+    when the summary was taken on the current kernel sources and on a launch
+    with this run's algorithmic bytes."""
+    import re
+    import bench
+    for path in sorted((ROOT / "profiles").glob("*_hbm_counters.md")):
+        text = path.read_text()
+        alg = int(re.search(r"Algorithmic bytes per launch \(bench.py\):\s*(\d+)", text).group(1))
+        hbm = float(re.search(r"hbm_bytes_per_launch:\s*([0-9.eE+]+)", text).group(1))
+        kernel, variant, workload = path.name[:-len("_hbm_counters.md")].split("_")
+        srcs = {"realign": bench.KERNEL_SRCS, "gather": bench.GATHER_SRCS, "varlen": bench.VARLEN_SRCS}[kernel]
+        value, src = bench.read_traffic_summary(workload, variant, alg, kernel=kernel, srcs=srcs)
+        if value is None:
+            assert src == "kernel changed since the counters were taken", (path.name, src)
+        else:
+            assert value == hbm and src == path.name
+            assert abs(hbm / alg - 1) < 1e-3, path.name          # the counters read the algorithmic bytes
+        value, src = bench.read_traffic_summary(workload, variant, alg + 1, kernel=kernel, srcs=srcs)
+        assert value is None, path.name
+    value, src = bench.read_traffic_summary("nosuch", "oop", 1)
+    assert value is None and src == "no counter summary"
