@@ -25,9 +25,12 @@ __device__ __forceinline__ u32x4 ld16(const u32x4* p) {
 // compiler does not count this store in its memory wait counters, so any wait
 // it places for a later load also covers the store: waits only get stricter,
 // and no kernel here reads what another thread of the same launch stored.
+// Nor does it see the store when it inserts wait states, so the statement
+// ends with the one wait state that a VALU write to the data registers of a
+// preceding store wider than 8 bytes needs.
 template <bool kNt>
 __device__ __forceinline__ void st16(u32x4* p, u32x4 v) {
-  if constexpr (kNt) asm volatile("global_store_dwordx4 %0, %1, off nt sc1" : : "v"(p), "v"(v) : "memory");
+  if constexpr (kNt) asm volatile("global_store_dwordx4 %0, %1, off nt sc1\n\ts_nop 0" : : "v"(p), "v"(v) : "memory");
   else *p = v;
 }
 
