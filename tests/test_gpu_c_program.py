@@ -1,10 +1,11 @@
 """The fused step driven from a plain C program: device memory from the HIP
 runtime (hipMalloc / hipMemcpy), no PyTorch in the process, the library
 called through include/specdec.h only.  The program reads seeded inputs from
-a file, runs specdec_step (out of place, with the token row) on the null
+a file, runs specdec_step (with the token row, out of place or in place) on the null
 stream, and writes every output back; the outputs must equal the oracle's
-element by element, and columns the step does not own keep the sentinels the
-program wrote there."""
+element by element, and out of place the columns the step does not own keep
+the sentinels the program wrote there.  In place the cache and the token row
+are updated in their own buffers."""
 import shutil
 import subprocess
 from pathlib import Path
@@ -55,8 +56,9 @@ int main(int argc, char** argv) {
   if (argc != 3) return 2;
   FILE* in = fopen(argv[1], "rb");
   if (!in) return 2;
-  int32_t h[12];
-  if (fread(h, sizeof(int32_t), 12, in) != 12) return 3;
+  int32_t h[13];
+  if (fread(h, sizeof(int32_t), 13, in) != 13) return 3;
+  const int in_place = h[12];
   const int32_t B = h[0], k = h[1], V = h[2], W_in = h[3], L = h[4], H = h[5], D = h[6], cap = h[7];
   const int32_t pm_cap = h[8], s_in_stride = h[9], s_out_stride = h[10], pad_id = h[11];
   const size_t n_logits = (size_t)B * (k + 1) * V * 2, n_draft = (size_t)B * k * 4, n_b = (size_t)B * 4;
@@ -73,9 +75,9 @@ int main(int argc, char** argv) {
   void* d_draft = dev(draft, n_draft, 0);
   void* d_pad_in = dev(pad_in, n_b, 0);
   void* d_src = dev(kv, n_kv, 0);
-  void* d_dst = dev(NULL, n_kv, 0x7F);        /* sentinel bytes outside the new width */
+  void* d_dst = in_place ? d_src : dev(NULL, n_kv, 0x7F);   /* sentinel bytes outside the new width */
   void* d_s_in = dev(s_in, n_s_in, 0);
-  void* d_s_out = dev(NULL, n_s_out, 0x55);
+  void* d_s_out = in_place ? d_s_in : dev(NULL, n_s_out, 0x55);
   void* d_tokens = dev(NULL, (size_t)B * (k + 1) * 4, 0);
   void* d_n_acc = dev(NULL, n_b, 0);
   void* d_bonus = dev(NULL, n_b, 0);
@@ -119,7 +121,8 @@ int main(int argc, char** argv) {
 """
 
 
-def test_fused_step_from_c(tmp_path):
+@pytest.mark.parametrize("in_place", [False, True], ids=["oop", "inplace"])
+def test_fused_step_from_c(tmp_path, in_place):
     if not torch.cuda.is_available():
         pytest.skip("needs a GPU")
     if shutil.which("gcc") is None:
@@ -136,15 +139,16 @@ def test_fused_step_from_c(tmp_path):
     n, W_in, pad_in, cap = wl.initial_geometry(w, seed)
     logits, draft, *_ = wl.logits_and_drafts(w, seed, 0, device="cpu")
     src = wl.make_kv(w, pad_in, W_in, cap, seed, device="cpu")
-    s_in_stride, s_out_stride, pm_cap = cap + 2, W_in + 1 + 3, W_in + w.k + 1 + 5
+    s_in_stride, s_out_stride, pm_cap = cap + 2, (cap + 2 if in_place else W_in + 1 + 3), W_in + w.k + 1 + 5
     s_in = wl.make_token_rows(w, pad_in, W_in, s_in_stride, seed, PAD_ID, device="cpu")
     kv_bits = src.view(torch.int16).numpy().view(np.uint16)
-    header = np.array([w.B, w.k, w.V, W_in, w.L, w.H, w.D, cap, pm_cap, s_in_stride, s_out_stride, PAD_ID], np.int32)
+    header = np.array([w.B, w.k, w.V, W_in, w.L, w.H, w.D, cap, pm_cap, s_in_stride, s_out_stride, PAD_ID,
+                       int(in_place)], np.int32)
     with open(tmp_path / "in.bin", "wb") as f:
         for a in (header, logits.view(torch.int16).numpy(), draft.numpy().astype(np.int32),
                   np.asarray(pad_in, np.int32), kv_bits, s_in.numpy().astype(np.int32)):
             f.write(np.ascontiguousarray(a).tobytes())
-    say(f"C program: B={w.B} k={w.k} V={w.V} L={w.L} H={w.H} D={w.D} W_in={W_in} cap={cap}")
+    say(f"C program: B={w.B} k={w.k} V={w.V} L={w.L} H={w.H} D={w.D} W_in={W_in} cap={cap} in_place={in_place}")
     r = subprocess.run([str(exe), str(tmp_path / "in.bin"), str(tmp_path / "out.bin")], capture_output=True,
                        text=True, timeout=120)
     assert r.returncode == 0 and r.stdout.strip() == "ok", r.stdout + r.stderr
@@ -177,11 +181,13 @@ def test_fused_step_from_c(tmp_path):
     assert w_new == W and w_host == W
     exp = oracle.realign_kv(kv_bits, k, W_in, pad_in, v["n_acc"], W)
     assert np.array_equal(dst[..., :W, :], exp[..., :W, :]), "cache differs from the oracle"
-    assert np.all(dst[..., W:, :] == 0x7F7F), "cache columns beyond L' were written"
+    if not in_place:
+        assert np.all(dst[..., W:, :] == 0x7F7F), "cache columns beyond L' were written"
     epos, emask = oracle.posmask(v["pad_out"], W, k, pm_cap)
     width = W + k + 1
     assert np.array_equal(pos[:, :width], epos[:, :width]) and np.array_equal(mask[:, :width], emask[:, :width])
     assert np.all(pos[:, width:] == 0x6666666666666666) and np.all(mask[:, width:] == 0x77)
     es = oracle.realign_tokens(s_in.numpy(), v["tokens"], pad_in, v["n_acc"], W, W_in, PAD_ID)
     assert np.array_equal(s_out[:, :W + 1], es[:, :W + 1]), "token row differs from the oracle"
-    assert np.all(s_out[:, W + 1:] == 0x55555555)
+    if not in_place:
+        assert np.all(s_out[:, W + 1:] == 0x55555555)
