@@ -9,9 +9,9 @@ here, and neither depends on the other.
 
 Every random draw is keyed by ``(seed, stream tag, step)`` so that each tensor
 and each chained step has its own sub-stream.  Logits and KV are drawn with
-``torch.Generator`` on the device where they will live (GPU machines generate the
-multi-GB caches in place); tests that need the same bytes on the host copy them
-back.  The small integer draws (prompt lengths, acceptance lengths, planted
+``torch.Generator`` on the device where they will live (the multi-GB caches
+are generated on the GPU, in place); tests that need the same bytes on the host
+copy them back.  The small integer draws (prompt lengths, acceptance lengths, planted
 tokens) use numpy on the host so they are identical everywhere.
 
 The five named workloads stand in for the paper's target/draft model pairs
