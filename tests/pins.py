@@ -676,6 +676,28 @@ def pin_scheduler_grouping_rate(o=None):
     assert sum(1 for _, r in rounds if not r) == 3          # one gather per batch of 4
 
 
+def pin_scheduler_bucket_golden(o=None):
+    """Alg. 2's GetBatch grouping on hand-derived windows
+    (``tests/golden/sched_bucket_choice.txt``): the oldest window member's
+    length bucket when it holds b = min(B, |window|) members, else the largest
+    bucket holding b (between equal sizes, the shorter length), else the first
+    b window members; the batch's lengths, width and flags follow from the
+    chosen slots."""
+    from oracle.exspec import SequencePool
+    g = _read_golden("sched_bucket_choice.txt")
+    cases = sorted({key.split("_", 1)[0] for key in g})
+    assert len(cases) == 7, cases
+    for c in cases:
+        lens0 = g[f"{c}_lens"]
+        sp = SequencePool(lens0, window=g[f"{c}_window"][0], batch=g[f"{c}_batch"][0], max_new=1,
+                          sort_by_length=False)
+        b = sp.next_batch()
+        assert b is not None and b.slots == g[f"{c}_slots"], (c, b.slots if b else None)
+        lens = [lens0[s] for s in b.slots]
+        assert b.lens == lens and b.width == max(lens) and not b.reuse, c
+        assert b.same_length == (len(set(lens)) == 1), c
+
+
 # ---- stochastic verification (T > 0): speculative sampling ---------------------------------------
 
 def _softmax64(x, T):
@@ -781,6 +803,60 @@ def pin_sample_special_cases(o=None):
         assert list(a["tokens"][i, :r]) == list(draft[i, :r]) and np.all(a["tokens"][i, r + 1:] == -1)
     from tests import checker
     checker.check_geometry(pad, a["n_acc"], a["pad_out"], a["w_new"], W_in, k)
+
+
+def pin_sample_widening_exact(o=None):
+    """Stochastic verification depends on the logits' values, not only their
+    order: a bf16 or f16 logit must enter the softmax exactly as the same
+    number held in float32 (every bf16 and f16 value is a float32 value).  The
+    oracle on 16-bit logits must therefore decide exactly as the oracle on
+    their float32 widenings, made here by numpy's float16 and torch's bfloat16
+    conversions.  Rows of normal values at T = 1, rows of subnormals and zeros
+    at a temperature of their own scale (where any slip in the subnormal
+    scale changes the distribution), and rows of mixed magnitudes with -inf
+    entries."""
+    rng = np.random.default_rng(33)
+    B, k, V = 48, 2, 37
+    for dt in ("f16", "bf16"):
+        for regime, T in (("normal", 1.0), ("subnormal", 4e-6 if dt == "f16" else 4e-40), ("mixed", 0.8)):
+            n = B * (2 * k + 1) * V
+            if regime == "normal":
+                vals = rng.normal(0, 2, size=n).astype(np.float32)
+                bits = (vals.astype(np.float16).view(np.uint16) if dt == "f16" else
+                        torch.from_numpy(vals).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16))
+            elif regime == "subnormal":
+                mant = 0x03FF if dt == "f16" else 0x007F
+                bits = (rng.integers(0, mant + 1, size=n) | (rng.integers(0, 2, size=n) << 15)).astype(np.uint16)
+            else:
+                bits = rng.integers(0, 2 ** 16, size=n).astype(np.uint16)
+                expo = (bits >> (10 if dt == "f16" else 7)) & (0x1F if dt == "f16" else 0xFF)
+                top = 0x1F if dt == "f16" else 0xFF
+                bits = np.where(expo == top, bits & np.uint16(0x83FF if dt == "f16" else 0x807F), bits)  # no inf/NaN
+                bits = bits.astype(np.uint16)
+                bits[rng.random(n) < 0.1] = 0xFC00 if dt == "f16" else 0xFF80                      # -inf entries
+                bits = bits.reshape(-1, V)
+                bits[:, 0] = 0x3C00 if dt == "f16" else 0x3F80                                     # a finite maximum per row
+                bits = bits.reshape(-1)
+            if dt == "f16":
+                f32 = bits.view(np.float16).astype(np.float32)
+            else:
+                f32 = torch.from_numpy(bits.view(np.int16).copy()).view(torch.bfloat16).float().numpy()
+            allb = bits.reshape(B, 2 * k + 1, V)
+            allf = f32.reshape(B, 2 * k + 1, V)
+            draft = rng.integers(0, V, size=(B, k)).astype(np.int32)
+            pad = rng.integers(0, 3, size=B).astype(np.int32)
+            ua = rng.random((B, k)).astype(np.float32)
+            us = rng.random(B).astype(np.float32)
+            W_in = 6 + k + 1
+            a = oracle.verify_sample(np.ascontiguousarray(allb[:, : k + 1]), np.ascontiguousarray(allb[:, k + 1:]), dt,
+                                     draft, pad, ua, us, T, W_in, oracle=o)
+            b = oracle.verify_sample(np.ascontiguousarray(allf[:, : k + 1]), np.ascontiguousarray(allf[:, k + 1:]), "f32",
+                                     draft, pad, ua, us, T, W_in, oracle=o)
+            for key in ("tokens", "n_acc", "bonus", "pad_out"):
+                assert np.array_equal(a[key], b[key]), (dt, regime, key)
+            assert a["w_new"] == b["w_new"], (dt, regime)
+            # the case is not degenerate: the draws differ from row to row
+            assert len(set(int(x) for x in a["bonus"])) > 3, (dt, regime)
 
 
 # ---- rollback (Family A) and variable-length rollback (Family B) ----------------------------------
@@ -898,8 +974,8 @@ ALL_PINS = [
     pin_posmask_closed_form, pin_golden_worked_example, pin_tokens_replay, pin_tokens_chain,
     pin_gather_list_model, pin_gather_same_length_is_concat, pin_regroup_equals_realign,
     pin_scatter_appends_to_batch_row, pin_exspec_output_equivalence, pin_eqspec_output_equivalence,
-    pin_scheduler_properties, pin_scheduler_grouping_rate,
-    pin_sample_preserves_target_distribution, pin_sample_special_cases,
+    pin_scheduler_properties, pin_scheduler_grouping_rate, pin_scheduler_bucket_golden,
+    pin_sample_preserves_target_distribution, pin_sample_special_cases, pin_sample_widening_exact,
     pin_rollback_list_model, pin_rollback_output_equivalence, pin_varlen_list_model,
     pin_varlen_equals_padded_realign,
 ]

@@ -24,8 +24,11 @@ MUTANTS = {
     "argmax_ignores_nan": ("if (isnan(x)) return v;", ""),
     "bf16_widen_wrong_shift": ("(uint32_t)h << 16", "(uint32_t)h << 15"),
     # (a slip in the f16 exponent bias or subnormal scale keeps the order of all
-    # values, so no argmax can observe it; these two break the order)
+    # values, so no argmax can observe it: stochastic verification, which uses
+    # the values, must)
     "f16_mantissa_bit": ("(m | 0x400)", "(m | 0x200)"),
+    "f16_exponent_bias": ("e - 25);", "e - 24);"),
+    "f16_subnormal_scale": ("v = ldexp((double)m, -24);", "v = ldexp((double)m, -23);"),
     "f16_sign_dropped": ("return sign ? -v : v;", "(void)sign;\n  return v;"),
     "all_accept_reads_as_zero": ("int32_t j = k;", "int32_t j = 0;"),
     "bonus_from_draft": ("if (bonus) bonus[i] = tokens[(int64_t)i * (k + 1) + j];",
@@ -102,6 +105,10 @@ PY_MUTANTS = {
     "reuse_ignores_finished": ("if self.prev is not None and all(self.active[s] for s in self.prev)",
                                "if self.prev is not None"),
     "length_without_bonus": ("a = int(n_acc[i]) + 1", "a = int(n_acc[i])"),
+    # the bucket choice of the same-length grouping
+    "bucket_tie_to_longer": ("key=lambda b: (len(b), -self.len[b[0]])", "key=lambda b: (len(b), self.len[b[0]])"),
+    "oldest_bucket_rule_dropped": ("if len(first) >= B:", "if False:"),
+    "largest_bucket_is_first_found": ("best = max(big, key=lambda b: (len(b), -self.len[b[0]]))", "best = big[0]"),
 }
 
 PY_RUNNER = r"""

@@ -118,3 +118,18 @@ def test_scheduler_rejects(sd):
     assert s.lengths() == [5, 6]
     b2 = s.next_batch()
     assert b2.slots == [0] and not b2.reuse               # row 1 finished at eos
+
+
+def test_native_scheduler_golden_bucket_choice(sd):
+    """The native scheduler takes the hand-derived batches of
+    tests/golden/sched_bucket_choice.txt (same-length grouping of Alg. 2's
+    GetBatch: oldest member's bucket, else the largest, ties to the shorter
+    length, else the first window members)."""
+    from tests import pins
+    g = pins._read_golden("sched_bucket_choice.txt")
+    for c in sorted({key.split("_", 1)[0] for key in g}):
+        lens0 = g[f"{c}_lens"]
+        s = sd.Scheduler(lens0, window=g[f"{c}_window"][0], batch=g[f"{c}_batch"][0], max_new=1, sort_by_length=False)
+        b = s.next_batch()
+        assert b is not None and b.slots == g[f"{c}_slots"], (c, b.slots if b else None)
+        assert b.lens == [lens0[x] for x in b.slots] and not b.reuse
