@@ -254,7 +254,10 @@ __global__ __launch_bounds__(kTpb) void writeback_append_kernel(WritebackArgs a)
   const u32x4* s = a.batch + static_cast<int64_t>(span) * a.batch_span_vecs + static_cast<int64_t>(a.Lb) * vpc;
   u32x4* d = a.pool + pool_span * a.pool_span_vecs + static_cast<int64_t>(g.n) * vpc;
   const int64_t nv = static_cast<int64_t>(g.a) * vpc;
-  for (int64_t u = threadIdx.x; u < nv; u += kTpb) st16<true>(d + u, ld16<true>(s + u));
+  const int64_t w = static_cast<int64_t>(wave_index()) * 64;
+  const int lane = static_cast<int>(threadIdx.x & 63);
+  for (int64_t u0 = 0; u0 < nv; u0 += kTpb)
+    if (u0 + w + lane < nv) st16_at<true>(d + (u0 + w), static_cast<uint32_t>(lane), ld16<true>(s + (u0 + w + lane)));
 }
 
 }  // namespace

@@ -17,22 +17,37 @@ __device__ __forceinline__ u32x4 ld16(const u32x4* p) {
   else return *p;
 }
 
-// Stores one 16-byte vector.  With kNt the store is nontemporal and
-// device-coherent (cache policy "nt sc1"): the line is written through the
-// XCD's L2 instead of staying dirty in it until eviction or the end of the
-// kernel.  Measured on MI355X against a nontemporal store alone: about 1%
-// faster for the out-of-place moves and 1.4-5% for the in-place walk.  The
-// compiler does not count this store in its memory wait counters, so any wait
-// it places for a later load also covers the store: waits only get stricter,
-// and no kernel here reads what another thread of the same launch stored.
-// Nor does it see the store when it inserts wait states, so the statement
-// ends with the one wait state that a VALU write to the data registers of a
-// preceding store wider than 8 bytes needs.
+// Stores one 16-byte vector at wave_base[lane_vec].  With kNt the store is
+// nontemporal and device-coherent (cache policy "nt sc1"): the line is
+// written through the XCD's L2 instead of staying dirty in it until eviction
+// or the end of the kernel.  Measured on MI355X against a nontemporal store
+// alone: about 1% faster for the out-of-place moves and 1.4-5% for the
+// in-place walk; the compiler's nontemporal store sets "nt" alone, and the
+// buffer-store builtin that takes the policy bits measured 0.5-1.5% slower
+// than this global store on the out-of-place moves.
+//
+// The store is inline assembly, so the compiler sees neither its memory
+// operation nor its data registers:
+//  * Wait counters: the compiler does not count it, so any wait it places
+//    for a later load also covers the store (waits only get stricter); no
+//    kernel here reads what another thread of the same launch stored.
+//  * Hazard: on gfx950 a VALU write of the data registers of a store wider
+//    than 8 bytes must come at least two wait states after the store, or the
+//    store may write the new value.  The compiler inserts these for its own
+//    stores; for this one the statement carries them ("s_nop 1").  With no
+//    wait state the compiler once placed a 64-bit register move into the low
+//    half of a zero store's data registers one instruction after it, and a
+//    padding column received 8 bytes of that value.
 template <bool kNt>
-__device__ __forceinline__ void st16(u32x4* p, u32x4 v) {
-  if constexpr (kNt) asm volatile("global_store_dwordx4 %0, %1, off nt sc1\n\ts_nop 0" : : "v"(p), "v"(v) : "memory");
-  else *p = v;
+__device__ __forceinline__ void st16_at(u32x4* wave_base, uint32_t lane_vec, u32x4 v) {
+  if constexpr (kNt)
+    asm volatile("global_store_dwordx4 %0, %1, off nt sc1\n\ts_nop 1" : : "v"(wave_base + lane_vec), "v"(v) : "memory");
+  else wave_base[lane_vec] = v;
 }
+
+// Index of the calling thread's wavefront in its workgroup, as a value the
+// compiler knows to be uniform across the wave.
+__device__ __forceinline__ int wave_index() { return __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x >> 6)); }
 
 // Loads a value that no kernel of this launch writes, through the constant
 // address space: a wave-uniform address then becomes a scalar load on the
@@ -72,18 +87,16 @@ __device__ __forceinline__ void split_pieces(const u32x4* s, u32x4* d, int64_t b
       v[j] = zero;
     }
   }
+  // every load has landed before the first store is issued, so no store
+  // waits behind another one (stores count in the same wait counter)
+#pragma unroll
+  for (int j = 0; j < kPieces; ++j) asm volatile("" ::"v"(v[j].x), "v"(v[j].y), "v"(v[j].z), "v"(v[j].w));
 #pragma unroll
   for (int j = 0; j < kPieces; ++j) {
-    const int64_t p0 = base + static_cast<int64_t>(j) * kSplit;
+    const int64_t p0 = base + static_cast<int64_t>(j) * kSplit;   // the piece's first vector (wave-uniform)
     if (p0 >= total) break;
     const int64_t u = p0 + t;
-    if (p0 >= 0 && p0 + kTpb <= zero_end) {
-      st16<(kNt & 2) != 0>(d + u, zero);
-    } else if (p0 >= zero_end && p0 + kTpb <= total) {
-      st16<(kNt & 2) != 0>(d + u, v[j]);
-    } else if (u >= 0 && u < total) {
-      st16<(kNt & 2) != 0>(d + u, u >= zero_end ? v[j] : zero);
-    }
+    if (u >= 0 && u < total) st16_at<(kNt & 2) != 0>(d + p0, t, u >= zero_end ? v[j] : zero);
   }
 }
 

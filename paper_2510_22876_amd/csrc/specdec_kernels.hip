@@ -548,11 +548,13 @@ __device__ __forceinline__ void load_chunk(const u32x4* base, int64_t from, int6
 
 template <int kVec, int kTpb, int kNt>
 __device__ __forceinline__ void store_chunk(u32x4* base, int64_t to, int64_t lo, int64_t n, const u32x4 (&v)[kVec]) {
-  const int64_t t0 = static_cast<int64_t>(threadIdx.x >> 6) * (64 * kVec) + (threadIdx.x & 63);
+  const int64_t w0 = lo + static_cast<int64_t>(wave_index()) * (64 * kVec);   // the wave's first vector
+  const int lane = static_cast<int>(threadIdx.x & 63);
+  u32x4* wb = base + (to + w0);
 #pragma unroll
   for (int j = 0; j < kVec; ++j) {
-    const int64_t u = lo + t0 + j * 64;
-    if (u >= 0 && u < n) st16<(kNt & 2) != 0>(base + (to + u), v[j]);
+    const int64_t u = w0 + lane + j * 64;
+    if (u >= 0 && u < n) st16_at<(kNt & 2) != 0>(wb, static_cast<uint32_t>(lane + j * 64), v[j]);
   }
 }
 
@@ -623,7 +625,11 @@ __global__ __launch_bounds__(kTpb) void realign_inplace_kernel(RealignArgs a) {
     // the vacated columns [pad_in, pad_out) become padding; every read of
     // them landed before the last barrier
     const u32x4 zero = {0u, 0u, 0u, 0u};
-    for (int64_t u = threadIdx.x; u < to - from; u += kTpb) st16<(kNt & 2) != 0>(base + (from + u), zero);
+    for (int64_t u0 = 0; u0 < to - from; u0 += kTpb) {
+      const int64_t w0 = u0 + static_cast<int64_t>(wave_index()) * 64;
+      const int lane = static_cast<int>(threadIdx.x & 63);
+      if (w0 + lane < to - from) st16_at<(kNt & 2) != 0>(base + (from + w0), static_cast<uint32_t>(lane), zero);
+    }
   }
   // columns [0, pad_out) already hold padding (+0.0) for a shift to lower addresses
 }
