@@ -83,6 +83,7 @@ typedef enum { SPECDEC_F32 = 0, SPECDEC_BF16 = 1, SPECDEC_F16 = 2 } specdec_dtyp
 #define SPECDEC_MAX_WIDTH 16777216    /* W_in, cap and pm_cap                      */
 #define SPECDEC_MAX_D 4096
 #define SPECDEC_MAX_SAMPLE_V 8388608  /* vocabulary of stochastic verification          */
+#define SPECDEC_NOALLOC_SCRATCH_BYTES 4194304  /* library scratch of specdec_step_noalloc */
 
 /* A bf16 KV cache [L][2][B][H][cap][D], contiguous, D fastest.  One
  * (layer, K/V, row, head) "span" is cap*D contiguous elements.  `data` is a
@@ -283,6 +284,34 @@ specdec_status_t specdec_step(const void* logits, int32_t dtype, const int32_t* 
                               int64_t s_out_stride, int32_t pad_id,
                               void* workspace, size_t workspace_bytes, uint32_t* dev_status,
                               int32_t* w_new_host, void* stream);
+
+/*
+ * specdec_step without a workspace argument, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid allocation).  Same arguments, outputs and checks as
+ * specdec_step, minus workspace / workspace_bytes.
+ *
+ * Verification's partial maxima live in a library-owned device array of
+ * SPECDEC_NOALLOC_SCRATCH_BYTES, one copy per device, held until the process
+ * ends; its address is looked up once per device (on the first call with
+ * that device current) and nothing is allocated or freed, ever.  A step whose
+ * verification needs more scratch than that (specdec_workspace_bytes(B, k, V)
+ * > SPECDEC_NOALLOC_SCRATCH_BYTES) is rejected with SPECDEC_ERR_WORKSPACE
+ * before anything is enqueued.  The stream must belong to the current device
+ * (SPECDEC_ERR_INVALID_ARGUMENT otherwise).  Every call on one device shares
+ * that device's scratch, so calls on one device that may overlap in time (on
+ * different streams, or graph replays running concurrently) race and give
+ * unspecified results; order them.  The scratch needs no initialisation: each
+ * call writes every slot it reads before reading it.
+ */
+specdec_status_t specdec_step_noalloc(const void* logits, int32_t dtype, const int32_t* draft,
+                                      const int32_t* pad_in, int32_t B, int32_t k, int32_t V,
+                                      int32_t W_in, const specdec_kv_t* src, const specdec_kv_t* dst,
+                                      int32_t* tokens, int32_t* n_acc, int32_t* bonus, int32_t* pad_out,
+                                      int32_t* w_new, int64_t* pos, uint8_t* mask, int64_t pm_cap,
+                                      const int32_t* s_in, int64_t s_in_stride, int32_t* s_out,
+                                      int64_t s_out_stride, int32_t pad_id, uint32_t* dev_status,
+                                      int32_t* w_new_host, void* stream);
 
 /* ---- EXSpec (Algorithm 2): sequence pool, batch gather and write-back ---------
  *

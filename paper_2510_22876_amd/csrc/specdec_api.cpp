@@ -705,6 +705,75 @@ specdec_status_t specdec_step(const void* logits, int32_t dtype, const int32_t* 
                       s_in_stride, s_out, s_out_stride, pad_id, dev_status, w_new_host, st);
 }
 
+// ---- specdec_step_noalloc: the fused step on library-owned scratch -----------
+//
+// Verification's partial maxima live in `scratch`, a file-scope device array.
+// Each device the library runs on holds its own copy until the process ends.
+// In host code the name only identifies the symbol (it is not a device
+// address): the device address of each device's copy is taken once, with
+// that device current, by hipGetSymbolAddress, and only that address is ever
+// handed to a kernel.
+static __device__ __align__(256) unsigned char scratch[SPECDEC_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxScratchDevices = 256;
+std::mutex g_scratch_mu;
+void* g_scratch_addr[kMaxScratchDevices] = {};
+
+// Device address of the current device's scratch; the stream, when given,
+// must belong to that device.
+specdec_status_t device_scratch(hipStream_t stream, void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (stream) {
+    int sdev = -1;
+    e = hipStreamGetDevice(stream, &sdev);
+    if (e != hipSuccess) return hip_fail(e, "hipStreamGetDevice");
+    if (sdev != dev)
+      return fail(SPECDEC_ERR_INVALID_ARGUMENT, "stream belongs to device %d, the current device is %d", sdev, dev);
+  }
+  if (dev < 0 || dev >= kMaxScratchDevices)
+    return fail(SPECDEC_ERR_UNSUPPORTED, "device index %d beyond the scratch table (%d)", dev, kMaxScratchDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_addr[dev]) {
+    void* addr = nullptr;
+    e = hipGetSymbolAddress(&addr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    if (!addr) return fail(SPECDEC_ERR_HIP, "hipGetSymbolAddress(scratch) returned NULL");
+    g_scratch_addr[dev] = addr;
+  }
+  *out = g_scratch_addr[dev];
+  return SPECDEC_OK;
+}
+
+}  // namespace
+
+specdec_status_t specdec_step_noalloc(const void* logits, int32_t dtype, const int32_t* draft, const int32_t* pad_in,
+                                      int32_t B, int32_t k, int32_t V, int32_t W_in, const specdec_kv_t* src,
+                                      const specdec_kv_t* dst, int32_t* tokens, int32_t* n_acc, int32_t* bonus,
+                                      int32_t* pad_out, int32_t* w_new, int64_t* pos, uint8_t* mask, int64_t pm_cap,
+                                      const int32_t* s_in, int64_t s_in_stride, int32_t* s_out, int64_t s_out_stride,
+                                      int32_t pad_id, uint32_t* dev_status, int32_t* w_new_host, void* stream) {
+  void* ws = nullptr;
+  size_t ws_bytes = 0;
+  if (B > 0) {
+    const size_t need = specdec_workspace_bytes(B, k, V);
+    if (need > SPECDEC_NOALLOC_SCRATCH_BYTES)
+      return fail(SPECDEC_ERR_WORKSPACE,
+                  "specdec_step_noalloc: verification of B=%d, k=%d, V=%d needs %zu bytes of scratch, more than the "
+                  "library's %d (use specdec_step with a workspace)",
+                  B, k, V, need, SPECDEC_NOALLOC_SCRATCH_BYTES);
+    const specdec_status_t s = device_scratch(static_cast<hipStream_t>(stream), &ws);
+    if (s) return s;
+    ws_bytes = SPECDEC_NOALLOC_SCRATCH_BYTES;
+  }
+  return specdec_step(logits, dtype, draft, pad_in, B, k, V, W_in, src, dst, tokens, n_acc, bonus, pad_out, w_new, pos,
+                      mask, pm_cap, s_in, s_in_stride, s_out, s_out_stride, pad_id, ws, ws_bytes, dev_status,
+                      w_new_host, stream);
+}
+
 specdec_status_t specdec_step_sample(const void* logits, const void* draft_logits, int32_t dtype,
                                      const int32_t* draft, const int32_t* pad_in, const float* u_accept,
                                      const float* u_sample, float temperature, int32_t B, int32_t k, int32_t V,

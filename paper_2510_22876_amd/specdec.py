@@ -30,7 +30,7 @@ WRITEBACK_FULL, WRITEBACK_APPEND = 0, 1
 EXPORTED = (
     "specdec_abi_version", "specdec_last_error", "specdec_workspace_bytes", "specdec_workspace_init",
     "specdec_verify_greedy", "specdec_sample_workspace_bytes", "specdec_verify_sample", "specdec_realign_kv", "specdec_build_posmask", "specdec_realign_tokens",
-    "specdec_step", "specdec_step_sample", "specdec_gather_batch", "specdec_scatter_accepted",
+    "specdec_step", "specdec_step_noalloc", "specdec_step_sample", "specdec_gather_batch", "specdec_scatter_accepted",
     "specdec_rollback", "specdec_varlen_rollback",
     "specdec_sched_create", "specdec_sched_destroy", "specdec_sched_next_batch", "specdec_sched_commit",
     "specdec_sched_lengths", "specdec_sched_active",
@@ -79,6 +79,8 @@ def _load(path: Path = _LIB_PATH) -> ctypes.CDLL:
     lib.specdec_realign_tokens.argtypes = [P, i64, P, i64, P, P, P, P, i32, i32, i32, i32, P, P]
     lib.specdec_step.argtypes = [P, i32, P, P, i32, i32, i32, i32, pKV, pKV, P, P, P, P, P, P, P, i64,
                                  P, i64, P, i64, i32, P, sz, P, P, P]
+    lib.specdec_step_noalloc.argtypes = [P, i32, P, P, i32, i32, i32, i32, pKV, pKV, P, P, P, P, P, P, P, i64,
+                                         P, i64, P, i64, i32, P, P, P]
     lib.specdec_sample_workspace_bytes.argtypes = [i32, i32, i32]
     lib.specdec_sample_workspace_bytes.restype = sz
     lib.specdec_verify_sample.argtypes = [P, P, i32, P, P, P, P, ctypes.c_float, i32, i32, i32, i32, P, P, P, P, P,
@@ -195,6 +197,8 @@ def _check_verify(logits, draft, pad_in, tokens, n_acc, bonus, pad_out, w_new, w
     _req("pad_out", pad_out, (B,), i32)
     _req("w_new", w_new, (1,), i32)
     _req("dev_status", dev_status, (1,), i32, optional=True)
+    if workspace is None:   # the library's own scratch (specdec_step_noalloc)
+        return
     if workspace.numel() * workspace.element_size() < workspace_bytes(B, kp1 - 1, V) or not workspace.is_cuda:
         raise ValueError("workspace too small")
 
@@ -310,6 +314,34 @@ def specdec_step(logits, draft, pad_in, W_in: int, src, dst, tokens, n_acc, bonu
         _p(pos), _p(mask), pos.shape[1], _p(s_in), s_in.shape[1] if s_in is not None else 0, _p(s_out),
         s_out.shape[1] if s_out is not None else 0, pad_id,
         _p(workspace), workspace.numel() * workspace.element_size(),
+        _p(dev_status), ctypes.byref(host) if sync_w_new else None, _stream(stream)))
+    return host.value if sync_w_new else None
+
+
+def specdec_step_noalloc(logits, draft, pad_in, W_in: int, src, dst, tokens, n_acc, bonus, pad_out, w_new,
+                         pos, mask, dev_status=None, sync_w_new: bool = False, stream=None,
+                         s_in=None, s_out=None, pad_id: int = 0):
+    """``specdec_step`` on the library's own scratch (no workspace argument);
+    returns L' as a Python int when ``sync_w_new``."""
+    B, kp1, V = logits.shape
+    _check_verify(logits, draft, pad_in, tokens, n_acc, bonus, pad_out, w_new, None, dev_status)
+    s = kv_desc(src)
+    d = kv_desc(dst)
+    if s.B != B:
+        raise ValueError("cache rows differ from logit rows")
+    _req("pos", pos, (B, pos.shape[1]), torch.int64)
+    _req("mask", mask, (B, pos.shape[1]), torch.uint8)
+    if (s_in is None) != (s_out is None):
+        raise ValueError("give both s_in and s_out, or neither")
+    if s_in is not None:
+        _req("s_in", s_in, (B, s_in.shape[1]), torch.int32)
+        _req("s_out", s_out, (B, s_out.shape[1]), torch.int32)
+    host = ctypes.c_int32(-1)
+    _check(lib.specdec_step_noalloc(
+        _p(logits), DTYPE_OF[logits.dtype], _p(draft), _p(pad_in), B, kp1 - 1, V, W_in,
+        ctypes.byref(s), ctypes.byref(d), _p(tokens), _p(n_acc), _p(bonus), _p(pad_out), _p(w_new),
+        _p(pos), _p(mask), pos.shape[1], _p(s_in), s_in.shape[1] if s_in is not None else 0, _p(s_out),
+        s_out.shape[1] if s_out is not None else 0, pad_id,
         _p(dev_status), ctypes.byref(host) if sync_w_new else None, _stream(stream)))
     return host.value if sync_w_new else None
 

@@ -174,6 +174,26 @@ def test_step_rejects(sd):
     assert step(pos=NA - 8) == 1                 # pos over n_acc
 
 
+def test_step_noalloc_rejects_beyond_its_scratch(sd):
+    """specdec_step_noalloc refuses, before any HIP call, a step whose
+    verification needs more than the library's scratch, and names the limit."""
+    _no_gpu()
+    limit = int(re.search(r"#define SPECDEC_NOALLOC_SCRATCH_BYTES (\d+)", HEADER).group(1))
+    src, dst = _kv(sd, B=16384), _kv(sd, data=A + (1 << 30), B=16384)
+    B, k, V = 16384, 7, 128256
+    assert sd.workspace_bytes(B, k, V) > limit
+    r = sd.lib.specdec_step_noalloc(LG, 1, DR, PI, B, k, V, 16, ctypes.byref(src), ctypes.byref(dst), TK, NA, BO,
+                                    PO, WN, POS, MSK, 64, None, 0, None, 0, -1, None, None, None)
+    assert r == sd.ERR_WORKSPACE
+    msg = sd.lib.specdec_last_error().decode()
+    assert str(limit) in msg and "specdec_step_noalloc" in msg
+    # an empty batch needs no scratch and returns before any device call
+    src, dst = _kv(sd, B=0), _kv(sd, data=A + (1 << 30), B=0)
+    assert sd.lib.specdec_step_noalloc(None, 1, None, None, 0, 3, 100, 10, ctypes.byref(src), ctypes.byref(dst),
+                                       None, None, None, None, None, None, None, 64, None, 0, None, 0, -1, None,
+                                       None, None) == 0
+
+
 def test_realign_tokens_rejects(sd):
     _no_gpu()
     f = sd.lib.specdec_realign_tokens
