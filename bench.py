@@ -18,6 +18,7 @@ the CPU oracle timed on a bounded sample of the same step.
   python bench.py --verify sample [--temperature T]
   python bench.py --path varlen        # Family B rollback of a flat cache
   python bench.py --path chained       # 16 chained in-place steps (per-step times)
+  python bench.py --path verify [--workload NAME]   # greedy verification alone, cold and warm caches
   python bench.py --copy-calibration GIB   # plain device copy, for counter scaling
 
 ``--path exspec`` measures EXSpec's step instead (Algorithm 2 without the
@@ -46,6 +47,7 @@ METRIC = "verify+realign steps/s and achieved HBM GB/s (% peak), B=8 7B-shaped K
 METRIC_EXSPEC = "EXSpec gather+verify+write-back steps/s and achieved HBM GB/s (% peak), B=8 7B-shaped KV"
 METRIC_SAMPLE = "stochastic verify+realign steps/s and achieved HBM GB/s (% peak), B=8 7B-shaped KV"
 METRIC_VARLEN = "variable-length rollback steps/s and achieved HBM GB/s (% peak), B=8 7B-shaped KV"
+METRIC_VERIFY = "greedy verification calls/s from cold caches and achieved HBM GB/s (% peak) of the vocabulary scan"
 CSRC = ROOT / "paper_2510_22876_amd" / "csrc"
 KERNEL_SRCS = [CSRC / f for f in ("specdec_kernels.hip", "span_copy.h", "posmask.h")]
 GATHER_SRCS = [CSRC / f for f in ("exspec_kernels.hip", "span_copy.h", "posmask.h")]
@@ -471,6 +473,109 @@ def bench_varlen(args, w):
     print(json.dumps(line), flush=True)
 
 
+def cpu_baseline_verify(w, logits, draft, pad_in, W_in, budget_s):
+    """The oracle's greedy verification (every logit row) on one host thread,
+    called until ``budget_s`` seconds have passed (at least once)."""
+    import oracle
+    lg = logits.cpu()
+    dr = draft.cpu().numpy()
+    t0 = time.perf_counter()
+    calls = 0
+    while True:
+        oracle.verify(lg, w.logit_dtype, dr, pad_in, W_in)
+        calls += 1
+        if time.perf_counter() - t0 >= budget_s:
+            break
+    wall = time.perf_counter() - t0
+    return dict(value=calls / wall, unit="calls/s", cores=1, kind="oracle", cpu_model=cpu_model(),
+                sample=f"{calls} whole oracle verifications ({w.B * (w.k + 1)} logit rows each) in {wall:.2f} s")
+
+
+def bench_verify(args, w):
+    """Greedy verification alone (Algorithm 3 and Eq. (1)-(2): the two
+    launches of specdec_verify_greedy) on the workload's logits.  Cold: before
+    every timed call a 1 GiB buffer is read (a reduction outside the events),
+    which evicts the 256 MB Infinity Cache and the L2s without leaving dirty
+    lines behind, so the scan reads its logits from HBM.  Warm: before every
+    call the GPU only waits (a bounded sleep kernel), so logits that fit the
+    Infinity Cache stay there.  Either way the call is queued behind a
+    kernel of some hundred microseconds, so the events time the GPU's work
+    and not the host's submission.  The roofline is the scan kernel's (events
+    around its launch alone); the line's value is cold calls per second of
+    event time."""
+    import torch
+    from paper_2510_22876_amd import specdec as sd
+    from paper_2510_22876_amd import workloads as wl
+
+    n, W_in, pad_in, cap = wl.initial_geometry(w, args.seed)
+    logits, draft, *_ = wl.logits_and_drafts(w, args.seed, 0, device="cuda")
+    bufs = sd.StepBuffers(w.B, w.k, w.V, 8, "cuda")
+    pad_t = torch.as_tensor(pad_in, device="cuda")
+    evict = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+    desc = (f"{w.name} verification: B={w.B} k={w.k} V={w.V} {w.logit_dtype} logits "
+            f"({w.B * (w.k + 1) * w.V * w.logit_bytes / 1e6:.2f} MB), W_in={W_in}")
+    log(f"[bench] verify: {desc}")
+
+    def call():
+        sd.specdec_verify_greedy(logits, draft, pad_t, W_in, bufs.tokens, bufs.n_acc, bufs.bonus, bufs.pad_out,
+                                 bufs.w_new, bufs.workspace, bufs.dev_status)
+
+    for _ in range(args.warmup):
+        call()
+    torch.cuda.synchronize()
+    if int(bufs.dev_status.cpu()[0]) != 0:
+        raise RuntimeError("device flagged invalid values")
+    K = args.steps
+    mask = (1 << sd.KERNEL_VERIFY) | (1 << sd.KERNEL_VERIFY_SCAN)
+
+    evict.fill_(1)
+    sink = torch.empty(K, dtype=torch.int64, device="cuda")
+
+    def timed_calls(cold: bool):
+        sd.timing_reset()
+        sd.timing_enable(mask)
+        for i in range(K):
+            if cold:
+                torch.sum(evict, dim=0, dtype=torch.int64, out=sink[i])
+            else:
+                torch.cuda._sleep(1 << 20)
+            call()
+        torch.cuda.synchronize()
+        sd.timing_enable(False)
+        v_ms, v_n = sd.timing_query(sd.KERNEL_VERIFY)
+        s_ms, s_n = sd.timing_query(sd.KERNEL_VERIFY_SCAN)
+        assert v_n == K and s_n == K
+        return v_ms / K, s_ms / K
+
+    warm_ms, warm_scan_ms = timed_calls(False)
+    cold_ms, cold_scan_ms = timed_calls(True)
+    by = step_bytes(w, pad_in, W_in, bufs.n_acc.cpu().numpy(), int(bufs.w_new.cpu()[0]), "oop", False)
+    scan_bytes = w.B * (w.k + 1) * w.V * w.logit_bytes
+    achieved = scan_bytes / (cold_scan_ms * 1e-3) / 1e9
+    traffic, traffic_src = read_traffic_summary(w.name, "cold", scan_bytes, kernel="verifyscan")
+    log(f"[bench] verify cold {cold_ms * 1e3:.2f} us (scan {cold_scan_ms * 1e3:.2f} us, {achieved:.0f} GB/s), "
+        f"warm {warm_ms * 1e3:.2f} us (scan {warm_scan_ms * 1e3:.2f} us); traffic: {traffic_src}")
+    cpu = None
+    if args.cpu_baseline_seconds > 0:
+        cpu = cpu_baseline_verify(w, logits, draft, pad_in, W_in, args.cpu_baseline_seconds)
+        log(f"[bench] cpu baseline: {cpu['value']:.2f} calls/s ({cpu['sample']})")
+    line = {
+        "metric": METRIC_VERIFY, "value": 1e3 / cold_ms, "unit": "calls/s", "n_gpus": 1, "steps": K,
+        "warmup": args.warmup, "ms_per_step": cold_ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": w.logit_dtype, "data": "synthetic",
+        "config": {"workload": desc, "B": w.B, "k": w.k, "V": w.V, "seed": args.seed,
+                   "verify_cold_ms": round(cold_ms, 5), "verify_warm_ms": round(warm_ms, 5),
+                   "scan_cold_ms": round(cold_scan_ms, 5), "scan_warm_ms": round(warm_scan_ms, 5),
+                   "scan_warm_GBps": round(scan_bytes / (warm_scan_ms * 1e-3) / 1e9, 1),
+                   "verify_bytes": by["verify"], "eviction_bytes": evict.numel()},
+        "roofline": {"bound": "hbm", "kernel": "verify_partial (vocabulary scan), cold caches",
+                     "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic, "algorithmic_bytes": scan_bytes},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
 def cpu_baseline_varlen(w, logits, draft, src, cu, budget_s):
     """The oracle, single-threaded, on a bounded sample of the Family B step:
     verification over every logit row, then the compaction of one-layer slabs
@@ -648,11 +753,14 @@ def main():
     ap.add_argument("--verify", choices=["greedy", "sample"], default="greedy",
                     help="greedy verification (default) or stochastic verification by speculative sampling")
     ap.add_argument("--temperature", type=float, default=1.0, help="--verify sample: the sampling temperature")
-    ap.add_argument("--path", choices=["eqspec", "exspec", "varlen", "chained"], default="eqspec",
+    ap.add_argument("--path", choices=["eqspec", "exspec", "varlen", "chained", "verify"], default="eqspec",
                     help="eqspec: the verify + realign step (default); exspec: gather + verify + write-back; "
                          "varlen: Family B rollback; chained: in-place steps along a chain (per-step times)")
     ap.add_argument("--exspec-batch", choices=["ragged", "same"], default="ragged",
                     help="exspec: a batch of prompt-distributed lengths (unpad-repad) or one length (concatenation)")
+    ap.add_argument("--noalloc", action="store_true",
+                    help="greedy steps through specdec_step_noalloc (library scratch; one-launch verification "
+                         "for small batches)")
     ap.add_argument("--graph", action="store_true",
                     help="capture the step in a HIP graph once and replay it in the timed loop")
     ap.add_argument("--copy-ceiling", type=int, choices=[0, 1], default=1,
@@ -684,6 +792,9 @@ def main():
         return
     if args.path == "varlen":
         bench_varlen(args, w)
+        return
+    if args.path == "verify":
+        bench_verify(args, w)
         return
     if args.path == "chained":
         bench_chained(args, w if w.steps > 1 else wl.WORKLOADS["vicuna7b_chained"])
@@ -721,6 +832,10 @@ def main():
             sd.specdec_step_sample(logits, draft_logits, draft, pad_t, u_accept, u_sample, args.temperature, W_in,
                                    src, dst, bufs.tokens, bufs.n_acc, bufs.bonus, bufs.pad_out, bufs.w_new, bufs.pos,
                                    bufs.mask, sws, bufs.dev_status, s_in=s_in, s_out=s_out, pad_id=-1)
+        elif args.noalloc:
+            sd.specdec_step_noalloc(logits, draft, pad_t, W_in, src, dst, bufs.tokens, bufs.n_acc, bufs.bonus,
+                                    bufs.pad_out, bufs.w_new, bufs.pos, bufs.mask, bufs.dev_status, s_in=s_in,
+                                    s_out=s_out, pad_id=-1)
         else:
             sd.specdec_step(logits, draft, pad_t, W_in, src, dst, bufs.tokens, bufs.n_acc, bufs.bonus, bufs.pad_out,
                             bufs.w_new, bufs.pos, bufs.mask, bufs.workspace, bufs.dev_status, s_in=s_in, s_out=s_out,
@@ -787,7 +902,8 @@ def main():
     # durations (and the realign kernel's when it was not timed above)
     sd.timing_reset()
     vkern = sd.KERNEL_SAMPLE if sample else sd.KERNEL_VERIFY
-    sd.timing_enable((1 << vkern) | (0 if timers else 1 << sd.KERNEL_REALIGN))
+    scan_bit = 0 if sample else 1 << sd.KERNEL_VERIFY_SCAN
+    sd.timing_enable((1 << vkern) | scan_bit | (0 if timers else 1 << sd.KERNEL_REALIGN))
     for _ in range(K):
         if pristine is not None:
             restore()
@@ -795,6 +911,7 @@ def main():
     torch.cuda.synchronize()
     sd.timing_enable(False)
     verify_ms, verify_n = sd.timing_query(vkern)
+    scan_ms, scan_n = sd.timing_query(sd.KERNEL_VERIFY_SCAN)
     if pristine is None:
         # the per-step distribution: events around each step of a third,
         # back-to-back pass
@@ -853,11 +970,12 @@ def main():
                                                  f"target + N(0,1), drafts drawn from q" if sample else ""),
             "B": w.B, "k": w.k, "V": w.V, "L": w.L, "H": w.H, "D": w.D, "W_in": W_in, "w_new": w_new,
             "variant": variant, "seed": args.seed, "token_row": token_row, "verify": args.verify,
-            "graph": bool(args.graph),
+            "graph": bool(args.graph), "noalloc": bool(args.noalloc),
             **({"temperature": args.temperature, "draft_noise": 1.0} if sample else {}),
             "step_GBps": round(step_gbs, 1),
             "step_bytes": realign_bytes + by["verify"],
             "verify_ms": round(verify_avg_ms, 5),
+            **({"verify_scan_ms": round(scan_ms / scan_n, 5)} if scan_n else {}),
             "realign_ms": round(realign_avg_ms, 5),
             **percentiles(step_ms),
         },

@@ -291,18 +291,29 @@ specdec_status_t specdec_step(const void* logits, int32_t dtype, const int32_t* 
  * that forbid allocation).  Same arguments, outputs and checks as
  * specdec_step, minus workspace / workspace_bytes.
  *
- * Verification's partial maxima live in a library-owned device array of
+ * The step's scratch is a library-owned device array of
  * SPECDEC_NOALLOC_SCRATCH_BYTES, one copy per device, held until the process
  * ends; its address is looked up once per device (on the first call with
- * that device current) and nothing is allocated or freed, ever.  A step whose
- * verification needs more scratch than that (specdec_workspace_bytes(B, k, V)
- * > SPECDEC_NOALLOC_SCRATCH_BYTES) is rejected with SPECDEC_ERR_WORKSPACE
- * before anything is enqueued.  The stream must belong to the current device
- * (SPECDEC_ERR_INVALID_ARGUMENT otherwise).  Every call on one device shares
- * that device's scratch, so calls on one device that may overlap in time (on
- * different streams, or graph replays running concurrently) race and give
- * unspecified results; order them.  The scratch needs no initialisation: each
- * call writes every slot it reads before reading it.
+ * that device current, which also enqueues one kernel that clears the
+ * array's completion counts) and nothing is allocated or freed, ever.
+ *
+ * Batches of at most 4096 logit rows (B*(k+1)) of at most 16 KB each
+ * (V*4 bytes for f32, V*2 for bf16 / f16) verify in ONE launch: a workgroup
+ * per row, and the last row of a sequence, then the last sequence, to finish
+ * merges (counted in the scratch; the realignment launch clears the counts
+ * again).  The step is then two launches.  Larger batches verify in the scan
+ * and merge launches of specdec_step, with the partial maxima in the
+ * scratch; one whose partial maxima need more than
+ * SPECDEC_NOALLOC_SCRATCH_BYTES - 64 KiB (specdec_workspace_bytes(B, k, V))
+ * is rejected with SPECDEC_ERR_WORKSPACE before anything is enqueued.  The
+ * outputs are the same bits as specdec_step's either way.
+ *
+ * The stream must belong to the current device (SPECDEC_ERR_INVALID_ARGUMENT
+ * otherwise).  Every call on one device shares that device's scratch, so
+ * calls on one device that may overlap in time (on different streams, or
+ * graph replays running concurrently) race and give unspecified results;
+ * order them.  A later step that runs alone is correct again: each step's
+ * realignment clears the counts it and any racing call left behind.
  */
 specdec_status_t specdec_step_noalloc(const void* logits, int32_t dtype, const int32_t* draft,
                                       const int32_t* pad_in, int32_t B, int32_t k, int32_t V,
@@ -550,8 +561,9 @@ specdec_status_t specdec_varlen_rollback(const specdec_varlen_t* src, const spec
  * specdec_timing_query waits for the recorded events, adds their durations to
  * the totals of `kernel` (0 = verify, 1 = realign, with the fused position ids
  * / mask in specdec_step, 2 = position ids / mask alone, 3 = batch gather,
- * 4 = write-back, 5 = stochastic verification, 6 = variable-length rollback)
- * and returns the totals since the last reset.
+ * 4 = write-back, 5 = stochastic verification, 6 = variable-length rollback,
+ * 7 = the vocabulary scan of greedy verification alone, the first of its two
+ * launches) and returns the totals since the last reset.
  */
 #define SPECDEC_KERNEL_VERIFY 0
 #define SPECDEC_KERNEL_REALIGN 1
@@ -560,7 +572,8 @@ specdec_status_t specdec_varlen_rollback(const specdec_varlen_t* src, const spec
 #define SPECDEC_KERNEL_WRITEBACK 4
 #define SPECDEC_KERNEL_SAMPLE 5
 #define SPECDEC_KERNEL_VARLEN 6
-#define SPECDEC_TIMING_ALL 127
+#define SPECDEC_KERNEL_VERIFY_SCAN 7
+#define SPECDEC_TIMING_ALL 255
 specdec_status_t specdec_timing_enable(int32_t kernel_mask);
 specdec_status_t specdec_timing_reset(void);
 specdec_status_t specdec_timing_query(int32_t kernel, double* total_ms, int64_t* launches);

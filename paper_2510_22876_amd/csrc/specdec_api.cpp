@@ -69,7 +69,7 @@ int logit_bytes(int32_t dtype) {
 
 // ---- kernel timers -------------------------------------------------------------
 
-constexpr int kTimedKernels = 7;
+constexpr int kTimedKernels = 8;
 
 struct TimedLaunch {
   int kernel;
@@ -176,6 +176,15 @@ specdec_status_t check_disjoint(std::initializer_list<Region> inputs, std::initi
 }
 
 int64_t clamp_bytes(size_t n) { return n > static_cast<size_t>(INT64_MAX) ? INT64_MAX : static_cast<int64_t>(n); }
+
+// Greedy verification's two launches, timed as a whole (SPECDEC_KERNEL_VERIFY)
+// and the vocabulary scan alone (SPECDEC_KERNEL_VERIFY_SCAN).
+hipError_t verify_launches(const specdec::VerifyLaunch& p, hipStream_t st) {
+  return timed(SPECDEC_KERNEL_VERIFY, st, [&] {
+    const hipError_t r = timed(SPECDEC_KERNEL_VERIFY_SCAN, st, [&] { return specdec::launch_verify_scan(p, st); });
+    return r != hipSuccess ? r : specdec::launch_verify_finalize(p, st);
+  });
+}
 
 specdec_status_t check_verify_args(const void* logits, int32_t dtype, const int32_t* draft,
                                    const int32_t* pad_in, int32_t B, int32_t k, int32_t V, int32_t W_in,
@@ -433,8 +442,10 @@ specdec_status_t step_realign(int32_t k, int32_t W_in, const specdec_kv_t* src, 
                               const int32_t* pad_out, const int32_t* w_new, int64_t* pos, uint8_t* mask,
                               int64_t pm_cap, const int32_t* s_in, int64_t s_in_stride, int32_t* s_out,
                               int64_t s_out_stride, int32_t pad_id, uint32_t* dev_status, int32_t* w_new_host,
-                              hipStream_t st) {
+                              hipStream_t st, uint32_t* clear_words = nullptr, uint32_t clear_count = 0) {
   specdec::RealignLaunch rp{};
+  rp.clear_words = clear_words;
+  rp.clear_count = clear_count;
   rp.src = src->data;
   rp.dst = dst->data;
   rp.src_cap = src->cap;
@@ -545,7 +556,7 @@ specdec_status_t specdec_verify_greedy(const void* logits, int32_t dtype, const 
   specdec::VerifyLaunch p{logits, dtype, draft, pad_in, B, k, V, W_in, tokens, n_acc,
                           bonus, pad_out, w_new, workspace, dev_status};
   hipStream_t st = static_cast<hipStream_t>(stream);
-  hipError_t e = timed(SPECDEC_KERNEL_VERIFY, st, [&] { return specdec::launch_verify(p, st); });
+  hipError_t e = verify_launches(p, st);
   if (e != hipSuccess) return hip_fail(e, "verify launch");
   return ok();
 }
@@ -674,13 +685,19 @@ specdec_status_t specdec_realign_tokens(const int32_t* s_in, int64_t s_in_stride
   return ok();
 }
 
-specdec_status_t specdec_step(const void* logits, int32_t dtype, const int32_t* draft, const int32_t* pad_in,
-                              int32_t B, int32_t k, int32_t V, int32_t W_in, const specdec_kv_t* src,
-                              const specdec_kv_t* dst, int32_t* tokens, int32_t* n_acc, int32_t* bonus,
-                              int32_t* pad_out, int32_t* w_new, int64_t* pos, uint8_t* mask, int64_t pm_cap,
-                              const int32_t* s_in, int64_t s_in_stride, int32_t* s_out, int64_t s_out_stride,
-                              int32_t pad_id, void* workspace, size_t workspace_bytes, uint32_t* dev_status,
-                              int32_t* w_new_host, void* stream) {
+namespace {
+
+// The fused step.  With `fused_counts` (library scratch whose B + 1 counts are
+// zero) verification runs as one launch and the realignment launch zeroes
+// the counts again; otherwise verification is the scan and merge launches on
+// the caller's workspace.
+specdec_status_t step_greedy(const void* logits, int32_t dtype, const int32_t* draft, const int32_t* pad_in, int32_t B,
+                             int32_t k, int32_t V, int32_t W_in, const specdec_kv_t* src, const specdec_kv_t* dst,
+                             int32_t* tokens, int32_t* n_acc, int32_t* bonus, int32_t* pad_out, int32_t* w_new,
+                             int64_t* pos, uint8_t* mask, int64_t pm_cap, const int32_t* s_in, int64_t s_in_stride,
+                             int32_t* s_out, int64_t s_out_stride, int32_t pad_id, void* workspace,
+                             size_t workspace_bytes, uint32_t* dev_status, int32_t* w_new_host, void* stream,
+                             uint32_t* fused_counts) {
   specdec_status_t s = check_verify_args(logits, dtype, draft, pad_in, B, k, V, W_in, tokens, n_acc, bonus,
                                          pad_out, w_new, workspace, workspace_bytes, dev_status);
   if (s) return s;
@@ -699,24 +716,48 @@ specdec_status_t specdec_step(const void* logits, int32_t dtype, const int32_t* 
   hipStream_t st = static_cast<hipStream_t>(stream);
   specdec::VerifyLaunch vp{logits, dtype, draft, pad_in, B, k, V, W_in, tokens, n_acc,
                            bonus, pad_out, w_new, workspace, dev_status};
-  hipError_t e = timed(SPECDEC_KERNEL_VERIFY, st, [&] { return specdec::launch_verify(vp, st); });
+  hipError_t e = fused_counts ? timed(SPECDEC_KERNEL_VERIFY, st, [&] {
+    return timed(SPECDEC_KERNEL_VERIFY_SCAN, st, [&] { return specdec::launch_verify_fused(vp, fused_counts, st); });
+  })
+                              : verify_launches(vp, st);
   if (e != hipSuccess) return hip_fail(e, "verify launch");
   return step_realign(k, W_in, src, dst, in_place, pad_in, tokens, n_acc, pad_out, w_new, pos, mask, pm_cap, s_in,
-                      s_in_stride, s_out, s_out_stride, pad_id, dev_status, w_new_host, st);
+                      s_in_stride, s_out, s_out_stride, pad_id, dev_status, w_new_host, st, fused_counts,
+                      fused_counts ? static_cast<uint32_t>(B) + 1u : 0u);
+}
+
+}  // namespace
+
+specdec_status_t specdec_step(const void* logits, int32_t dtype, const int32_t* draft, const int32_t* pad_in,
+                              int32_t B, int32_t k, int32_t V, int32_t W_in, const specdec_kv_t* src,
+                              const specdec_kv_t* dst, int32_t* tokens, int32_t* n_acc, int32_t* bonus,
+                              int32_t* pad_out, int32_t* w_new, int64_t* pos, uint8_t* mask, int64_t pm_cap,
+                              const int32_t* s_in, int64_t s_in_stride, int32_t* s_out, int64_t s_out_stride,
+                              int32_t pad_id, void* workspace, size_t workspace_bytes, uint32_t* dev_status,
+                              int32_t* w_new_host, void* stream) {
+  return step_greedy(logits, dtype, draft, pad_in, B, k, V, W_in, src, dst, tokens, n_acc, bonus, pad_out, w_new, pos,
+                     mask, pm_cap, s_in, s_in_stride, s_out, s_out_stride, pad_id, workspace, workspace_bytes,
+                     dev_status, w_new_host, stream, nullptr);
 }
 
 // ---- specdec_step_noalloc: the fused step on library-owned scratch -----------
 //
-// Verification's partial maxima live in `scratch`, a file-scope device array.
-// Each device the library runs on holds its own copy until the process ends.
-// In host code the name only identifies the symbol (it is not a device
+// The step's scratch lives in `scratch`, a file-scope device array.  Each
+// device the library runs on holds its own copy until the process ends.  In
+// host code the name only identifies the symbol (it is not a device
 // address): the device address of each device's copy is taken once, with
 // that device current, by hipGetSymbolAddress, and only that address is ever
-// handed to a kernel.
+// handed to a kernel.  Layout: the partial maxima of the two-launch
+// verification from the start, and, in the last kCountsBytes, the completion
+// counts of the one-launch verification, zeroed when the address is first
+// taken and zeroed again by every step's realignment launch.
 static __device__ __align__(256) unsigned char scratch[SPECDEC_NOALLOC_SCRATCH_BYTES];
 
 namespace {
 
+constexpr size_t kCountsBytes = 64 * 1024;   // 2 * kMaxFusedVerifyRows + 1 words and then some
+static_assert((2 * specdec::kMaxFusedVerifyRows + 1) * 4 <= static_cast<int64_t>(kCountsBytes), "counts fit");
+constexpr size_t kPartialBytes = SPECDEC_NOALLOC_SCRATCH_BYTES - kCountsBytes;
 constexpr int kMaxScratchDevices = 256;
 std::mutex g_scratch_mu;
 void* g_scratch_addr[kMaxScratchDevices] = {};
@@ -742,6 +783,10 @@ specdec_status_t device_scratch(hipStream_t stream, void** out) {
     e = hipGetSymbolAddress(&addr, HIP_SYMBOL(scratch));
     if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
     if (!addr) return fail(SPECDEC_ERR_HIP, "hipGetSymbolAddress(scratch) returned NULL");
+    // the one-launch verification's counts start at zero (a kernel, not a
+    // memset, so that a first call under graph capture records no memset node)
+    e = specdec::launch_zero(static_cast<char*>(addr) + kPartialBytes, kCountsBytes, stream);
+    if (e != hipSuccess) return hip_fail(e, "scratch count clear");
     g_scratch_addr[dev] = addr;
   }
   *out = g_scratch_addr[dev];
@@ -758,20 +803,23 @@ specdec_status_t specdec_step_noalloc(const void* logits, int32_t dtype, const i
                                       int32_t pad_id, uint32_t* dev_status, int32_t* w_new_host, void* stream) {
   void* ws = nullptr;
   size_t ws_bytes = 0;
+  uint32_t* counts = nullptr;
   if (B > 0) {
+    const bool fused = specdec::verify_fused_fits(B, k, V, dtype);
     const size_t need = specdec_workspace_bytes(B, k, V);
-    if (need > SPECDEC_NOALLOC_SCRATCH_BYTES)
+    if (!fused && need > kPartialBytes)
       return fail(SPECDEC_ERR_WORKSPACE,
                   "specdec_step_noalloc: verification of B=%d, k=%d, V=%d needs %zu bytes of scratch, more than the "
-                  "library's %d (use specdec_step with a workspace)",
-                  B, k, V, need, SPECDEC_NOALLOC_SCRATCH_BYTES);
+                  "library's %zu of %d (use specdec_step with a workspace)",
+                  B, k, V, need, kPartialBytes, SPECDEC_NOALLOC_SCRATCH_BYTES);
     const specdec_status_t s = device_scratch(static_cast<hipStream_t>(stream), &ws);
     if (s) return s;
-    ws_bytes = SPECDEC_NOALLOC_SCRATCH_BYTES;
+    ws_bytes = kPartialBytes;
+    if (fused) counts = reinterpret_cast<uint32_t*>(static_cast<char*>(ws) + kPartialBytes);
   }
-  return specdec_step(logits, dtype, draft, pad_in, B, k, V, W_in, src, dst, tokens, n_acc, bonus, pad_out, w_new, pos,
-                      mask, pm_cap, s_in, s_in_stride, s_out, s_out_stride, pad_id, ws, ws_bytes, dev_status,
-                      w_new_host, stream);
+  return step_greedy(logits, dtype, draft, pad_in, B, k, V, W_in, src, dst, tokens, n_acc, bonus, pad_out, w_new, pos,
+                     mask, pm_cap, s_in, s_in_stride, s_out, s_out_stride, pad_id, ws, ws_bytes, dev_status,
+                     w_new_host, stream, counts);
 }
 
 specdec_status_t specdec_step_sample(const void* logits, const void* draft_logits, int32_t dtype,

@@ -48,6 +48,9 @@ struct RealignLaunch {
   int64_t s_in_stride, s_out_stride;
   const int32_t* tokens;
   int32_t pad_id;
+  // words the launch zeroes in one extra workgroup (NULL: none)
+  uint32_t* clear_words = nullptr;
+  uint32_t clear_count = 0;
 };
 
 struct PosmaskLaunch {
@@ -183,6 +186,21 @@ void clear_last_error();
 int64_t max_launch_items();
 
 hipError_t launch_verify(const VerifyLaunch& p, hipStream_t stream);
+// The two launches of launch_verify: the vocabulary scan (partial maxima),
+// then the one-workgroup merge (tokens, accepted counts, width, paddings).
+hipError_t launch_verify_scan(const VerifyLaunch& p, hipStream_t stream);
+hipError_t launch_verify_finalize(const VerifyLaunch& p, hipStream_t stream);
+// Greedy verification in one launch (one workgroup per logit row): for
+// batches of at most kMaxFusedVerifyRows rows of at most
+// kMaxFusedVerifyRowBytes bytes each (verify_fused_fits).  `counts` holds
+// 1 + 2 * kMaxFusedVerifyRows words: the batch completion count, the B
+// per-sequence counts, then (from word 1 + kMaxFusedVerifyRows) the new
+// lengths.  The first B + 1 words must be zero on entry and are left
+// non-zero.
+constexpr int64_t kMaxFusedVerifyRows = 4096;
+constexpr int64_t kMaxFusedVerifyRowBytes = 16 * 1024;
+bool verify_fused_fits(int64_t B, int64_t k, int64_t V, int dtype);
+hipError_t launch_verify_fused(const VerifyLaunch& p, uint32_t* counts, hipStream_t stream);
 hipError_t launch_realign(const RealignLaunch& p, hipStream_t stream);
 hipError_t launch_posmask(const PosmaskLaunch& p, hipStream_t stream);
 // Token row only (RealignLaunch's cache fields are ignored).

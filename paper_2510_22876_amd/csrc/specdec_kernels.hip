@@ -166,13 +166,30 @@ struct VerifyArgs {
   int32_t chunks;               // workgroups per logit row
 };
 
+// Tunables of the vocabulary scan (compile-time; chosen by sweeping on
+// MI355X with the logits read from HBM):
+//   SPECDEC_VERIFY_UNROLL     16-byte loads per thread in flight per iteration
+//   SPECDEC_VERIFY_TARGET     workgroups the scan aims for in total
+//   SPECDEC_VERIFY_MIN_CHUNK / SPECDEC_VERIFY_MAX_CHUNK  logits per workgroup
+#ifndef SPECDEC_VERIFY_UNROLL
+#define SPECDEC_VERIFY_UNROLL 4
+#endif
+#ifndef SPECDEC_VERIFY_TARGET
+#define SPECDEC_VERIFY_TARGET 2048
+#endif
+#ifndef SPECDEC_VERIFY_MIN_CHUNK
+#define SPECDEC_VERIFY_MIN_CHUNK 2048
+#endif
+#ifndef SPECDEC_VERIFY_MAX_CHUNK
+#define SPECDEC_VERIFY_MAX_CHUNK 16384
+#endif
+
 // Scan logit elements [beg, end) of one row; 16-byte vectors over the aligned
 // interior, single elements for the unaligned head and the tail.
-template <int DT>
+template <int DT, int kTpb = kThreads, int kUnroll = SPECDEC_VERIFY_UNROLL>
 __device__ __forceinline__ void scan_range(const char* row, int64_t beg, int64_t end, Best& b) {
   using T = Logit<DT>;
   constexpr int kPerVec = 16 / T::kBytes;
-  constexpr int kUnroll = 4;
   const int tid = threadIdx.x;
   const uintptr_t addr = reinterpret_cast<uintptr_t>(row) + static_cast<uintptr_t>(beg) * T::kBytes;
   int64_t head = static_cast<int64_t>((16u - (addr & 15u)) & 15u) / T::kBytes;
@@ -188,16 +205,16 @@ __device__ __forceinline__ void scan_range(const char* row, int64_t beg, int64_t
     uint32_t vk = 0u;
     int32_t ve = -1;
     uint4 vq = make_uint4(0u, 0u, 0u, 0u);
-    for (int64_t v0 = 0; v0 < nvec; v0 += kThreads * kUnroll) {
+    for (int64_t v0 = 0; v0 < nvec; v0 += kTpb * kUnroll) {
       uint4 q[kUnroll];
 #pragma unroll
       for (int u = 0; u < kUnroll; ++u) {
-        const int64_t v = v0 + u * kThreads + tid;
+        const int64_t v = v0 + u * kTpb + tid;
         q[u] = v < nvec ? vp[v] : make_uint4(0u, 0u, 0u, 0u);
       }
 #pragma unroll
       for (int u = 0; u < kUnroll; ++u) {
-        const int64_t v = v0 + u * kThreads + tid;
+        const int64_t v = v0 + u * kTpb + tid;
         const uint32_t k = T::vec_key(q[u]);
         if (v < nvec && k > vk) {
           vk = k;
@@ -208,16 +225,16 @@ __device__ __forceinline__ void scan_range(const char* row, int64_t beg, int64_t
     }
     if (ve >= 0) T::take_in_vec(b, vq, vk, ve);
   } else {
-    for (int64_t v0 = 0; v0 < nvec; v0 += kThreads * kUnroll) {
+    for (int64_t v0 = 0; v0 < nvec; v0 += kTpb * kUnroll) {
       uint4 q[kUnroll];
 #pragma unroll
       for (int u = 0; u < kUnroll; ++u) {
-        const int64_t v = v0 + u * kThreads + tid;
+        const int64_t v = v0 + u * kTpb + tid;
         q[u] = v < nvec ? vp[v] : make_uint4(0u, 0u, 0u, 0u);
       }
 #pragma unroll
       for (int u = 0; u < kUnroll; ++u) {
-        const int64_t v = v0 + u * kThreads + tid;
+        const int64_t v = v0 + u * kTpb + tid;
         if (v < nvec) T::take_vec(b, q[u], static_cast<int32_t>(a0 + v * kPerVec));
       }
     }
@@ -303,6 +320,107 @@ __global__ __launch_bounds__(kFinalizeThreads) void verify_finalize_kernel(Verif
   if (threadIdx.x == 0) a.w_new[0] = w;
 }
 
+// One launch of greedy verification for batches whose logit rows are short
+// enough for one workgroup each (used where the library owns the scratch and
+// so knows its counters start at zero).  Every workgroup scans one whole row
+// and writes its prediction; the last row of a sequence to finish (an
+// agent-scope acquire-release count per sequence) does that sequence's
+// prefix-match scan, bonus token and new length; the last sequence to finish
+// (one more count) computes the width and the paddings.  A release fence
+// costs a serialized L2 write-back on this GPU (about 19 ns each, measured),
+// so the design keeps one count per row and one per sequence, never one per
+// chunk of a row.  No workgroup waits for another: each one counts and either
+// exits or, being last, carries on.
+struct FusedVerifyArgs {
+  VerifyArgs v;
+  uint32_t* seq_count;    // [B], zero on entry
+  uint32_t* batch_count;  // [1], zero on entry
+  int32_t* lens;          // [B] new lengths (0 for a row with a bad pad_in)
+};
+
+constexpr int kFusedThreads = 1024, kFusedUnroll = 8, kFusedWaves = kFusedThreads / 64;
+static_assert(kFusedThreads * kFusedUnroll * 16 >= 128 * 1024, "a fused row is one iteration of loads");
+
+template <int DT>
+__global__ __launch_bounds__(kFusedThreads) void verify_fused_kernel(FusedVerifyArgs f) {
+  const VerifyArgs& a = f.v;
+  __shared__ unsigned long long wkey[kFusedWaves];
+  __shared__ int32_t wmax[kFusedWaves];
+  __shared__ int seq_last, batch_last;   // one flag per stage: no wave reads a flag another stage rewrites
+  const int64_t row = blockIdx.x;
+  const int kp1 = a.k + 1;
+  const int i = static_cast<int>(row / kp1);
+  Best b;
+  scan_range<DT, kFusedThreads, kFusedUnroll>(a.logits + row * static_cast<int64_t>(a.V) * Logit<DT>::kBytes, 0,
+                                              a.V, b);
+  unsigned long long key =
+      (static_cast<unsigned long long>(b.key) << 32) | static_cast<uint32_t>(~static_cast<uint32_t>(b.idx));
+  key = wave_max_u64(key);
+  if ((threadIdx.x & 63) == 0) wkey[threadIdx.x >> 6] = key;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    unsigned long long k2 = wkey[0];
+#pragma unroll
+    for (int q = 1; q < kFusedWaves; ++q) k2 = wkey[q] > k2 ? wkey[q] : k2;
+    a.tokens[row] = static_cast<int32_t>(~static_cast<uint32_t>(k2 & 0xFFFFFFFFull));
+    const uint32_t before = __hip_atomic_fetch_add(f.seq_count + i, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+    seq_last = before == static_cast<uint32_t>(a.k);
+  }
+  __syncthreads();
+  if (!seq_last) return;
+  // the sequence's k+1 predictions are all written: wave 0 makes them visible
+  // to itself and loads them, and the drafts, at once (one lane per slot)
+  if (threadIdx.x < 64) {
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    const int lane = static_cast<int>(threadIdx.x);
+    const int32_t L = a.W_in - kp1;
+    const int32_t* tok = a.tokens + static_cast<int64_t>(i) * kp1;
+    const int32_t* dr = a.draft + static_cast<int64_t>(i) * a.k;
+    const int32_t t = lane <= a.k ? tok[lane] : 0;
+    const int32_t d = lane < a.k ? dr[lane] : 0;
+    const int32_t t_last = tok[a.k];                       // the prediction after the last draft (lane 64 for k = 64)
+    const unsigned long long miss = __ballot(lane < a.k && d != t);
+    const int32_t nacc = miss ? static_cast<int32_t>(__builtin_ctzll(miss)) : a.k;
+    const int32_t bon = __shfl(t, nacc < 64 ? nacc : 0);
+    if (lane == 0) {
+      const int32_t p = a.pad_in[i];
+      a.n_acc[i] = nacc;
+      if (a.bonus) a.bonus[i] = nacc < 64 ? bon : t_last;
+      const bool ok = p >= 0 && p <= L;
+      f.lens[i] = ok ? (L - p) + nacc + 1 : 0;           // 0: left out of the width, padding -1
+      if (!ok && a.dev_status) atomicOr(a.dev_status, kBadPadIn);
+      const uint32_t before = __hip_atomic_fetch_add(f.batch_count, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+      batch_last = before == static_cast<uint32_t>(a.B - 1);
+    }
+  }
+  __syncthreads();
+  if (!batch_last) return;
+  // every sequence's length is written; each wave makes them visible to
+  // itself, and one load of each length gives both the width and the padding
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+  constexpr int kPer = kMaxFusedVerifyRows / kFusedThreads;   // sequences per thread at most (B <= rows)
+  int32_t len[kPer];
+  int32_t local = 0;
+#pragma unroll
+  for (int j = 0; j < kPer; ++j) {
+    const int q = static_cast<int>(threadIdx.x) + j * kFusedThreads;
+    len[j] = q < a.B ? f.lens[q] : 0;
+    local = len[j] > local ? len[j] : local;
+  }
+  local = wave_max_i32(local);
+  if ((threadIdx.x & 63) == 0) wmax[threadIdx.x >> 6] = local;
+  __syncthreads();
+  int32_t w = wmax[0];
+#pragma unroll
+  for (int q = 1; q < kFusedWaves; ++q) w = wmax[q] > w ? wmax[q] : w;
+#pragma unroll
+  for (int j = 0; j < kPer; ++j) {
+    const int q = static_cast<int>(threadIdx.x) + j * kFusedThreads;
+    if (q < a.B) a.pad_out[q] = len[j] > 0 ? w - len[j] : -1;
+  }
+  if (threadIdx.x == 0) a.w_new[0] = w;
+}
+
 // ---------------------------------------------------------------------------
 // realign
 //
@@ -370,6 +488,9 @@ struct RealignArgs {
   const int32_t* tokens;                 // [B][k+1] predictions from verification
   int32_t pad_id;
   uint32_t tok_col_blocks;               // workgroups per token row (1 in place)
+  uint32_t tok_blocks;                   // token-row workgroups in all
+  uint32_t* clear_words;                 // one more workgroup zeroes these (NULL: none)
+  uint32_t clear_count;
 };
 
 struct RowGeom {
@@ -489,8 +610,10 @@ template <int kTpb>
 __device__ __forceinline__ void extra_block(const RealignArgs& a, uint32_t b) {
   if (b < a.pm_blocks)
     posmask_block<kTpb>(b, a.pos, a.mask, a.pad_out, a.w_new, a.k, a.pm_cap, a.pm_col_blocks, a.dev_status);
-  else
+  else if (b - a.pm_blocks < a.tok_blocks)
     token_block<kTpb>(a, b - a.pm_blocks);
+  else   // the completion counts of the one-launch verification that ran before
+    for (uint32_t q = threadIdx.x; q < a.clear_count; q += kTpb) a.clear_words[q] = 0u;
 }
 
 // Out of place: the output of a span is cut into groups of kPieces*kSplit
@@ -668,12 +791,15 @@ int64_t max_launch_items() {
 }
 
 int64_t verify_chunk_elems(int64_t rows, int64_t V) {
-  // about 2048 workgroups in total, each scanning 2048..16384 elements, and
-  // at most kMaxVerifyChunks workgroups per row
-  const int64_t per = (rows * V + 2047) / 2048;
-  int64_t c = ((per + 2047) / 2048) * 2048;
-  if (c < 2048) c = 2048;
-  if (c > 16384) c = 16384;
+  // about SPECDEC_VERIFY_TARGET workgroups in total, each scanning
+  // SPECDEC_VERIFY_MIN_CHUNK..SPECDEC_VERIFY_MAX_CHUNK elements (a multiple
+  // of the minimum), and at most kMaxVerifyChunks workgroups per row
+  constexpr int64_t kTarget = SPECDEC_VERIFY_TARGET, kMin = SPECDEC_VERIFY_MIN_CHUNK, kMax = SPECDEC_VERIFY_MAX_CHUNK;
+  static_assert(kMin % 8 == 0 && kMax % kMin == 0, "chunks are whole 16-byte vectors");
+  const int64_t per = (rows * V + kTarget - 1) / kTarget;
+  int64_t c = ((per + kMin - 1) / kMin) * kMin;
+  if (c < kMin) c = kMin;
+  if (c > kMax) c = kMax;
   int64_t min_c = (V + kMaxVerifyChunks - 1) / kMaxVerifyChunks;
   min_c = ((min_c + 7) / 8) * 8;
   if (c < min_c) c = min_c;
@@ -686,7 +812,7 @@ int64_t verify_chunks(int64_t rows, int64_t V) {
   return (V + c - 1) / c;
 }
 
-hipError_t launch_verify(const VerifyLaunch& p, hipStream_t stream) {
+static VerifyArgs verify_args(const VerifyLaunch& p) {
   VerifyArgs a;
   a.logits = static_cast<const char*>(p.logits);
   a.draft = p.draft;
@@ -705,17 +831,53 @@ hipError_t launch_verify(const VerifyLaunch& p, hipStream_t stream) {
   const int64_t rows = static_cast<int64_t>(p.B) * (p.k + 1);
   a.chunk_elems = verify_chunk_elems(rows, p.V);
   a.chunks = static_cast<int32_t>((p.V + a.chunk_elems - 1) / a.chunk_elems);
-  const int64_t blocks = rows * a.chunks;
+  return a;
+}
+
+hipError_t launch_verify_scan(const VerifyLaunch& p, hipStream_t stream) {
+  const VerifyArgs a = verify_args(p);
+  const int64_t blocks = static_cast<int64_t>(p.B) * (p.k + 1) * a.chunks;
   const dim3 grid(static_cast<uint32_t>(blocks)), block(kThreads);
   switch (p.dtype) {
     case 0: hipLaunchKernelGGL(verify_partial_kernel<0>, grid, block, 0, stream, a); break;
     case 1: hipLaunchKernelGGL(verify_partial_kernel<1>, grid, block, 0, stream, a); break;
     default: hipLaunchKernelGGL(verify_partial_kernel<2>, grid, block, 0, stream, a); break;
   }
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  return hipGetLastError();
+}
+
+hipError_t launch_verify_finalize(const VerifyLaunch& p, hipStream_t stream) {
+  const VerifyArgs a = verify_args(p);
   hipLaunchKernelGGL(verify_finalize_kernel, dim3(1), dim3(kFinalizeThreads), 0, stream, a);
   return hipGetLastError();
+}
+
+bool verify_fused_fits(int64_t B, int64_t k, int64_t V, int dtype) {
+  const int64_t eb = dtype == 0 ? 4 : 2;
+  return B >= 1 && B * (k + 1) <= kMaxFusedVerifyRows && V * eb <= kMaxFusedVerifyRowBytes;
+}
+
+hipError_t launch_verify_fused(const VerifyLaunch& p, uint32_t* counts, hipStream_t stream) {
+  FusedVerifyArgs f;
+  f.v = verify_args(p);
+  // the counts first (cleared after the call), the lengths above every count
+  // a batch of any size uses, so that no call's lengths land in another's counts
+  f.batch_count = counts;
+  f.seq_count = counts + 1;
+  f.lens = reinterpret_cast<int32_t*>(counts + 1 + kMaxFusedVerifyRows);
+  const dim3 grid(static_cast<uint32_t>(static_cast<int64_t>(p.B) * (p.k + 1))), block(kFusedThreads);
+  switch (p.dtype) {
+    case 0: hipLaunchKernelGGL(verify_fused_kernel<0>, grid, block, 0, stream, f); break;
+    case 1: hipLaunchKernelGGL(verify_fused_kernel<1>, grid, block, 0, stream, f); break;
+    default: hipLaunchKernelGGL(verify_fused_kernel<2>, grid, block, 0, stream, f); break;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_verify(const VerifyLaunch& p, hipStream_t stream) {
+  const hipError_t e = launch_verify_scan(p, stream);
+  if (e != hipSuccess) return e;
+  return launch_verify_finalize(p, stream);
 }
 
 static void fill_token_args(RealignArgs& a, const RealignLaunch& p, int tpb) {
@@ -726,6 +888,8 @@ static void fill_token_args(RealignArgs& a, const RealignLaunch& p, int tpb) {
   a.tokens = p.tokens;
   a.pad_id = p.pad_id;
   a.tok_col_blocks = 0;
+  a.clear_words = p.clear_words;
+  a.clear_count = p.clear_words ? p.clear_count : 0u;
   if (p.s_in) {
     const int64_t width = static_cast<int64_t>(p.W_in) + 1;   // L' + 1 <= W_in + 1
     a.tok_col_blocks = p.s_in == p.s_out ? 1u : static_cast<uint32_t>((width + 4 * tpb - 1) / (4 * tpb));
@@ -763,7 +927,8 @@ hipError_t launch_realign(const RealignLaunch& p, hipStream_t stream) {
   }
   fill_token_args(a, p, tpb);
   const int64_t tok_blocks = static_cast<int64_t>(a.tok_col_blocks) * p.B;
-  const int64_t extra = pm_blocks + tok_blocks;
+  a.tok_blocks = static_cast<uint32_t>(tok_blocks);
+  const int64_t extra = pm_blocks + tok_blocks + (a.clear_words ? 1 : 0);
   a.misaligned = !p.in_place && !split_spans_aligned<kOopVec, kOopSplit>(p.dst, a.dst_span_vecs);
   const int64_t chunks = p.in_place ? 1 : split_blocks<kOopVec, kOopTpb, kOopSplit>(
                                                 static_cast<int64_t>(p.W_in) * a.vpc, a.misaligned != 0);

@@ -24,7 +24,7 @@ def test_more_than_one_gpu_is_refused():
 def test_help_lists_the_paths():
     r = _run("--help")
     assert r.returncode == 0
-    for word in ("exspec", "varlen", "chained", "--verify", "--graph", "--variant"):
+    for word in ("exspec", "varlen", "chained", "verify", "--verify", "--graph", "--variant"):
         assert word in r.stdout, word
 
 
@@ -39,7 +39,8 @@ def test_traffic_comes_only_from_counters_of_the_same_step():
         alg = int(re.search(r"Algorithmic bytes per launch \(bench.py\):\s*(\d+)", text).group(1))
         hbm = float(re.search(r"hbm_bytes_per_launch:\s*([0-9.eE+]+)", text).group(1))
         kernel, variant, workload = path.name[:-len("_hbm_counters.md")].split("_")
-        srcs = {"realign": bench.KERNEL_SRCS, "gather": bench.GATHER_SRCS, "varlen": bench.VARLEN_SRCS}[kernel]
+        srcs = {"realign": bench.KERNEL_SRCS, "gather": bench.GATHER_SRCS, "varlen": bench.VARLEN_SRCS,
+                "verifyscan": bench.KERNEL_SRCS}[kernel]
         value, src = bench.read_traffic_summary(workload, variant, alg, kernel=kernel, srcs=srcs)
         if value is None:
             assert src == "kernel changed since the counters were taken", (path.name, src)

@@ -27,6 +27,8 @@ PATHS = [
     ["--path", "exspec"],
     ["--path", "exspec", "--exspec-batch", "same"],
     ["--path", "varlen"],
+    ["--path", "verify"],
+    ["--path", "verify", "--workload", "stress"],
 ]
 
 
@@ -50,7 +52,8 @@ def test_bench_line(args):
                 "scaling", "vs_baseline", "dtype", "data", "config", "roofline", "cpu_baseline"):
         assert key in d, key
     assert d["n_gpus"] == 1 and d["steps"] == 3 and d["warmup"] == 1
-    assert d["unit"] == "steps/s" and d["higher_is_better"] is True and d["dtype"] == "bf16"
+    unit = "calls/s" if "verify" in args and "--path" in args else "steps/s"
+    assert d["unit"] == unit and d["higher_is_better"] is True and d["dtype"] == "bf16"
     assert d["value"] > 0 and abs(d["value"] * d["ms_per_step"] - 1e3) < 1e-3
     assert "workload" in d["config"]
     if not args:

@@ -1,13 +1,18 @@
 """specdec_step_noalloc (the fused step on the library's own scratch, for
 callers that cannot allocate) against specdec_step with a caller workspace,
 through the C ABI: every output bit for bit, on consecutive calls that share
-the library scratch, the second with a smaller batch, vocabulary and cache.
-Both calls of a pair see identical input bytes and identically pre-filled
-output buffers."""
+the library scratch, each later one smaller.  The first two cases have
+logit rows longer than 16 KB (verification in the scan and merge launches,
+partial maxima in the scratch); the others verify in one launch (one
+workgroup per row, completion counted in the scratch), including planted
+ties, f16 logits, k = 0 and a row whose pad_in is out of range.  Both calls of a pair see
+identical input bytes and identically pre-filled output buffers, and the
+verification outputs are also checked against the oracle."""
 import numpy as np
 import pytest
 import torch
 
+import oracle
 from paper_2510_22876_amd import workloads as wl
 from tests.gpu_util import PAD_ID, SENT_KV, SENT_TOK, alloc_outputs, say
 
@@ -15,17 +20,27 @@ pytestmark = pytest.mark.gpu
 
 SHAPES = [
     # (name, workload overrides): each later case is smaller than the one before it
-    ("vicuna7b", dict(B=8, V=32000, L=2, H=4, D=128, prompt=("uniform", 64, 300))),
+    ("vicuna7b", dict(B=4, V=70000, L=2, H=2, D=128, prompt=("uniform", 64, 300))),     # rows of 140 KB
+    ("vicuna7b", dict(B=8, V=32000, L=2, H=4, D=64, prompt=("uniform", 32, 200))),
+    ("stress", dict(B=6, V=4099, L=1, H=2, D=16, prompt=("uniform", 3, 50), tie_frac=0.25)),
     ("gqa8b", dict(B=5, V=3001, L=1, H=2, D=64, prompt=("loguniform", 4, 120))),
-    ("tiny", dict()),
+    ("tiny", dict(logit_dtype="f16", logit_std=3.0, V=777)),
+    ("tiny", dict(k=0, B=1, V=500)),
 ]
 
 
-def _inputs(w, seed):
+def _workload(name, over):
+    return wl.WORKLOADS[name].scaled(**over) if over else wl.WORKLOADS[name]
+
+
+def _inputs(w, seed, bad_row=None):
     n, W_in, pad_in, cap = wl.initial_geometry(w, seed)
     logits, draft, *_ = wl.logits_and_drafts(w, seed, 0, device="cuda")
     src = wl.make_kv(w, pad_in, W_in, cap, seed, device="cuda")
     s_rows = wl.make_token_rows(w, pad_in, W_in, cap + 2, seed, PAD_ID, device="cuda")
+    if bad_row is not None:
+        pad_in = pad_in.copy()
+        pad_in[bad_row] = W_in - (w.k + 1) + 1          # outside [0, L]: flagged, the row left out
     return W_in, cap, pad_in, logits, draft, src, s_rows
 
 
@@ -56,6 +71,13 @@ def _one(sd, w, W_in, cap, pad_in, logits, draft, src, s_rows, variant, noalloc)
     return out
 
 
+def _against_oracle(w, W_in, pad_in, logits, draft, got):
+    v = oracle.verify(logits.cpu(), w.logit_dtype, draft.cpu().numpy(), pad_in, W_in)
+    assert np.array_equal(got["tokens"], v["tokens"]) and np.array_equal(got["n_acc"], v["n_acc"])
+    assert np.array_equal(got["bonus"], v["bonus"])
+    assert int(got["w_new"][0]) == v["w_new"]
+
+
 @pytest.mark.parametrize("variant", ["oop", "inplace"])
 def test_noalloc_step_equals_step(variant):
     """The reference outputs first (caller workspace filled with garbage),
@@ -64,19 +86,51 @@ def test_noalloc_step_equals_step(variant):
     from paper_2510_22876_amd import specdec as sd
     cases = []
     for i, (name, over) in enumerate(SHAPES):
-        w = wl.WORKLOADS[name].scaled(**over) if over else wl.WORKLOADS[name]
+        w = _workload(name, over)
         cases.append((name, w, _inputs(w, seed=i)))
     refs = []
     for name, w, inp in cases:
-        say(f"step (workspace): {name} B={w.B} k={w.k} V={w.V} L={w.L} H={w.H} D={w.D} variant={variant}")
+        say(f"step (workspace): {name} B={w.B} k={w.k} V={w.V} {w.logit_dtype} L={w.L} H={w.H} D={w.D} {variant}")
         refs.append(_one(sd, w, *inp, variant, noalloc=False))
     for (name, w, inp), ref in zip(cases, refs):
-        say(f"step_noalloc: {name} B={w.B} k={w.k} V={w.V} L={w.L} H={w.H} D={w.D} variant={variant}")
+        say(f"step_noalloc: {name} B={w.B} k={w.k} V={w.V} {w.logit_dtype} L={w.L} H={w.H} D={w.D} {variant}")
         got = _one(sd, w, *inp, variant, noalloc=True)
         assert int(ref["dev_status"][0]) == 0 and int(got["dev_status"][0]) == 0
         for key in ref:
             assert np.array_equal(np.asarray(ref[key]), np.asarray(got[key])), (name, variant, key)
         assert got["w_host"] == int(ref["w_new"][0])
+        W_in, cap, pad_in, logits, draft, *_ = inp
+        _against_oracle(w, W_in, pad_in, logits, draft, got)
+
+
+def test_noalloc_consecutive_one_launch_verifications():
+    """Ten one-launch verifications in a row of changing batch size, each
+    equal to specdec_step: the realignment clears the completion counts that
+    the next call's verification starts from."""
+    from paper_2510_22876_amd import specdec as sd
+    for t, B in enumerate([8, 3, 8, 1, 5, 2, 8, 7, 1, 4]):
+        w = _workload("vicuna7b", dict(B=B, V=5000 + 97 * t, L=1, H=2, D=16, prompt=("uniform", 8, 60)))
+        say(f"consecutive one-launch call {t}: B={B} V={w.V}")
+        inp = _inputs(w, seed=40 + t)
+        ref = _one(sd, w, *inp, "oop", noalloc=False)
+        got = _one(sd, w, *inp, "oop", noalloc=True)
+        for key in ref:
+            assert np.array_equal(np.asarray(ref[key]), np.asarray(got[key])), (t, key)
+
+
+def test_noalloc_bad_pad_in_flagged_like_step():
+    """A row whose pad_in lies outside [0, L] is flagged and left out of the
+    width by the one-launch verification exactly as by specdec_step."""
+    from paper_2510_22876_amd import specdec as sd
+    w = _workload("vicuna7b", dict(B=4, V=3001, L=1, H=2, D=16, prompt=("uniform", 8, 60)))
+    say("bad pad_in: B=4 V=3001, row 1 out of range")
+    inp = _inputs(w, seed=7, bad_row=1)
+    ref = _one(sd, w, *inp, "oop", noalloc=False)
+    got = _one(sd, w, *inp, "oop", noalloc=True)
+    assert int(ref["dev_status"][0]) & sd.DEV_BAD_PAD_IN
+    for key in ref:
+        assert np.array_equal(np.asarray(ref[key]), np.asarray(got[key])), key
+    assert int(got["pad_out"][1]) == -1
 
 
 def test_noalloc_rejects_beyond_its_scratch():
