@@ -104,8 +104,11 @@ const char* specdec_last_error(void);
 
 /* Bytes of device workspace specdec_verify_greedy / specdec_step need for a
  * batch of B rows, k drafts and a vocabulary of V (0 on invalid sizes).  The
- * workspace holds per-workgroup partial maxima of the argmax; it needs no
- * initialisation and its contents after a call are unspecified.  One
+ * workspace holds per-workgroup partial maxima of the argmax and, for an
+ * in-place specdec_step, the order in which the realignment takes the rows
+ * (longest moving rows first); it needs no initialisation and its contents
+ * after a call are unspecified.  The size does not depend on the logit
+ * dtype, so no dtype argument is taken.  One
  * workspace serves one in-flight call: calls that share a workspace must be
  * ordered (same stream). */
 size_t specdec_workspace_bytes(int32_t B, int32_t k, int32_t V);

@@ -442,10 +442,12 @@ specdec_status_t step_realign(int32_t k, int32_t W_in, const specdec_kv_t* src, 
                               const int32_t* pad_out, const int32_t* w_new, int64_t* pos, uint8_t* mask,
                               int64_t pm_cap, const int32_t* s_in, int64_t s_in_stride, int32_t* s_out,
                               int64_t s_out_stride, int32_t pad_id, uint32_t* dev_status, int32_t* w_new_host,
-                              hipStream_t st, uint32_t* clear_words = nullptr, uint32_t clear_count = 0) {
+                              hipStream_t st, uint32_t* clear_words = nullptr, uint32_t clear_count = 0,
+                              const int32_t* order = nullptr) {
   specdec::RealignLaunch rp{};
   rp.clear_words = clear_words;
   rp.clear_count = clear_count;
+  rp.order = order;
   rp.src = src->data;
   rp.dst = dst->data;
   rp.src_cap = src->cap;
@@ -532,8 +534,8 @@ const char* specdec_last_error(void) { return g_last_error.c_str(); }
 
 size_t specdec_workspace_bytes(int32_t B, int32_t k, int32_t V) {
   if (B < 0 || B > SPECDEC_MAX_B || k < 0 || k > SPECDEC_MAX_K || V < 1) return 0;
-  const int64_t rows = static_cast<int64_t>(B) * (k + 1);
-  return specdec::kWsHeaderBytes + static_cast<size_t>(rows * specdec::verify_chunks(rows, V)) * 8u;
+  // header, partial maxima, then the in-place realignment order
+  return static_cast<size_t>(specdec::order_offset(B, k, V) + specdec::order_bytes(B));
 }
 
 specdec_status_t specdec_workspace_init(void* workspace, size_t workspace_bytes, void* stream) {
@@ -716,6 +718,11 @@ specdec_status_t step_greedy(const void* logits, int32_t dtype, const int32_t* d
   hipStream_t st = static_cast<hipStream_t>(stream);
   specdec::VerifyLaunch vp{logits, dtype, draft, pad_in, B, k, V, W_in, tokens, n_acc,
                            bonus, pad_out, w_new, workspace, dev_status};
+  // in place, the merge launch also writes the order the walk takes the rows in
+  vp.write_order = in_place && !fused_counts;
+  const int32_t* order =
+      vp.write_order ? reinterpret_cast<const int32_t*>(static_cast<const char*>(workspace) + specdec::order_offset(B, k, V))
+                     : nullptr;
   hipError_t e = fused_counts ? timed(SPECDEC_KERNEL_VERIFY, st, [&] {
     return timed(SPECDEC_KERNEL_VERIFY_SCAN, st, [&] { return specdec::launch_verify_fused(vp, fused_counts, st); });
   })
@@ -723,7 +730,7 @@ specdec_status_t step_greedy(const void* logits, int32_t dtype, const int32_t* d
   if (e != hipSuccess) return hip_fail(e, "verify launch");
   return step_realign(k, W_in, src, dst, in_place, pad_in, tokens, n_acc, pad_out, w_new, pos, mask, pm_cap, s_in,
                       s_in_stride, s_out, s_out_stride, pad_id, dev_status, w_new_host, st, fused_counts,
-                      fused_counts ? static_cast<uint32_t>(B) + 1u : 0u);
+                      fused_counts ? static_cast<uint32_t>(B) + 1u : 0u, order);
 }
 
 }  // namespace

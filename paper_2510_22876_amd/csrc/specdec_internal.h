@@ -22,9 +22,22 @@ struct VerifyLaunch {
   int32_t* bonus;            // may be null
   int32_t* pad_out;
   int32_t* w_new;
-  void* workspace;           // [header][partial maxima: B*(k+1)*chunks uint64]
+  void* workspace;           // [header][partial maxima: B*(k+1)*chunks uint64][order table]
   uint32_t* dev_status;      // may be null
+  bool write_order = false;  // also write the in-place realignment order into the workspace
 };
+
+// In-place realignment order, written by the verification merge into the
+// workspace after the partial maxima: one int4 per row (row, pad_in,
+// pad_out, new length), the moving rows first in classes of decreasing
+// length (the cache's order within a class), then the rows that do not move
+// or whose pad_in is out of range (written with pad_out = pad_in: nothing
+// to do).
+constexpr int kMaxOrderClasses = 8;
+// Byte offset of the order table in a verification workspace, and its size.
+int64_t order_offset(int64_t B, int64_t k, int64_t V);
+int64_t order_bytes(int64_t B);
+int64_t order_bytes(int64_t B);
 
 struct RealignLaunch {
   const void* src;
@@ -48,6 +61,8 @@ struct RealignLaunch {
   int64_t s_in_stride, s_out_stride;
   const int32_t* tokens;
   int32_t pad_id;
+  // in place: the order table written by verification (NULL: the cache's order)
+  const int32_t* order = nullptr;
   // words the launch zeroes in one extra workgroup (NULL: none)
   uint32_t* clear_words = nullptr;
   uint32_t clear_count = 0;

@@ -164,6 +164,7 @@ struct VerifyArgs {
   uint32_t* dev_status;
   int64_t chunk_elems;
   int32_t chunks;               // workgroups per logit row
+  int32_t* order;               // in-place realignment order table (NULL: not written)
 };
 
 // Tunables of the vocabulary scan (compile-time; chosen by sweeping on
@@ -182,6 +183,16 @@ struct VerifyArgs {
 #endif
 #ifndef SPECDEC_VERIFY_MAX_CHUNK
 #define SPECDEC_VERIFY_MAX_CHUNK 16384
+#endif
+// In-place realignment order that the merge writes: length classes of the
+// moving rows (longest first; 1: every moving row in the cache's order), and
+// rows per group of the walk (the walk takes the rows a group at a time, each
+// group slab by slab in the cache's order)
+#ifndef SPECDEC_INPLACE_CLASSES
+#define SPECDEC_INPLACE_CLASSES 2
+#endif
+#ifndef SPECDEC_INPLACE_ROWGROUP
+#define SPECDEC_INPLACE_ROWGROUP 32
 #endif
 
 // Scan logit elements [beg, end) of one row; 16-byte vectors over the aligned
@@ -267,10 +278,121 @@ __global__ __launch_bounds__(kThreads) void verify_partial_kernel(VerifyArgs a) 
   }
 }
 
+constexpr int kFinalizeThreads = 1024;
+constexpr int kInClasses = SPECDEC_INPLACE_CLASSES;
+constexpr uint32_t kInRowGroup = SPECDEC_INPLACE_ROWGROUP;
+
+// Geometry of row i after verification: ok (pad_in in range), the new length
+// and padding; the row moves when its padding changes.
+struct RowMove {
+  bool ok, moves;
+  int32_t p, po, len;
+};
+__device__ __forceinline__ RowMove row_move(const VerifyArgs& a, int i, int32_t w) {
+  const int32_t L = a.W_in - (a.k + 1);
+  RowMove m;
+  m.p = a.pad_in[i];
+  m.ok = m.p >= 0 && m.p <= L;
+  m.len = (L - m.p) + a.n_acc[i] + 1;
+  m.po = w - m.len;
+  m.moves = m.ok && m.po != m.p;
+  return m;
+}
+
+// The in-place realignment order (one workgroup of kFinalizeThreads, after
+// the paddings): moving rows in kInClasses classes of equal length range,
+// longest first, then the rows with nothing to move; each class in
+// increasing row order (a stable partition: per chunk of rows a ballot per
+// class, then prefixes over the waves).  The in-place walk takes the spans
+// of the longest rows first, so that the longest walks do not start last.
+__device__ void write_inplace_order(const VerifyArgs& a, int32_t w) {
+  constexpr int kW = kFinalizeThreads / 64;
+  constexpr int kCls = kInClasses + 1;   // the last class: rows with nothing to move
+  __shared__ int32_t s_lo[kW], s_hi[kW];
+  __shared__ int32_t s_cnt[kCls], s_start[kCls], s_carry[kCls];
+  __shared__ int32_t s_wave[kCls][kW];
+  static_assert(kInClasses >= 1 && kCls <= kMaxOrderClasses, "order classes");
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  int32_t lo = 0x7FFFFFFF, hi = 0;
+  for (int i = tid; i < a.B; i += kFinalizeThreads) {
+    const RowMove m = row_move(a, i, w);
+    if (m.moves) {
+      lo = m.len < lo ? m.len : lo;
+      hi = m.len > hi ? m.len : hi;
+    }
+  }
+  hi = wave_max_i32(hi);
+  lo = -wave_max_i32(-lo);
+  if (lane == 0) {
+    s_hi[wv] = hi;
+    s_lo[wv] = lo;
+  }
+  if (tid < kCls) {
+    s_cnt[tid] = 0;
+    s_carry[tid] = 0;
+  }
+  __syncthreads();
+  hi = s_hi[0];
+  lo = s_lo[0];
+#pragma unroll
+  for (int q = 1; q < kW; ++q) {
+    hi = s_hi[q] > hi ? s_hi[q] : hi;
+    lo = s_lo[q] < lo ? s_lo[q] : lo;
+  }
+  const int64_t range = static_cast<int64_t>(hi) - lo + 1;
+  auto cls = [&](const RowMove& m) {
+    if (!m.moves) return kInClasses;
+    const int64_t c = (static_cast<int64_t>(hi) - m.len) * kInClasses / range;
+    return static_cast<int>(c < kInClasses ? c : kInClasses - 1);
+  };
+  for (int i = tid; i < a.B; i += kFinalizeThreads) atomicAdd(&s_cnt[cls(row_move(a, i, w))], 1);
+  __syncthreads();
+  if (tid == 0) {
+    int32_t acc = 0;
+    for (int c = 0; c < kCls; ++c) {
+      s_start[c] = acc;
+      acc += s_cnt[c];
+    }
+  }
+  __syncthreads();
+  for (int base = 0; base < a.B; base += kFinalizeThreads) {
+    const int i = base + tid;
+    RowMove m{};
+    int c = kCls;   // past the end of the batch
+    if (i < a.B) {
+      m = row_move(a, i, w);
+      c = cls(m);
+    }
+    int rank = 0;
+#pragma unroll
+    for (int cc = 0; cc < kCls; ++cc) {
+      const unsigned long long bits = __ballot(c == cc);
+      if (lane == 0) s_wave[cc][wv] = __popcll(bits);
+      if (c == cc) rank = __popcll(bits & ((1ull << lane) - 1ull));
+    }
+    __syncthreads();
+    if (c < kCls) {
+      int32_t pos = s_start[c] + s_carry[c] + rank;
+      for (int q = 0; q < wv; ++q) pos += s_wave[c][q];
+      int32_t* e = a.order + 4 * static_cast<int64_t>(pos);   // four words (the workspace is 8-byte aligned)
+      e[0] = i;
+      e[1] = m.p;
+      e[2] = m.moves ? m.po : m.p;   // nothing to move: equal paddings
+      e[3] = m.len;
+    }
+    __syncthreads();
+    if (tid < kCls) {
+      int32_t add = 0;
+      for (int q = 0; q < kW; ++q) add += s_wave[tid][q];
+      s_carry[tid] += add;
+    }
+    __syncthreads();
+  }
+}
+
 // One workgroup of kFinalizeThreads: row maxima, then per sequence the
 // prefix-match scan, the bonus token and its new length; then the width and
 // the paddings.
-constexpr int kFinalizeThreads = 1024;
 
 __global__ __launch_bounds__(kFinalizeThreads) void verify_finalize_kernel(VerifyArgs a) {
   __shared__ int32_t wmax[kFinalizeThreads / 64];
@@ -318,6 +440,7 @@ __global__ __launch_bounds__(kFinalizeThreads) void verify_finalize_kernel(Verif
     a.pad_out[i] = ok ? w - ((L - p) + a.n_acc[i] + 1) : -1;
   }
   if (threadIdx.x == 0) a.w_new[0] = w;
+  if (a.order) write_inplace_order(a, w);
 }
 
 // One launch of greedy verification for batches whose logit rows are short
@@ -491,6 +614,8 @@ struct RealignArgs {
   uint32_t tok_blocks;                   // token-row workgroups in all
   uint32_t* clear_words;                 // one more workgroup zeroes these (NULL: none)
   uint32_t clear_count;
+  const int32_t* order;                  // in place: verification's order table (NULL: the cache's order)
+  uint32_t span_rows;                    // spans per row: L * 2 * H
 };
 
 struct RowGeom {
@@ -709,15 +834,40 @@ __global__ __launch_bounds__(kTpb) void realign_inplace_kernel(RealignArgs a) {
   // group index: any periodic pattern of moving rows spreads over all XCDs.
   const uint32_t rel = a.span_base + (blockIdx.x - a.extra_blocks);
   const uint32_t grp = rel >> 3;
-  const uint32_t span =
+  const uint32_t lin =
       static_cast<uint64_t>(grp) * 8u + 8u <= a.nspans ? (grp << 3) + ((rel + grp) & 7u) : rel;
-  const uint32_t row_u = (span / static_cast<uint32_t>(a.H)) % static_cast<uint32_t>(a.B);
-  const int row = static_cast<int>(row_u);
+  uint32_t span;
   RowGeom g;
-  const uint32_t err = row_geometry(a, row, g);
-  if (err) {
-    if (span == row_u * static_cast<uint32_t>(a.H) && threadIdx.x == 0 && a.dev_status) atomicOr(a.dev_status, err);
-    return;
+  if (a.order) {
+    // the rows in the order verification wrote (longest moving rows first),
+    // kInRowGroup rows at a time, each group slab by slab in the cache's
+    // order: the index alone gives (group, slab, row, head), and one load the
+    // row's geometry
+    const uint32_t B = static_cast<uint32_t>(a.B), H = static_cast<uint32_t>(a.H);
+    // R <= B, so a group's spans (R * span_rows <= nspans) fit 32 bits
+    const uint32_t R = kInRowGroup && kInRowGroup < B ? kInRowGroup : B;   // 0: the whole batch is one group
+    const uint32_t grp_spans = R * a.span_rows;
+    const uint32_t gi = lin / grp_spans;
+    const uint32_t rem = lin - gi * grp_spans;
+    const uint32_t rows_here = B - gi * R < R ? B - gi * R : R;
+    const uint32_t slab = rem / (rows_here * H);
+    const uint32_t rr = rem - slab * rows_here * H;
+    const uint32_t r = rr / H, h = rr - r * H;
+    const int32_t* info = a.order + 4 * static_cast<int64_t>(gi * R + r);
+    const uint32_t row_u = static_cast<uint32_t>(load_invariant(info));
+    g.pad_in = load_invariant(info + 1);
+    g.pad_out = load_invariant(info + 2);
+    g.len = load_invariant(info + 3);
+    span = (slab * B + row_u) * H + h;
+  } else {
+    span = lin;
+    const uint32_t row_u = (span / static_cast<uint32_t>(a.H)) % static_cast<uint32_t>(a.B);
+    const int row = static_cast<int>(row_u);
+    const uint32_t err = row_geometry(a, row, g);
+    if (err) {
+      if (span == row_u * static_cast<uint32_t>(a.H) && threadIdx.x == 0 && a.dev_status) atomicOr(a.dev_status, err);
+      return;
+    }
   }
   const int32_t s = g.pad_out - g.pad_in;
   if (s == 0) return;  // no shift: the row is already in place (uniform acceptance)
@@ -831,8 +981,17 @@ static VerifyArgs verify_args(const VerifyLaunch& p) {
   const int64_t rows = static_cast<int64_t>(p.B) * (p.k + 1);
   a.chunk_elems = verify_chunk_elems(rows, p.V);
   a.chunks = static_cast<int32_t>((p.V + a.chunk_elems - 1) / a.chunk_elems);
+  a.order = p.write_order ? reinterpret_cast<int32_t*>(static_cast<char*>(p.workspace) + order_offset(p.B, p.k, p.V))
+                          : nullptr;
   return a;
 }
+
+int64_t order_offset(int64_t B, int64_t k, int64_t V) {
+  const int64_t rows = B * (k + 1);
+  return static_cast<int64_t>(kWsHeaderBytes) + ((rows * verify_chunks(rows, V) * 8 + 15) / 16) * 16;
+}
+
+int64_t order_bytes(int64_t B) { return 16 * B; }
 
 hipError_t launch_verify_scan(const VerifyLaunch& p, hipStream_t stream) {
   const VerifyArgs a = verify_args(p);
@@ -917,6 +1076,8 @@ hipError_t launch_realign(const RealignLaunch& p, hipStream_t stream) {
   a.mask = p.mask;
   a.pad_out = p.pad_out;
   a.pm_cap = p.pm_cap;
+  a.order = p.in_place ? p.order : nullptr;
+  a.span_rows = static_cast<uint32_t>(static_cast<int64_t>(p.L) * 2 * p.H);
   const int tpb = p.in_place ? kInTpb : kOopTpb;
   int64_t pm_blocks = 0;
   a.pm_col_blocks = 1;

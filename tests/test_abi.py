@@ -42,14 +42,15 @@ def test_abi_version_matches_header(sd):
 
 
 def test_workspace_bytes(sd):
-    # 48 rows of 32000: 16 workgroups of 2048 elements per row
-    assert sd.workspace_bytes(8, 5, 32000) == 256 + 8 * 6 * 16 * 8
+    # 48 rows of 32000: 16 workgroups of 2048 elements per row; then the
+    # in-place order table (4 words per row)
+    assert sd.workspace_bytes(8, 5, 32000) == 256 + 8 * 6 * 16 * 8 + 16 * 8
     assert sd.workspace_bytes(0, 0, 10) == 256
     assert sd.workspace_bytes(-1, 2, 10) == 0
     assert sd.workspace_bytes(4, 65, 10) == 0
     assert sd.workspace_bytes(4, 2, 0) == 0
     # never more than 64 workgroups per row
-    assert sd.workspace_bytes(1, 0, 2 ** 31 - 1) == 256 + 64 * 8
+    assert sd.workspace_bytes(1, 0, 2 ** 31 - 1) == 256 + 64 * 8 + 16
 
 
 def _no_gpu():

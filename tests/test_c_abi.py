@@ -22,7 +22,7 @@ PROGRAM = r"""
 int main(void) {
   CHECK(specdec_abi_version() == SPECDEC_ABI_VERSION);
   /* 48 logit rows of 32000: 16 workgroups of 2048 elements per row */
-  CHECK(specdec_workspace_bytes(8, 5, 32000) == 256 + 8 * 6 * 16 * 8);
+  CHECK(specdec_workspace_bytes(8, 5, 32000) == 256 + 8 * 6 * 16 * 8 + 16 * 8);
   /* an argument error is reported before anything is enqueued */
   CHECK(specdec_verify_greedy(NULL, SPECDEC_BF16, NULL, NULL, -1, 3, 100, 10, NULL, NULL, NULL, NULL, NULL,
                               NULL, 0, NULL, NULL) == SPECDEC_ERR_INVALID_ARGUMENT);
