@@ -48,10 +48,13 @@ METRIC_EXSPEC = "EXSpec gather+verify+write-back steps/s and achieved HBM GB/s (
 METRIC_SAMPLE = "stochastic verify+realign steps/s and achieved HBM GB/s (% peak), B=8 7B-shaped KV"
 METRIC_VARLEN = "variable-length rollback steps/s and achieved HBM GB/s (% peak), B=8 7B-shaped KV"
 METRIC_VERIFY = "greedy verification calls/s from cold caches and achieved HBM GB/s (% peak) of the vocabulary scan"
+METRIC_VERIFY_SAMPLE = ("stochastic verification calls/s from cold caches and achieved HBM GB/s (% peak) of the "
+                        "row statistics")
 CSRC = ROOT / "paper_2510_22876_amd" / "csrc"
 KERNEL_SRCS = [CSRC / f for f in ("specdec_kernels.hip", "span_copy.h", "posmask.h")]
 GATHER_SRCS = [CSRC / f for f in ("exspec_kernels.hip", "span_copy.h", "posmask.h")]
 VARLEN_SRCS = [CSRC / f for f in ("rollback_kernels.hip", "span_copy.h")]
+SAMPLE_SRCS = [CSRC / "sample_kernels.hip"]
 
 
 def log(*a):
@@ -473,22 +476,31 @@ def bench_varlen(args, w):
     print(json.dumps(line), flush=True)
 
 
-def cpu_baseline_verify(w, logits, draft, pad_in, W_in, budget_s):
-    """The oracle's greedy verification (every logit row) on one host thread,
+def cpu_baseline_verify(w, logits, draft, pad_in, W_in, budget_s, sample=None):
+    """The oracle's verification (every logit row; stochastic when ``sample``
+    holds the draft logits, uniforms and temperature) on one host thread,
     called until ``budget_s`` seconds have passed (at least once)."""
     import oracle
     lg = logits.cpu()
     dr = draft.cpu().numpy()
+    if sample:
+        dl, ua, us, T = sample
+        dl, ua, us = dl.cpu(), ua.cpu().numpy(), us.cpu().numpy()
     t0 = time.perf_counter()
     calls = 0
     while True:
-        oracle.verify(lg, w.logit_dtype, dr, pad_in, W_in)
+        if sample:
+            oracle.verify_sample(lg, dl, w.logit_dtype, dr, pad_in, ua, us, T, W_in)
+        else:
+            oracle.verify(lg, w.logit_dtype, dr, pad_in, W_in)
         calls += 1
         if time.perf_counter() - t0 >= budget_s:
             break
     wall = time.perf_counter() - t0
+    rows = w.B * ((2 * w.k + 1) if sample else (w.k + 1))
     return dict(value=calls / wall, unit="calls/s", cores=1, kind="oracle", cpu_model=cpu_model(),
-                sample=f"{calls} whole oracle verifications ({w.B * (w.k + 1)} logit rows each) in {wall:.2f} s")
+                sample=f"{calls} whole oracle {'stochastic ' if sample else ''}verifications ({rows} logit rows each) "
+                       f"in {wall:.2f} s")
 
 
 def bench_verify(args, w):
@@ -508,17 +520,31 @@ def bench_verify(args, w):
     from paper_2510_22876_amd import workloads as wl
 
     n, W_in, pad_in, cap = wl.initial_geometry(w, args.seed)
-    logits, draft, *_ = wl.logits_and_drafts(w, args.seed, 0, device="cuda")
+    sample = args.verify == "sample"
+    if sample:
+        logits, draft_logits, draft, u_accept, u_sample = wl.sampled_inputs(w, args.seed, 0, device="cuda",
+                                                                            temperature=args.temperature)
+        sws = sd.alloc_sample_workspace(w.B, w.k, w.V)
+        rows = w.B * (2 * w.k + 1)
+    else:
+        logits, draft, *_ = wl.logits_and_drafts(w, args.seed, 0, device="cuda")
+        rows = w.B * (w.k + 1)
     bufs = sd.StepBuffers(w.B, w.k, w.V, 8, "cuda")
     pad_t = torch.as_tensor(pad_in, device="cuda")
     evict = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
-    desc = (f"{w.name} verification: B={w.B} k={w.k} V={w.V} {w.logit_dtype} logits "
-            f"({w.B * (w.k + 1) * w.V * w.logit_bytes / 1e6:.2f} MB), W_in={W_in}")
+    kind = f"stochastic verification (T={args.temperature}, target and draft logits)" if sample else "verification"
+    desc = (f"{w.name} {kind}: B={w.B} k={w.k} V={w.V} {w.logit_dtype} logits "
+            f"({rows * w.V * w.logit_bytes / 1e6:.2f} MB), W_in={W_in}")
     log(f"[bench] verify: {desc}")
 
     def call():
-        sd.specdec_verify_greedy(logits, draft, pad_t, W_in, bufs.tokens, bufs.n_acc, bufs.bonus, bufs.pad_out,
-                                 bufs.w_new, bufs.workspace, bufs.dev_status)
+        if sample:
+            sd.specdec_verify_sample(logits, draft_logits, draft, pad_t, u_accept, u_sample, args.temperature, W_in,
+                                     bufs.tokens, bufs.n_acc, bufs.bonus, bufs.pad_out, bufs.w_new, sws,
+                                     bufs.dev_status)
+        else:
+            sd.specdec_verify_greedy(logits, draft, pad_t, W_in, bufs.tokens, bufs.n_acc, bufs.bonus, bufs.pad_out,
+                                     bufs.w_new, bufs.workspace, bufs.dev_status)
 
     for _ in range(args.warmup):
         call()
@@ -526,14 +552,16 @@ def bench_verify(args, w):
     if int(bufs.dev_status.cpu()[0]) != 0:
         raise RuntimeError("device flagged invalid values")
     K = args.steps
-    mask = (1 << sd.KERNEL_VERIFY) | (1 << sd.KERNEL_VERIFY_SCAN)
+    whole, scan = (sd.KERNEL_SAMPLE, sd.KERNEL_SAMPLE_STATS) if sample else (sd.KERNEL_VERIFY, sd.KERNEL_VERIFY_SCAN)
 
     evict.fill_(1)
     sink = torch.empty(K, dtype=torch.int64, device="cuda")
 
-    def timed_calls(cold: bool):
+    def timed_calls(cold: bool, kernel: int):
+        # one timer per pass: a timer nested inside another would add its
+        # events to the outer interval
         sd.timing_reset()
-        sd.timing_enable(mask)
+        sd.timing_enable(1 << kernel)
         for i in range(K):
             if cold:
                 torch.sum(evict, dim=0, dtype=torch.int64, out=sink[i])
@@ -542,25 +570,27 @@ def bench_verify(args, w):
             call()
         torch.cuda.synchronize()
         sd.timing_enable(False)
-        v_ms, v_n = sd.timing_query(sd.KERNEL_VERIFY)
-        s_ms, s_n = sd.timing_query(sd.KERNEL_VERIFY_SCAN)
-        assert v_n == K and s_n == K
-        return v_ms / K, s_ms / K
+        ms, n = sd.timing_query(kernel)
+        assert n == K
+        return ms / K
 
-    warm_ms, warm_scan_ms = timed_calls(False)
-    cold_ms, cold_scan_ms = timed_calls(True)
+    warm_ms, warm_scan_ms = timed_calls(False, whole), timed_calls(False, scan)
+    cold_ms, cold_scan_ms = timed_calls(True, whole), timed_calls(True, scan)
     by = step_bytes(w, pad_in, W_in, bufs.n_acc.cpu().numpy(), int(bufs.w_new.cpu()[0]), "oop", False)
-    scan_bytes = w.B * (w.k + 1) * w.V * w.logit_bytes
+    scan_bytes = rows * w.V * w.logit_bytes
     achieved = scan_bytes / (cold_scan_ms * 1e-3) / 1e9
-    traffic, traffic_src = read_traffic_summary(w.name, "cold", scan_bytes, kernel="verifyscan")
+    traffic, traffic_src = read_traffic_summary(w.name, "cold", scan_bytes,
+                                                kernel="samplestats" if sample else "verifyscan",
+                                                srcs=SAMPLE_SRCS if sample else KERNEL_SRCS)
     log(f"[bench] verify cold {cold_ms * 1e3:.2f} us (scan {cold_scan_ms * 1e3:.2f} us, {achieved:.0f} GB/s), "
         f"warm {warm_ms * 1e3:.2f} us (scan {warm_scan_ms * 1e3:.2f} us); traffic: {traffic_src}")
     cpu = None
     if args.cpu_baseline_seconds > 0:
-        cpu = cpu_baseline_verify(w, logits, draft, pad_in, W_in, args.cpu_baseline_seconds)
+        cpu = cpu_baseline_verify(w, logits, draft, pad_in, W_in, args.cpu_baseline_seconds,
+                                  sample=(draft_logits, u_accept, u_sample, args.temperature) if sample else None)
         log(f"[bench] cpu baseline: {cpu['value']:.2f} calls/s ({cpu['sample']})")
     line = {
-        "metric": METRIC_VERIFY, "value": 1e3 / cold_ms, "unit": "calls/s", "n_gpus": 1, "steps": K,
+        "metric": METRIC_VERIFY_SAMPLE if sample else METRIC_VERIFY, "value": 1e3 / cold_ms, "unit": "calls/s", "n_gpus": 1, "steps": K,
         "warmup": args.warmup, "ms_per_step": cold_ms, "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": w.logit_dtype, "data": "synthetic",
         "config": {"workload": desc, "B": w.B, "k": w.k, "V": w.V, "seed": args.seed,
@@ -568,7 +598,8 @@ def bench_verify(args, w):
                    "scan_cold_ms": round(cold_scan_ms, 5), "scan_warm_ms": round(warm_scan_ms, 5),
                    "scan_warm_GBps": round(scan_bytes / (warm_scan_ms * 1e-3) / 1e9, 1),
                    "verify_bytes": by["verify"], "eviction_bytes": evict.numel()},
-        "roofline": {"bound": "hbm", "kernel": "verify_partial (vocabulary scan), cold caches",
+        "roofline": {"bound": "hbm", "kernel": ("sample_stats (row statistics of target and draft logits)" if sample
+                                                else "verify_partial (vocabulary scan)") + ", cold caches",
                      "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic, "algorithmic_bytes": scan_bytes},
         "cpu_baseline": cpu,
@@ -936,7 +967,7 @@ def main():
     achieved = realign_bytes / (realign_avg_ms * 1e-3) / 1e9
     ms_per_step = elapsed / K * 1e3
     step_gbs = (realign_bytes + by["verify"]) / (ms_per_step * 1e-3) / 1e9
-    traffic, traffic_src = read_traffic_summary(w.name, variant, realign_bytes)
+    traffic, traffic_src = read_traffic_summary(w.name, variant + ("sample" if sample else ""), realign_bytes)
     copy_gbs = copy_ceiling(realign_bytes // 2) if args.copy_ceiling else None
     log(f"[bench] n_acc={n_acc.tolist()} w_new={w_new} realign {realign_avg_ms:.4f} ms "
         f"({realign_bytes / 1e9:.3f} GB, {achieved:.0f} GB/s), verify {verify_avg_ms:.4f} ms "

@@ -566,7 +566,8 @@ specdec_status_t specdec_varlen_rollback(const specdec_varlen_t* src, const spec
  * / mask in specdec_step, 2 = position ids / mask alone, 3 = batch gather,
  * 4 = write-back, 5 = stochastic verification, 6 = variable-length rollback,
  * 7 = the vocabulary scan of greedy verification alone, the first of its two
- * launches) and returns the totals since the last reset.
+ * launches, 8 = the row statistics of stochastic verification alone, the
+ * first of its four launches) and returns the totals since the last reset.
  */
 #define SPECDEC_KERNEL_VERIFY 0
 #define SPECDEC_KERNEL_REALIGN 1
@@ -576,7 +577,8 @@ specdec_status_t specdec_varlen_rollback(const specdec_varlen_t* src, const spec
 #define SPECDEC_KERNEL_SAMPLE 5
 #define SPECDEC_KERNEL_VARLEN 6
 #define SPECDEC_KERNEL_VERIFY_SCAN 7
-#define SPECDEC_TIMING_ALL 255
+#define SPECDEC_KERNEL_SAMPLE_STATS 8
+#define SPECDEC_TIMING_ALL 511
 specdec_status_t specdec_timing_enable(int32_t kernel_mask);
 specdec_status_t specdec_timing_reset(void);
 specdec_status_t specdec_timing_query(int32_t kernel, double* total_ms, int64_t* launches);

@@ -635,8 +635,7 @@ int64_t sample_mass_chunk_elems(int64_t V) {
   return c;
 }
 
-hipError_t launch_verify_sample(const SampleLaunch& p, hipStream_t stream) {
-  SampleArgs a{};
+static hipError_t sample_args(const SampleLaunch& p, SampleArgs& a) {
   a.logits = static_cast<const char*>(p.logits);
   a.draft_logits = static_cast<const char*>(p.draft_logits);
   a.draft = p.draft;
@@ -667,13 +666,26 @@ hipError_t launch_verify_sample(const SampleLaunch& p, hipStream_t stream) {
   a.partial = reinterpret_cast<float2*>(ws);
   a.last = reinterpret_cast<int2*>(ws + rows * a.chunks * 8);
   a.mass = reinterpret_cast<float2*>(ws + (rows * a.chunks + static_cast<int64_t>(p.B) * a.mchunks) * 8);
+  return hipSuccess;
+}
+
+hipError_t launch_sample_stats(const SampleLaunch& p, hipStream_t stream) {
+  SampleArgs a{};
+  const hipError_t r = sample_args(p, a);
+  if (r != hipSuccess) return r;
+  const int64_t rows = static_cast<int64_t>(p.B) * (2 * p.k + 1);
   const dim3 grid(static_cast<uint32_t>(rows * a.chunks));
   switch (p.dtype) {
     case 0: hipLaunchKernelGGL(sample_stats_kernel<0>, grid, dim3(kStatsThreads), 0, stream, a); break;
     case 1: hipLaunchKernelGGL(sample_stats_kernel<1>, grid, dim3(kStatsThreads), 0, stream, a); break;
     default: hipLaunchKernelGGL(sample_stats_kernel<2>, grid, dim3(kStatsThreads), 0, stream, a); break;
   }
-  hipError_t e = hipGetLastError();
+  return hipGetLastError();
+}
+
+hipError_t launch_sample_finish(const SampleLaunch& p, hipStream_t stream) {
+  SampleArgs a{};
+  hipError_t e = sample_args(p, a);
   if (e != hipSuccess) return e;
   const dim3 seqs(static_cast<uint32_t>(p.B));
   switch (p.dtype) {
@@ -697,6 +709,11 @@ hipError_t launch_verify_sample(const SampleLaunch& p, hipStream_t stream) {
     default: hipLaunchKernelGGL(sample_pick_kernel<2>, seqs, dim3(kPickThreads), 0, stream, a); break;
   }
   return hipGetLastError();
+}
+
+hipError_t launch_verify_sample(const SampleLaunch& p, hipStream_t stream) {
+  const hipError_t e = launch_sample_stats(p, stream);
+  return e != hipSuccess ? e : launch_sample_finish(p, stream);
 }
 
 }  // namespace specdec

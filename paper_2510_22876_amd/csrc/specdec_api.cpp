@@ -69,7 +69,7 @@ int logit_bytes(int32_t dtype) {
 
 // ---- kernel timers -------------------------------------------------------------
 
-constexpr int kTimedKernels = 8;
+constexpr int kTimedKernels = 9;
 
 struct TimedLaunch {
   int kernel;
@@ -183,6 +183,15 @@ hipError_t verify_launches(const specdec::VerifyLaunch& p, hipStream_t st) {
   return timed(SPECDEC_KERNEL_VERIFY, st, [&] {
     const hipError_t r = timed(SPECDEC_KERNEL_VERIFY_SCAN, st, [&] { return specdec::launch_verify_scan(p, st); });
     return r != hipSuccess ? r : specdec::launch_verify_finalize(p, st);
+  });
+}
+
+// Stochastic verification's launches, timed as a whole (SPECDEC_KERNEL_SAMPLE)
+// and the row statistics alone (SPECDEC_KERNEL_SAMPLE_STATS).
+hipError_t sample_launches(const specdec::SampleLaunch& p, hipStream_t st) {
+  return timed(SPECDEC_KERNEL_SAMPLE, st, [&] {
+    const hipError_t r = timed(SPECDEC_KERNEL_SAMPLE_STATS, st, [&] { return specdec::launch_sample_stats(p, st); });
+    return r != hipSuccess ? r : specdec::launch_sample_finish(p, st);
   });
 }
 
@@ -590,7 +599,7 @@ specdec_status_t specdec_verify_sample(const void* logits, const void* draft_log
   specdec::SampleLaunch p{logits, draft_logits, dtype, draft, pad_in, u_accept, u_sample, c,
                           B, k, V, W_in, tokens, n_acc, bonus, pad_out, w_new, workspace, dev_status};
   hipStream_t st = static_cast<hipStream_t>(stream);
-  hipError_t e = timed(SPECDEC_KERNEL_SAMPLE, st, [&] { return specdec::launch_verify_sample(p, st); });
+  hipError_t e = sample_launches(p, st);
   if (e != hipSuccess) return hip_fail(e, "stochastic verify launch");
   return ok();
 }
@@ -859,7 +868,7 @@ specdec_status_t specdec_step_sample(const void* logits, const void* draft_logit
   hipStream_t st = static_cast<hipStream_t>(stream);
   specdec::SampleLaunch sp{logits, draft_logits, dtype, draft, pad_in, u_accept, u_sample, c,
                            B, k, V, W_in, tokens, n_acc, bonus, pad_out, w_new, workspace, dev_status};
-  hipError_t e = timed(SPECDEC_KERNEL_SAMPLE, st, [&] { return specdec::launch_verify_sample(sp, st); });
+  hipError_t e = sample_launches(sp, st);
   if (e != hipSuccess) return hip_fail(e, "stochastic verify launch");
   return step_realign(k, W_in, src, dst, in_place, pad_in, tokens, n_acc, pad_out, w_new, pos, mask, pm_cap, s_in,
                       s_in_stride, s_out, s_out_stride, pad_id, dev_status, w_new_host, st);

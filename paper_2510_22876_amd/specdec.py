@@ -21,8 +21,8 @@ OK, ERR_INVALID_ARGUMENT, ERR_UNSUPPORTED, ERR_HIP, ERR_WORKSPACE = 0, 1, 2, 3, 
 F32, BF16, F16 = 0, 1, 2
 DTYPE_OF = {torch.float32: F32, torch.bfloat16: BF16, torch.float16: F16}
 KERNEL_VERIFY, KERNEL_REALIGN, KERNEL_POSMASK, KERNEL_GATHER, KERNEL_WRITEBACK, KERNEL_SAMPLE = 0, 1, 2, 3, 4, 5
-KERNEL_VARLEN, KERNEL_VERIFY_SCAN = 6, 7
-TIMING_ALL = 255
+KERNEL_VARLEN, KERNEL_VERIFY_SCAN, KERNEL_SAMPLE_STATS = 6, 7, 8
+TIMING_ALL = 511
 DEV_BAD_PAD_IN, DEV_BAD_ACCEPT, DEV_BAD_WIDTH, DEV_BAD_PAD_OUT = 1, 2, 4, 8
 DEV_BAD_SLOT, DEV_SLOT_LEN, DEV_BAD_UNIFORM = 0x10, 0x20, 0x40
 WRITEBACK_FULL, WRITEBACK_APPEND = 0, 1

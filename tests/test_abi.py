@@ -219,11 +219,11 @@ def test_realign_tokens_rejects(sd):
 
 
 def test_timing_query_rejects_unknown_kernel(sd):
-    assert sd.lib.specdec_timing_query(8, None, None) == 1
+    assert sd.lib.specdec_timing_query(9, None, None) == 1
     assert sd.lib.specdec_timing_query(-1, None, None) == 1
     assert sd.lib.specdec_timing_enable(0) == 0
-    assert sd.lib.specdec_timing_enable(255) == 0
-    assert sd.lib.specdec_timing_enable(256) == 1
+    assert sd.lib.specdec_timing_enable(511) == 0
+    assert sd.lib.specdec_timing_enable(512) == 1
     assert sd.lib.specdec_timing_enable(0) == 0
     assert sd.lib.specdec_timing_enable(-1) == 1
 

@@ -40,13 +40,16 @@ def test_traffic_comes_only_from_counters_of_the_same_step():
         hbm = float(re.search(r"hbm_bytes_per_launch:\s*([0-9.eE+]+)", text).group(1))
         kernel, variant, workload = path.name[:-len("_hbm_counters.md")].split("_")
         srcs = {"realign": bench.KERNEL_SRCS, "gather": bench.GATHER_SRCS, "varlen": bench.VARLEN_SRCS,
-                "verifyscan": bench.KERNEL_SRCS}[kernel]
+                "verifyscan": bench.KERNEL_SRCS, "samplestats": bench.SAMPLE_SRCS}[kernel]
         value, src = bench.read_traffic_summary(workload, variant, alg, kernel=kernel, srcs=srcs)
         if value is None:
             assert src == "kernel changed since the counters were taken", (path.name, src)
         else:
             assert value == hbm and src == path.name
-            assert abs(hbm / alg - 1) < 1e-3, path.name          # the counters read the algorithmic bytes
+            # the counters read the algorithmic bytes: cache moves to 0.1%; the scans to 0.5% (their algorithmic
+            # bytes count the logits alone, the counters also see the partial maxima and row-boundary lines)
+            tol = 5e-3 if kernel in ("verifyscan", "samplestats") else 1e-3
+            assert abs(hbm / alg - 1) < tol, path.name
         value, src = bench.read_traffic_summary(workload, variant, alg + 1, kernel=kernel, srcs=srcs)
         assert value is None, path.name
     value, src = bench.read_traffic_summary("nosuch", "oop", 1)

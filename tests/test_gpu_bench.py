@@ -29,6 +29,7 @@ PATHS = [
     ["--path", "varlen"],
     ["--path", "verify"],
     ["--path", "verify", "--workload", "stress"],
+    ["--path", "verify", "--verify", "sample"],
 ]
 
 
