@@ -43,6 +43,7 @@ ROOT = Path(__file__).resolve().parent
 sys.path.insert(0, str(ROOT))
 
 PEAK_HBM_GBS = 8000.0
+WHOLE_STEP_MAX_BYTES = 16 << 30   # the CPU baseline runs one whole oracle step when the cache is at most this
 METRIC = "verify+realign steps/s and achieved HBM GB/s (% peak), B=8 7B-shaped KV"
 METRIC_EXSPEC = "EXSpec gather+verify+write-back steps/s and achieved HBM GB/s (% peak), B=8 7B-shaped KV"
 METRIC_SAMPLE = "stochastic verify+realign steps/s and achieved HBM GB/s (% peak), B=8 7B-shaped KV"
@@ -145,14 +146,35 @@ def oracle_threads(layer_job, budget_s: float, L: int, serial_s: float):
     return dict(value=1.0 / est, unit="steps/s", cores=n, sample=f"{calls} one-layer calls on {n} threads")
 
 
-def cpu_model() -> str:
+def cpu_info() -> dict:
+    """The host CPU as /proc/cpuinfo describes it: the full model name, the
+    cache size line, family / model / stepping, and the logical CPUs seen."""
+    info = {"model": "unknown", "cache": "unknown", "family_model_stepping": "unknown", "logical_cpus": 0}
+    fms = {}
     try:
         for ln in Path("/proc/cpuinfo").read_text().splitlines():
-            if ln.startswith("model name"):
-                return ln.split(":", 1)[1].strip()
+            key, _, val = ln.partition(":")
+            key, val = key.strip(), val.strip()
+            if key == "processor":
+                info["logical_cpus"] += 1
+            elif key == "model name" and info["model"] == "unknown":
+                info["model"] = val
+            elif key == "cache size" and info["cache"] == "unknown":
+                info["cache"] = val
+            elif key in ("cpu family", "model", "stepping") and key not in fms:
+                fms[key] = val
     except OSError:
         pass
-    return "unknown"
+    if fms:
+        info["family_model_stepping"] = "/".join(fms.get(k, "?") for k in ("cpu family", "model", "stepping"))
+    return info
+
+
+def cpu_fields() -> dict:
+    """The cpu_baseline fields that name the host CPU."""
+    ci = cpu_info()
+    return dict(cpu_model=ci["model"], cpu_cache=ci["cache"], cpu_family_model_stepping=ci["family_model_stepping"],
+                host_logical_cpus=ci["logical_cpus"])
 
 
 def copy_ceiling(nbytes: int, reps: int = 5) -> float:
@@ -186,12 +208,15 @@ def percentiles(ms):
 
 
 def cpu_baseline(w, logits, draft, pad_in, W_in, src, budget_s: float, s_rows=None, sample=None):
-    """The oracle as it stands, single-threaded on the host, on a bounded
-    sample: verification over every logit row (greedy, or stochastic when
-    ``sample`` = (draft_logits, u_accept, u_sample, temperature)), the KV
-    realignment of whole layer slabs (cycling over up to two layers until
-    ``budget_s`` seconds of work), position ids / mask and the token row;
-    scaled to one whole step."""
+    """The oracle as it stands, single-threaded on the host: verification
+    over every logit row (greedy, or stochastic when ``sample`` =
+    (draft_logits, u_accept, u_sample, temperature)), position ids / mask and
+    the token row, and the KV realignment, timed two ways: over the whole
+    cache in one call (one whole step; when the cache is at most
+    WHOLE_STEP_MAX_BYTES) and on a bounded sample of whole layer slabs
+    (cycling over up to two layers until ``budget_s`` seconds of work) scaled
+    to every layer.  The value is the whole step when it ran, else the
+    estimate; the same layer calls on N host threads give ``threads``."""
     import oracle
     k = w.k
     lg = logits.cpu()
@@ -225,12 +250,30 @@ def cpu_baseline(w, logits, draft, pad_in, W_in, src, budget_s: float, s_rows=No
     est = t_verify + per_layer * w.L + t_pm
     mt = oracle_threads(lambda i: oracle.realign_kv(host[i % nl], k, W_in, pad_in, v["n_acc"], v["w_new"]),
                         budget_s, w.L, t_verify + t_pm)
-    return dict(value=1.0 / est, unit="steps/s", cores=1, kind="oracle", cpu_model=cpu_model(), threads=mt,
+    del host, slabs
+    # one whole step, every layer in one oracle call, when the cache (and the
+    # oracle's output of the same size) fits comfortably in host memory
+    whole = None
+    cache_bytes = w.L * 2 * w.B * w.H * W_in * w.D * 2
+    if cache_bytes <= WHOLE_STEP_MAX_BYTES:
+        full = src[:, :, :, :, :W_in, :].contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+        t0 = time.perf_counter()
+        oracle.realign_kv(full, k, W_in, pad_in, v["n_acc"], v["w_new"])
+        t_full = time.perf_counter() - t0
+        del full
+        whole = t_verify + t_full + t_pm
+    value = 1.0 / whole if whole is not None else 1.0 / est
+    return dict(value=value, unit="steps/s", cores=1, kind="oracle", **cpu_fields(),
+                whole_step_s=round(whole, 4) if whole is not None else None, sampled_estimate_s=round(est, 4),
+                threads=mt,
                 sample=(f"oracle {'stochastic ' if sample is not None else ''}verify over all "
                         f"{w.B * (w.k + 1) + (w.B * w.k if sample is not None else 0)} logit rows ({t_verify * 1e3:.1f} ms), "
-                        f"KV realign of {runs} one-layer slabs cycling over layers 0..{nl - 1} "
-                        f"({per_layer * 1e3:.1f} ms per layer, x{w.L} layers), pos/mask and token row ({t_pm * 1e3:.2f} ms); "
-                        f"single-threaded, scaled to one whole step ({est:.2f} s)"))
+                        + (f"KV realign of the whole {cache_bytes / 1e9:.2f} GB cache in one call "
+                           f"({(whole - t_verify - t_pm) * 1e3:.1f} ms), pos/mask and token row ({t_pm * 1e3:.2f} ms): "
+                           f"one whole step single-threaded ({whole:.3f} s); the estimate from " if whole is not None
+                           else "KV realign estimated from ")
+                        + f"{runs} one-layer slabs cycling over layers 0..{nl - 1} ({per_layer * 1e3:.1f} ms per layer, "
+                        f"x{w.L} layers) gives {est:.3f} s" + ("" if whole is not None else " (value)")))
 
 
 def exspec_bytes(w, lens_b, Lb, n_acc):
@@ -277,7 +320,7 @@ def cpu_baseline_exspec(w, pool, pool_tok, lens, slots, Lb, logits, draft, budge
         runs += 1
     per_layer = t_layers / runs
     est = t_verify + per_layer * w.L
-    return dict(value=1.0 / est, unit="steps/s", cores=1, kind="oracle", cpu_model=cpu_model(),
+    return dict(value=1.0 / est, unit="steps/s", cores=1, kind="oracle", **cpu_fields(),
                 sample=(f"oracle verify over all {w.B * (k + 1)} logit rows ({t_verify * 1e3:.1f} ms), gather + "
                         f"whole-row write-back of {runs} one-layer pool slabs ({per_layer * 1e3:.1f} ms per layer, "
                         f"x{w.L} layers); single-threaded, scaled to one whole step ({est:.2f} s)"))
@@ -498,7 +541,7 @@ def cpu_baseline_verify(w, logits, draft, pad_in, W_in, budget_s, sample=None):
             break
     wall = time.perf_counter() - t0
     rows = w.B * ((2 * w.k + 1) if sample else (w.k + 1))
-    return dict(value=calls / wall, unit="calls/s", cores=1, kind="oracle", cpu_model=cpu_model(),
+    return dict(value=calls / wall, unit="calls/s", cores=1, kind="oracle", **cpu_fields(),
                 sample=f"{calls} whole oracle {'stochastic ' if sample else ''}verifications ({rows} logit rows each) "
                        f"in {wall:.2f} s")
 
@@ -627,7 +670,7 @@ def cpu_baseline_varlen(w, logits, draft, src, cu, budget_s):
         runs += 1
     per_layer = t_layers / runs
     est = t_verify + per_layer * w.L
-    return dict(value=1.0 / est, unit="steps/s", cores=1, kind="oracle", cpu_model=cpu_model(),
+    return dict(value=1.0 / est, unit="steps/s", cores=1, kind="oracle", **cpu_fields(),
                 sample=(f"oracle verify over all {w.B * (k + 1)} logit rows ({t_verify * 1e3:.1f} ms), compaction of "
                         f"{runs} one-layer slabs of the flat cache ({per_layer * 1e3:.1f} ms per layer, x{w.L} layers); "
                         f"single-threaded, scaled to one whole step ({est:.2f} s)"))

@@ -268,9 +268,14 @@ specdec_status_t specdec_realign_tokens(const int32_t* s_in, int64_t s_in_stride
                                         int32_t pad_id, uint32_t* dev_status, void* stream);
 
 /*
- * The whole step on one stream: specdec_verify_greedy, then one fused launch
- * of the cache realignment, the position ids / mask and (when s_in is not
- * NULL) the token row realignment.  Arguments as above; pm_cap must be
+ * One EqSpec step after the forwards (Algorithm 1, phases 2 and 3: batch
+ * verification, then unpad-append-repad of the cache, the token row and the
+ * attention inputs so that I1 and I2 hold for the next forward), on one
+ * stream: specdec_verify_greedy, then one fused launch of the cache
+ * realignment, the position ids / mask and (when s_in is not NULL) the token
+ * row realignment.  In place, the verification also writes into the
+ * workspace the order in which the realignment takes the rows (the longest
+ * moving rows first).  Arguments as above; pm_cap must be
  * >= W_in + k + 1.  Every output (tokens, n_acc, bonus, pad_out, w_new, the
  * workspace, pos, mask, dst, s_out, dev_status) stands apart from every
  * input (logits, draft, pad_in, src, s_in) and from the other outputs,
