@@ -14,7 +14,7 @@ import torch
 
 import oracle
 from paper_2510_22876_amd import workloads as wl
-from tests.gpu_util import PAD_ID, SENT_KV, SENT_TOK, alloc_outputs, say
+from tests.gpu_util import PAD_ID, SENT_KV, SENT_MASK, SENT_POS, SENT_TOK, alloc_outputs, say
 
 pytestmark = pytest.mark.gpu
 
@@ -151,3 +151,66 @@ def test_noalloc_rejects_beyond_its_scratch():
     assert e.value.code == sd.ERR_WORKSPACE
     torch.cuda.synchronize()
     assert int(o.w_new.cpu()[0]) == -99        # nothing ran
+
+
+@pytest.mark.parametrize("V", [5000, 32000], ids=["one_launch_verify", "two_launch_verify"])
+def test_noalloc_step_replayed_from_a_graph(V):
+    """The caller this entry point is for: the step captured once in a HIP
+    graph and replayed on new inputs (eager copies and synchronisations in
+    between), each replay equal to an eager specdec_step with a caller
+    workspace, bit for bit.  Replays of the one-launch verification rely on
+    the realignment launch clearing the completion counts for the next
+    replay."""
+    from paper_2510_22876_amd import specdec as sd
+    sd.timing_enable(False)     # kernel timers record events: none inside the capture
+    w = _workload("vicuna7b", dict(B=6, V=V, L=2, H=2, D=64, prompt=("uniform", 16, 120)))
+    n, W_in, pad_in, cap = wl.initial_geometry(w, 3)
+    src0 = wl.make_kv(w, pad_in, W_in, cap, 3, device="cuda")
+    inputs = [wl.logits_and_drafts(w, 3, t, device="cuda")[:2] for t in range(4)]
+    pad_t = torch.as_tensor(np.asarray(pad_in, np.int32), device="cuda")
+    lg = inputs[0][0].clone()
+    dr = inputs[0][1].clone()
+    src = src0.clone()
+    dst = torch.empty_like(src0)
+    o = alloc_outputs(w.B, w.k, w.V, W_in + w.k + 1)
+
+    def step():
+        sd.specdec_step_noalloc(lg, dr, pad_t, W_in, src, dst, o.tokens, o.n_acc, o.bonus, o.pad_out, o.w_new,
+                                o.pos, o.mask, o.dev_status)
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step()                  # warm-up (and the scratch's first use) outside the capture
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step()
+    torch.cuda.synchronize()
+    seen = set()
+    for t in (1, 2, 3, 1, 2):
+        say(f"noalloc graph replay V={V} inputs={t}")
+        e = alloc_outputs(w.B, w.k, w.V, W_in + w.k + 1)
+        e_dst = torch.empty_like(src0)
+        sd.specdec_step(inputs[t][0], inputs[t][1], pad_t, W_in, src0, e_dst, e.tokens, e.n_acc, e.bonus, e.pad_out,
+                        e.w_new, e.pos, e.mask, e.workspace, e.dev_status)
+        torch.cuda.synchronize()
+        lg.copy_(inputs[t][0])
+        dr.copy_(inputs[t][1])
+        for x in (o.tokens, o.n_acc, o.bonus, o.pad_out, o.w_new):
+            x.fill_(-77)
+        o.pos.fill_(SENT_POS)       # columns past w_new + k + 1 are left as they are:
+        o.mask.fill_(SENT_MASK)     # the same sentinels as the eager outputs
+        dst.view(torch.int16).fill_(0x7FC1)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        W = int(e.w_new.cpu()[0])
+        assert int(o.dev_status.cpu()[0]) == 0 and int(e.dev_status.cpu()[0]) == 0
+        for name in ("tokens", "n_acc", "bonus", "pad_out", "w_new", "pos", "mask"):
+            assert np.array_equal(getattr(o, name).cpu().numpy(), getattr(e, name).cpu().numpy()), (t, name)
+        assert np.array_equal(dst[..., :W, :].view(torch.int16).cpu().numpy(),
+                              e_dst[..., :W, :].view(torch.int16).cpu().numpy()), (t, "kv")
+        seen.add(tuple(o.n_acc.cpu().tolist()))
+    assert len(seen) > 1, "the replays should see different acceptance patterns"
