@@ -14,6 +14,7 @@ counters when the committed summary matches the current kernel source, and
 the CPU oracle timed on a bounded sample of the same step.
 
   python bench.py [--steps K] [--warmup W] [--workload NAME] [--variant oop|inplace]
+                  [--noalloc] [--graph | --bound]
   python bench.py --path exspec [--exspec-batch ragged|same]
   python bench.py --verify sample [--temperature T]
   python bench.py --path varlen        # Family B rollback of a flat cache
@@ -837,6 +838,9 @@ def main():
                          "for small batches)")
     ap.add_argument("--graph", action="store_true",
                     help="capture the step in a HIP graph once and replay it in the timed loop")
+    ap.add_argument("--bound", action="store_true",
+                    help="greedy eager steps through specdec.bind_step: the arguments checked and marshalled "
+                         "once, each step one library call with the stored arguments")
     ap.add_argument("--copy-ceiling", type=int, choices=[0, 1], default=1,
                     help="also time the runtime's device-to-device memcpy of the realign's bytes, for comparison")
     ap.add_argument("--copy-calibration", type=float, default=0.0,
@@ -900,9 +904,18 @@ def main():
     pristine_s = s_in.clone() if (token_row and variant != "oop") else None
 
     sws = sd.alloc_sample_workspace(w.B, w.k, w.V) if sample else None
+    bound = None
+    if args.bound:
+        if sample or args.graph:
+            raise SystemExit("--bound applies to eager greedy steps")
+        bound = sd.bind_step(logits, draft, pad_t, W_in, src, dst, bufs.tokens, bufs.n_acc, bufs.bonus,
+                             bufs.pad_out, bufs.w_new, bufs.pos, bufs.mask, None if args.noalloc else bufs.workspace,
+                             bufs.dev_status, s_in=s_in, s_out=s_out, pad_id=-1, noalloc=args.noalloc)
 
     def step():
-        if sample:
+        if bound is not None:
+            bound()
+        elif sample:
             sd.specdec_step_sample(logits, draft_logits, draft, pad_t, u_accept, u_sample, args.temperature, W_in,
                                    src, dst, bufs.tokens, bufs.n_acc, bufs.bonus, bufs.pad_out, bufs.w_new, bufs.pos,
                                    bufs.mask, sws, bufs.dev_status, s_in=s_in, s_out=s_out, pad_id=-1)
@@ -1054,7 +1067,7 @@ def main():
                                                  f"target + N(0,1), drafts drawn from q" if sample else ""),
             "B": w.B, "k": w.k, "V": w.V, "L": w.L, "H": w.H, "D": w.D, "W_in": W_in, "w_new": w_new,
             "variant": variant, "seed": args.seed, "token_row": token_row, "verify": args.verify,
-            "graph": bool(args.graph), "noalloc": bool(args.noalloc),
+            "graph": bool(args.graph), "noalloc": bool(args.noalloc), "bound": bool(args.bound),
             **({"temperature": args.temperature, "draft_noise": 1.0} if sample else {}),
             "step_GBps": round(step_gbs, 1),
             "step_bytes": realign_bytes + by["verify"],

@@ -289,13 +289,13 @@ def specdec_realign_tokens(s_in, s_out, tokens, pad_in, n_acc, w_new, W_in: int,
                                       _stream(stream)))
 
 
-def specdec_step(logits, draft, pad_in, W_in: int, src, dst, tokens, n_acc, bonus, pad_out, w_new,
-                 pos, mask, workspace, dev_status=None, sync_w_new: bool = False, stream=None,
-                 s_in=None, s_out=None, pad_id: int = 0):
-    """The fused step (with the token row S when ``s_in`` / ``s_out`` are
-    given); returns L' as a Python int when ``sync_w_new``."""
+def _greedy_step(noalloc, logits, draft, pad_in, W_in, src, dst, tokens, n_acc, bonus, pad_out, w_new, pos, mask,
+                 workspace, dev_status, sync_w_new, stream, s_in, s_out, pad_id):
+    """Checks and marshals the arguments of specdec_step (or, with
+    ``noalloc``, specdec_step_noalloc): (function, arguments, host word)."""
     B, kp1, V = logits.shape
-    _check_verify(logits, draft, pad_in, tokens, n_acc, bonus, pad_out, w_new, workspace, dev_status)
+    _check_verify(logits, draft, pad_in, tokens, n_acc, bonus, pad_out, w_new, None if noalloc else workspace,
+                  dev_status)
     s = kv_desc(src)
     d = kv_desc(dst)
     if s.B != B:
@@ -308,13 +308,23 @@ def specdec_step(logits, draft, pad_in, W_in: int, src, dst, tokens, n_acc, bonu
         _req("s_in", s_in, (B, s_in.shape[1]), torch.int32)
         _req("s_out", s_out, (B, s_out.shape[1]), torch.int32)
     host = ctypes.c_int32(-1)
-    _check(lib.specdec_step(
-        _p(logits), DTYPE_OF[logits.dtype], _p(draft), _p(pad_in), B, kp1 - 1, V, W_in,
-        ctypes.byref(s), ctypes.byref(d), _p(tokens), _p(n_acc), _p(bonus), _p(pad_out), _p(w_new),
-        _p(pos), _p(mask), pos.shape[1], _p(s_in), s_in.shape[1] if s_in is not None else 0, _p(s_out),
-        s_out.shape[1] if s_out is not None else 0, pad_id,
-        _p(workspace), workspace.numel() * workspace.element_size(),
-        _p(dev_status), ctypes.byref(host) if sync_w_new else None, _stream(stream)))
+    head = (_p(logits), DTYPE_OF[logits.dtype], _p(draft), _p(pad_in), B, kp1 - 1, V, W_in,
+            ctypes.byref(s), ctypes.byref(d), _p(tokens), _p(n_acc), _p(bonus), _p(pad_out), _p(w_new),
+            _p(pos), _p(mask), pos.shape[1], _p(s_in), s_in.shape[1] if s_in is not None else 0, _p(s_out),
+            s_out.shape[1] if s_out is not None else 0, pad_id)
+    ws = () if noalloc else (_p(workspace), workspace.numel() * workspace.element_size())
+    tail = (_p(dev_status), ctypes.byref(host) if sync_w_new else None, _stream(stream))
+    return (lib.specdec_step_noalloc if noalloc else lib.specdec_step), head + ws + tail, host
+
+
+def specdec_step(logits, draft, pad_in, W_in: int, src, dst, tokens, n_acc, bonus, pad_out, w_new,
+                 pos, mask, workspace, dev_status=None, sync_w_new: bool = False, stream=None,
+                 s_in=None, s_out=None, pad_id: int = 0):
+    """The fused step (with the token row S when ``s_in`` / ``s_out`` are
+    given); returns L' as a Python int when ``sync_w_new``."""
+    fn, args, host = _greedy_step(False, logits, draft, pad_in, W_in, src, dst, tokens, n_acc, bonus, pad_out, w_new,
+                                  pos, mask, workspace, dev_status, sync_w_new, stream, s_in, s_out, pad_id)
+    _check(fn(*args))
     return host.value if sync_w_new else None
 
 
@@ -323,27 +333,47 @@ def specdec_step_noalloc(logits, draft, pad_in, W_in: int, src, dst, tokens, n_a
                          s_in=None, s_out=None, pad_id: int = 0):
     """``specdec_step`` on the library's own scratch (no workspace argument);
     returns L' as a Python int when ``sync_w_new``."""
-    B, kp1, V = logits.shape
-    _check_verify(logits, draft, pad_in, tokens, n_acc, bonus, pad_out, w_new, None, dev_status)
-    s = kv_desc(src)
-    d = kv_desc(dst)
-    if s.B != B:
-        raise ValueError("cache rows differ from logit rows")
-    _req("pos", pos, (B, pos.shape[1]), torch.int64)
-    _req("mask", mask, (B, pos.shape[1]), torch.uint8)
-    if (s_in is None) != (s_out is None):
-        raise ValueError("give both s_in and s_out, or neither")
-    if s_in is not None:
-        _req("s_in", s_in, (B, s_in.shape[1]), torch.int32)
-        _req("s_out", s_out, (B, s_out.shape[1]), torch.int32)
-    host = ctypes.c_int32(-1)
-    _check(lib.specdec_step_noalloc(
-        _p(logits), DTYPE_OF[logits.dtype], _p(draft), _p(pad_in), B, kp1 - 1, V, W_in,
-        ctypes.byref(s), ctypes.byref(d), _p(tokens), _p(n_acc), _p(bonus), _p(pad_out), _p(w_new),
-        _p(pos), _p(mask), pos.shape[1], _p(s_in), s_in.shape[1] if s_in is not None else 0, _p(s_out),
-        s_out.shape[1] if s_out is not None else 0, pad_id,
-        _p(dev_status), ctypes.byref(host) if sync_w_new else None, _stream(stream)))
+    fn, args, host = _greedy_step(True, logits, draft, pad_in, W_in, src, dst, tokens, n_acc, bonus, pad_out, w_new,
+                                  pos, mask, None, dev_status, sync_w_new, stream, s_in, s_out, pad_id)
+    _check(fn(*args))
     return host.value if sync_w_new else None
+
+
+class Bound:
+    """One library call whose arguments were checked and converted once.
+
+    Each call passes the stored arguments again: the same device buffers (the
+    tensors are kept alive here), sizes and stream.  For loops that reuse one
+    set of buffers every step, where checking and converting some thirty
+    arguments per call costs more host time than the step's kernels take at
+    small batches.  New inputs go into the bound tensors in place (``copy_``);
+    a tensor that is reallocated or resized needs a new binding."""
+    __slots__ = ("_fn", "_args", "_keep")
+
+    def __init__(self, fn, args, keep):
+        byref = type(ctypes.byref(ctypes.c_int32()))
+        self._args = tuple(a if a is None or isinstance(a, byref) else typ(a) for typ, a in zip(fn.argtypes, args))
+        self._fn, self._keep = fn, keep
+
+    def __call__(self) -> None:
+        code = self._fn(*self._args)
+        if code != OK:
+            raise SpecdecError(code, lib.specdec_last_error().decode())
+
+
+def bind_step(logits, draft, pad_in, W_in: int, src, dst, tokens, n_acc, bonus, pad_out, w_new, pos, mask,
+              workspace=None, dev_status=None, stream=None, s_in=None, s_out=None, pad_id: int = 0,
+              noalloc: bool = False) -> Bound:
+    """``specdec_step`` (``specdec_step_noalloc`` with ``noalloc``, which takes
+    no workspace) checked and marshalled once; call the result to run a step.
+    The stream is the one given, else the current stream at binding time."""
+    if noalloc and workspace is not None:
+        raise ValueError("specdec_step_noalloc takes no workspace")
+    fn, args, _ = _greedy_step(noalloc, logits, draft, pad_in, W_in, src, dst, tokens, n_acc, bonus, pad_out, w_new,
+                               pos, mask, workspace, dev_status, False, stream, s_in, s_out, pad_id)
+    keep = (logits, draft, pad_in, src, dst, tokens, n_acc, bonus, pad_out, w_new, pos, mask, workspace, dev_status,
+            s_in, s_out)
+    return Bound(fn, args, keep)
 
 
 def specdec_gather_batch(pool, pool_tok, lens, slots, Lb: int, batch, pads, batch_tok=None, pos=None, mask=None,

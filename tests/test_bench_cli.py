@@ -24,7 +24,7 @@ def test_more_than_one_gpu_is_refused():
 def test_help_lists_the_paths():
     r = _run("--help")
     assert r.returncode == 0
-    for word in ("exspec", "varlen", "chained", "verify", "--verify", "--graph", "--variant"):
+    for word in ("exspec", "varlen", "chained", "verify", "--verify", "--graph", "--bound", "--noalloc", "--variant"):
         assert word in r.stdout, word
 
 

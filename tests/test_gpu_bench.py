@@ -23,6 +23,8 @@ PATHS = [
     ["--variant", "inplace"],
     ["--verify", "sample"],
     ["--graph"],
+    ["--bound"],
+    ["--bound", "--noalloc", "--variant", "inplace"],
     ["--path", "chained"],
     ["--path", "exspec"],
     ["--path", "exspec", "--exspec-batch", "same"],

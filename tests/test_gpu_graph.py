@@ -8,6 +8,8 @@ copied into the captured input buffers, with eager work (copies, output
 fills) and synchronisations between the replays, and must equal an eager call
 on the same inputs bit for bit: tokens, counts, bonus, paddings, width,
 positions, mask, token row and every cache byte up to the new width.
+The step bound once (``specdec.bind_step``) and called on new contents of the
+same buffers is held to the same bar.
 """
 import numpy as np
 import pytest
@@ -126,3 +128,34 @@ def test_step_replayed_from_a_graph(sd, variant, sample):
             assert np.array_equal(np.asarray(got[name]), np.asarray(want[name])), f"inputs {t}: {name} differs"
         accepted.add(tuple(got["n_acc"].tolist()))
     assert len(accepted) > 1, "the replays should see different acceptance patterns"
+
+
+@pytest.mark.parametrize("noalloc", [False, True], ids=["workspace", "noalloc"])
+@pytest.mark.parametrize("variant", ["oop", "inplace"])
+def test_bound_step_equals_the_plain_call(sd, variant, noalloc):
+    """specdec.bind_step: the step checked and marshalled once, then called on
+    new contents of the same buffers, equals the plain call bit for bit."""
+    n, W_in, pad_in, cap = wl.initial_geometry(W, 0)
+    src0 = wl.make_kv(W, pad_in, W_in, cap, 0, device="cuda")
+    s0 = wl.make_token_rows(W, pad_in, W_in, W_in + 2, 0, PAD_ID, device="cuda")
+    inputs = [_inputs(t, False) for t in range(4)]
+    eager = _Step(sd, variant, False, src0, pad_in, W_in, inputs[0])
+    bound = _Step(sd, variant, False, src0, pad_in, W_in, inputs[0])
+    b, i = bound.bufs, bound.inp
+    call = sd.bind_step(i["logits"], i["draft"], bound.pad, W_in, bound.src, bound.dst, b.tokens, b.n_acc, b.bonus,
+                        b.pad_out, b.w_new, b.pos, b.mask, None if noalloc else b.workspace, b.dev_status,
+                        s_in=bound.s_in, s_out=bound.s_out, pad_id=PAD_ID, noalloc=noalloc)
+    accepted = set()
+    for t in (1, 2, 3, 1):
+        say(f"bound step variant={variant} noalloc={noalloc} inputs={t}")
+        eager.load(inputs[t], src0, s0)
+        eager()
+        bound.load(inputs[t], src0, s0)
+        call()
+        torch.cuda.synchronize()
+        want, got = eager.result(), bound.result()
+        assert want["status"] == 0 and got["status"] == 0
+        for name in want:
+            assert np.array_equal(np.asarray(got[name]), np.asarray(want[name])), f"inputs {t}: {name} differs"
+        accepted.add(tuple(got["n_acc"].tolist()))
+    assert len(accepted) > 1
