@@ -175,6 +175,37 @@ def test_step_rejects(sd):
     assert step(pos=NA - 8) == 1                 # pos over n_acc
 
 
+def test_bound_call_passes_its_stored_arguments(sd):
+    """specdec.Bound converts each argument once to the type the function
+    declares and passes the stored values on every call: a step that fails
+    validation (pm_cap below W_in + k + 1) fails the same way on each call."""
+    _no_gpu()
+    src, dst = _kv(sd), _kv(sd, data=A + (1 << 30))
+    args = (LG, 1, DR, PI, 2, 3, 100, 10, ctypes.byref(src), ctypes.byref(dst), TK, NA, BO, PO, WN, POS, MSK, 13,
+            None, 0, None, 0, -1, WS, sd.workspace_bytes(2, 3, 100), None, None, None)
+    call = sd.Bound(sd.lib.specdec_step, args, (src, dst))
+    for _ in range(2):
+        with pytest.raises(sd.SpecdecError) as e:
+            call()
+        assert e.value.code == 1 and "pm_cap=13 < W_in+k+1=14" in str(e.value)
+
+
+def test_bind_step_checks_its_arguments_once(sd):
+    """bind_step runs the wrapper's checks when it binds: host tensors and a
+    workspace handed to the no-allocation step are refused there."""
+    import torch
+    B, k, V, W_in = 2, 3, 100, 10
+    lg = torch.zeros(B, k + 1, V)
+    i32 = lambda *shape: torch.zeros(*shape, dtype=torch.int32)   # noqa: E731
+    kv = torch.zeros(1, 2, B, 1, 16, 8, dtype=torch.bfloat16)
+    args = (lg, i32(B, k), i32(B), W_in, kv, kv, i32(B, k + 1), i32(B), i32(B), i32(B), i32(1),
+            torch.zeros(B, 16, dtype=torch.int64), torch.zeros(B, 16, dtype=torch.uint8))
+    with pytest.raises(ValueError, match="contiguous device tensor"):
+        sd.bind_step(*args, torch.zeros(64, dtype=torch.int64))
+    with pytest.raises(ValueError, match="takes no workspace"):
+        sd.bind_step(*args, torch.zeros(64, dtype=torch.int64), noalloc=True)
+
+
 def test_step_noalloc_rejects_beyond_its_scratch(sd):
     """specdec_step_noalloc refuses, before any HIP call, a step whose
     verification needs more than the library's scratch, and names the limit."""
