@@ -12,7 +12,7 @@ something other than itself:
 * I1 and the tight-width characterisation of Eq. (1), exhaustively on tiny
   batches; Corollary B.3 (one sequence) and Corollary B.4 (uniform
   acceptance);
-* a replay of every row alone at batch size 1 (the north-star brute force);
+* a replay of every row alone at batch size 1 through the same accept rule;
 * tagged KV (the cache clause of I2, Theorem B.1, over 16 chained steps);
 * the closed form and structure of I2's position ids;
 * a worked example derived by hand under ``tests/golden/``.
