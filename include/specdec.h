@@ -302,8 +302,10 @@ specdec_status_t specdec_step(const void* logits, int32_t dtype, const int32_t* 
  * The step's scratch is a library-owned device array of
  * SPECDEC_NOALLOC_SCRATCH_BYTES, one copy per device, held until the process
  * ends; its address is looked up once per device (on the first call with
- * that device current, which also enqueues one kernel that clears the
- * array's completion counts) and nothing is allocated or freed, ever.
+ * that device current) and nothing is allocated or freed, ever.  The
+ * device's first step that passes every argument check also enqueues, ahead
+ * of its own kernels, one kernel that clears the array's completion counts;
+ * a call that fails a check enqueues nothing.
  *
  * Batches of at most 4096 logit rows (B*(k+1)) of at most 16 KB each
  * (V*4 bytes for f32, V*2 for bf16 / f16) verify in ONE launch: a workgroup

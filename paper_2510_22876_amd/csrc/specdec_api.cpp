@@ -708,7 +708,8 @@ specdec_status_t step_greedy(const void* logits, int32_t dtype, const int32_t* d
                              int64_t* pos, uint8_t* mask, int64_t pm_cap, const int32_t* s_in, int64_t s_in_stride,
                              int32_t* s_out, int64_t s_out_stride, int32_t pad_id, void* workspace,
                              size_t workspace_bytes, uint32_t* dev_status, int32_t* w_new_host, void* stream,
-                             uint32_t* fused_counts) {
+                             uint32_t* fused_counts, specdec_status_t (*before_launch)(void*) = nullptr,
+                             void* before_launch_ctx = nullptr) {
   specdec_status_t s = check_verify_args(logits, dtype, draft, pad_in, B, k, V, W_in, tokens, n_acc, bonus,
                                          pad_out, w_new, workspace, workspace_bytes, dev_status);
   if (s) return s;
@@ -724,6 +725,11 @@ specdec_status_t step_greedy(const void* logits, int32_t dtype, const int32_t* d
     if (s) return s;
   }
   if (B == 0) return ok();
+  // every check has passed: only now may anything be enqueued
+  if (before_launch) {
+    s = before_launch(before_launch_ctx);
+    if (s) return s;
+  }
   hipStream_t st = static_cast<hipStream_t>(stream);
   specdec::VerifyLaunch vp{logits, dtype, draft, pad_in, B, k, V, W_in, tokens, n_acc,
                            bonus, pad_out, w_new, workspace, dev_status};
@@ -765,8 +771,9 @@ specdec_status_t specdec_step(const void* logits, int32_t dtype, const int32_t* 
 // that device current, by hipGetSymbolAddress, and only that address is ever
 // handed to a kernel.  Layout: the partial maxima of the two-launch
 // verification from the start, and, in the last kCountsBytes, the completion
-// counts of the one-launch verification, zeroed when the address is first
-// taken and zeroed again by every step's realignment launch.
+// counts of the one-launch verification, zeroed by a kernel before the
+// device's first step that passes its argument checks and zeroed again by
+// every step's realignment launch.
 static __device__ __align__(256) unsigned char scratch[SPECDEC_NOALLOC_SCRATCH_BYTES];
 
 namespace {
@@ -777,10 +784,17 @@ constexpr size_t kPartialBytes = SPECDEC_NOALLOC_SCRATCH_BYTES - kCountsBytes;
 constexpr int kMaxScratchDevices = 256;
 std::mutex g_scratch_mu;
 void* g_scratch_addr[kMaxScratchDevices] = {};
+bool g_scratch_counts_clear[kMaxScratchDevices] = {};
 
-// Device address of the current device's scratch; the stream, when given,
-// must belong to that device.
-specdec_status_t device_scratch(hipStream_t stream, void** out) {
+struct ScratchUse {
+  int dev;
+  void* addr;
+  hipStream_t stream;
+};
+
+// Device address of the current device's scratch (a query: nothing is
+// enqueued); the stream, when given, must belong to that device.
+specdec_status_t scratch_address(hipStream_t stream, ScratchUse* u) {
   int dev = -1;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
@@ -799,13 +813,23 @@ specdec_status_t device_scratch(hipStream_t stream, void** out) {
     e = hipGetSymbolAddress(&addr, HIP_SYMBOL(scratch));
     if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
     if (!addr) return fail(SPECDEC_ERR_HIP, "hipGetSymbolAddress(scratch) returned NULL");
-    // the one-launch verification's counts start at zero (a kernel, not a
-    // memset, so that a first call under graph capture records no memset node)
-    e = specdec::launch_zero(static_cast<char*>(addr) + kPartialBytes, kCountsBytes, stream);
-    if (e != hipSuccess) return hip_fail(e, "scratch count clear");
     g_scratch_addr[dev] = addr;
   }
-  *out = g_scratch_addr[dev];
+  *u = ScratchUse{dev, g_scratch_addr[dev], stream};
+  return SPECDEC_OK;
+}
+
+// Run by the step once its arguments have passed every check: on the
+// device's first such step, clears the one-launch verification's counts on
+// the step's stream, ahead of its kernels (a kernel, not a memset, so that a
+// first call under graph capture records no memset node).
+specdec_status_t scratch_first_use(void* ctx) {
+  const ScratchUse* u = static_cast<const ScratchUse*>(ctx);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_counts_clear[u->dev]) return SPECDEC_OK;
+  const hipError_t e = specdec::launch_zero(static_cast<char*>(u->addr) + kPartialBytes, kCountsBytes, u->stream);
+  if (e != hipSuccess) return hip_fail(e, "scratch count clear");
+  g_scratch_counts_clear[u->dev] = true;
   return SPECDEC_OK;
 }
 
@@ -820,6 +844,7 @@ specdec_status_t specdec_step_noalloc(const void* logits, int32_t dtype, const i
   void* ws = nullptr;
   size_t ws_bytes = 0;
   uint32_t* counts = nullptr;
+  ScratchUse use{};
   if (B > 0) {
     const bool fused = specdec::verify_fused_fits(B, k, V, dtype);
     const size_t need = specdec_workspace_bytes(B, k, V);
@@ -828,14 +853,15 @@ specdec_status_t specdec_step_noalloc(const void* logits, int32_t dtype, const i
                   "specdec_step_noalloc: verification of B=%d, k=%d, V=%d needs %zu bytes of scratch, more than the "
                   "library's %zu of %d (use specdec_step with a workspace)",
                   B, k, V, need, kPartialBytes, SPECDEC_NOALLOC_SCRATCH_BYTES);
-    const specdec_status_t s = device_scratch(static_cast<hipStream_t>(stream), &ws);
+    const specdec_status_t s = scratch_address(static_cast<hipStream_t>(stream), &use);
     if (s) return s;
+    ws = use.addr;
     ws_bytes = kPartialBytes;
     if (fused) counts = reinterpret_cast<uint32_t*>(static_cast<char*>(ws) + kPartialBytes);
   }
   return step_greedy(logits, dtype, draft, pad_in, B, k, V, W_in, src, dst, tokens, n_acc, bonus, pad_out, w_new, pos,
                      mask, pm_cap, s_in, s_in_stride, s_out, s_out_stride, pad_id, ws, ws_bytes, dev_status,
-                     w_new_host, stream, counts);
+                     w_new_host, stream, counts, B > 0 ? scratch_first_use : nullptr, &use);
 }
 
 specdec_status_t specdec_step_sample(const void* logits, const void* draft_logits, int32_t dtype,
