@@ -575,6 +575,7 @@ specdec_status_t specdec_varlen_rollback(const specdec_varlen_t* src, const spec
  * 7 = the vocabulary scan of greedy verification alone, the first of its two
  * launches, 8 = the row statistics of stochastic verification alone, the
  * first of its four launches) and returns the totals since the last reset.
+ * Launches recorded into a graph capture are not timed.
  */
 #define SPECDEC_KERNEL_VERIFY 0
 #define SPECDEC_KERNEL_REALIGN 1

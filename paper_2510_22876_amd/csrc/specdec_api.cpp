@@ -101,17 +101,34 @@ hipEvent_t take_event(Timers& t) {
   return e;
 }
 
-// Runs `launch` on `stream`, bracketed by timer events when timing is on.
+// True when work enqueued on `stream` now would be recorded into a graph
+// being captured (or when that cannot be told): such a launch is not timed,
+// since its events would never be recorded by themselves.  A failed query's
+// error is cleared so that the launch that follows does not report it.
+bool capturing(hipStream_t stream) {
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  if (hipStreamIsCapturing(stream, &cs) != hipSuccess) {
+    (void)hipGetLastError();
+    return true;
+  }
+  return cs != hipStreamCaptureStatusNone;
+}
+
+// Runs `launch` on `stream`, bracketed by timer events when timing is on and
+// the stream is not being captured.
 template <typename F>
 hipError_t timed(int kernel, hipStream_t stream, F&& launch) {
   Timers& t = timers();
   hipEvent_t b = nullptr, e = nullptr;
+  bool want = false;
   {
     std::lock_guard<std::mutex> lk(t.mu);
-    if (t.mask & (1 << kernel)) {
-      b = take_event(t);
-      e = take_event(t);
-    }
+    want = (t.mask & (1 << kernel)) != 0;
+  }
+  if (want && !capturing(stream)) {
+    std::lock_guard<std::mutex> lk(t.mu);
+    b = take_event(t);
+    e = take_event(t);
   }
   // events that end up unused go back to the pool
   auto give_back = [&] {

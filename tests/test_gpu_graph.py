@@ -159,3 +159,38 @@ def test_bound_step_equals_the_plain_call(sd, variant, noalloc):
             assert np.array_equal(np.asarray(got[name]), np.asarray(want[name])), f"inputs {t}: {name} differs"
         accepted.add(tuple(got["n_acc"].tolist()))
     assert len(accepted) > 1
+
+
+def test_timers_skip_launches_recorded_into_a_graph(sd):
+    """With the kernel timers on, a step captured into a graph records no
+    timer events; its replays are not counted, the eager steps after them
+    are, and the timers keep working."""
+    n, W_in, pad_in, cap = wl.initial_geometry(W, 0)
+    src0 = wl.make_kv(W, pad_in, W_in, cap, 0, device="cuda")
+    s0 = wl.make_token_rows(W, pad_in, W_in, W_in + 2, 0, PAD_ID, device="cuda")
+    step = _Step(sd, "oop", False, src0, pad_in, W_in, _inputs(0, False))
+    step.load(_inputs(0, False), src0, s0)
+    sd.timing_reset()
+    sd.timing_enable(sd.TIMING_ALL)
+    try:
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            step()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            step()
+        for _ in range(3):
+            g.replay()
+        step()
+        step()
+        torch.cuda.synchronize()
+        say("timers after a captured step")
+        for kernel in (sd.KERNEL_VERIFY, sd.KERNEL_REALIGN):
+            ms, n_launch = sd.timing_query(kernel)
+            assert n_launch == 3 and ms > 0, (kernel, n_launch, ms)   # the warm-up and the two eager steps
+    finally:
+        sd.timing_enable(False)
+        sd.timing_reset()
