@@ -604,8 +604,8 @@ __global__ __launch_bounds__(kPickThreads) void sample_pick_kernel(SampleArgs a)
   __syncthreads();
   int32_t x_out = s_pick;
   if (x_out < 0 || x_out >= a.V) x_out = s_fallback;
-  if (threadIdx.x <= k) {
-    const int r = threadIdx.x;
+  if (static_cast<int>(threadIdx.x) <= k) {
+    const int r = static_cast<int>(threadIdx.x);
     a.tokens[static_cast<int64_t>(i) * (k + 1) + r] =
         r < j ? a.draft[static_cast<int64_t>(i) * k + r] : (r == j ? x_out : -1);
   }
