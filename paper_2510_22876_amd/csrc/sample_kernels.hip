@@ -304,6 +304,7 @@ constexpr int kMassThreads = 256;               // kMassThreads * kGroup == kTil
 constexpr int kPickThreads = 256;
 static_assert(kMassThreads * kGroup == kTile && kPickThreads * kGroup == kTile, "a tile is one group per thread");
 constexpr int kMaxTiles = 64;                   // tiles per chunk (V <= 64 * 64 * kTile)
+constexpr int64_t kMassTarget = 2048;           // mass workgroups the chunking aims for
 
 // One workgroup per sequence: the normalisers of its 2k+1 rows (one wave per
 // row), the acceptance tests (wave 0), then n_acc and the normalisers of the
@@ -625,10 +626,15 @@ int64_t sample_chunks(int64_t rows, int64_t V) {
   return (V + c - 1) / c;
 }
 
-int64_t sample_mass_chunk_elems(int64_t V) {
+int64_t sample_mass_chunk_elems(int64_t B, int64_t V) {
   // at most 64 chunks per row (one lane each in the pick kernel), at least
-  // one tile each
+  // one tile each, and about kMassTarget workgroups in all: 8 of 256 threads
+  // per CU, so the whole grid is resident at once (at B = 64, V = 151936,
+  // 64 chunks per row took two rounds of workgroups: 13.4 us against 11.5)
   int64_t c = (V + 63) / 64;
+  int64_t t = (B * V + kMassTarget - 1) / kMassTarget;
+  if (t > kMaxTiles * kTile) t = kMaxTiles * kTile;   // at most kMaxTiles tiles a chunk
+  if (t > c) c = t;
   c = ((c + kGroup - 1) / kGroup) * kGroup;
   if (c < kTile) c = kTile;
   if (c > V) c = V;
@@ -656,7 +662,7 @@ static hipError_t sample_args(const SampleLaunch& p, SampleArgs& a) {
   const int64_t rows = static_cast<int64_t>(p.B) * (2 * p.k + 1);
   a.chunk_elems = sample_chunk_elems(rows, p.V);
   a.chunks = static_cast<int32_t>((p.V + a.chunk_elems - 1) / a.chunk_elems);
-  a.mchunk_elems = sample_mass_chunk_elems(p.V);
+  a.mchunk_elems = sample_mass_chunk_elems(p.B, p.V);
   a.mchunks = static_cast<int32_t>((p.V + a.mchunk_elems - 1) / a.mchunk_elems);
   a.tiles = static_cast<int32_t>((a.mchunk_elems + kTile - 1) / kTile);
   if (a.tiles > kMaxTiles || a.mchunks > 64) return hipErrorInvalidValue;

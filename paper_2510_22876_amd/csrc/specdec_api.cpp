@@ -595,7 +595,7 @@ size_t specdec_sample_workspace_bytes(int32_t B, int32_t k, int32_t V) {
   // chunk statistics of every row, then per (sequence, chunk) the two last
   // indices and per (sequence, chunk, tile of 2048 logits) the two masses
   const int64_t chunks = specdec::sample_chunks(rows, V);
-  const int64_t mc = specdec::sample_mass_chunk_elems(V);
+  const int64_t mc = specdec::sample_mass_chunk_elems(B, V);
   const int64_t mchunks = (V + mc - 1) / mc;
   const int64_t tiles = (mc + 2047) / 2048;
   return specdec::kWsHeaderBytes + static_cast<size_t>(B) * 16u +

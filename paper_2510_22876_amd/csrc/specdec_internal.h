@@ -154,7 +154,7 @@ struct SampleLaunch {
 // Chunking of the stochastic verification's row statistics.
 int64_t sample_chunk_elems(int64_t rows, int64_t V);
 int64_t sample_chunks(int64_t rows, int64_t V);
-int64_t sample_mass_chunk_elems(int64_t V);
+int64_t sample_mass_chunk_elems(int64_t B, int64_t V);
 hipError_t launch_verify_sample(const SampleLaunch& p, hipStream_t stream);
 // The launches of launch_verify_sample: the row statistics over every target
 // and draft logit, then the accept tests, masses and draws.
